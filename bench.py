@@ -1,0 +1,199 @@
+"""Benchmark: one GPU's share of a Mixtral-8x7B-shaped MoE layer on MI355X.
+
+A step is one pass of the whole share (gate scores + top-k, histograms,
+packaging, grouped SwiGLU FFN, weighted combine) over one batch of synthetic
+tokens already resident in HBM.  The headline is the prefill batch (T=4096);
+the decode batch (T=64) is reported beside it.  Prints ONE JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME:REGIME]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+from paper_2607_08782_amd import moe, synth  # noqa: E402
+from paper_2607_08782_amd.layer import LayerShare  # noqa: E402
+
+METRIC = "MoE-layer tokens/s on 1 GPU; grouped-GEMM % bf16 MFMA peak; decode HBM GB/s"
+PEAK_BF16_FLOPS = 2.5e15        # MI355X dense bf16 MFMA
+PEAK_HBM_BYTES = 8.0e12         # MI355X HBM3E
+PHASES = ("route_topk", "histogram", "permute", "grouped_ffn", "shared_ffn", "combine")
+
+
+def make_share(cfg, T, seed=0, weights=None):
+    inp = synth.make_layer(cfg, T, seed=seed, device="cuda", experts="none" if weights else "local")
+    w13, w2, shared = weights if weights else (inp.w13, inp.w2, inp.shared)
+    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, w13, w2, shared=shared,
+                       coact=cfg.coact)
+    return inp, share, (w13, w2, shared)
+
+
+def run_phases(share, ev):
+    """The five C-ABI calls of LayerShare.run, with an event after each."""
+    ev[0].record()
+    share.route()
+    ev[1].record()
+    moe.moe_expert_histogram(share.topk_idx, share.E, counts=share.counts, coact=share.coact)
+    ev[2].record()
+    moe.moe_permute(share.X, share.topk_idx, share.topk_gate, share.counts, share.placement,
+                    share.dev, E=share.E, cap_rows=share.cap_rows, out=share.perm, ws=share.ws_perm)
+    ev[3].record()
+    if share.weights is not None:
+        moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
+                            cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
+    ev[4].record()
+    if share.shared_weights is not None:
+        moe.moe_grouped_ffn(share.X, share.shared_offsets, share.shared_weights, cap_rows=share.T,
+                            y_perm=share.y_shared, ws=share.ws_shared)
+    ev[5].record()
+    moe.moe_combine(share.y_perm, share.perm["token_row"], share.topk_gate, share.y_shared,
+                    T=share.T, d=share.d, y=share.y)
+    ev[6].record()
+
+
+def time_share(share, steps, warmup):
+    for _ in range(warmup):
+        share.run()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        run_phases(share, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_phase = np.zeros(len(PHASES))
+    total = 0.0
+    for ev in evs:
+        for j in range(len(PHASES)):
+            per_phase[j] += ev[j].elapsed_time(ev[j + 1])
+    total = evs[0][0].elapsed_time(evs[-1][6])
+    per_phase /= steps
+    return total / steps, dict(zip(PHASES, per_phase)), wall
+
+
+def ffn_work(share, cfg):
+    go = share.perm["group_offsets"].cpu().numpy()
+    sizes = np.diff(go)
+    N = int(go[-1])
+    active = int((sizes > 0).sum())
+    flops = 6.0 * cfg.d * cfg.f * N
+    bytes_ = active * 3.0 * cfg.d * cfg.f * 2 + 2.0 * N * cfg.d * 2
+    return N, active, flops, bytes_, sizes.tolist()
+
+
+def cpu_baseline(cfg, inp_gpu, w13, w2, shared, T_full):
+    """The oracle, as it stands, on a bounded sample of the same batch."""
+    import oracle
+
+    f32 = lambda t: t.detach().float().cpu().numpy()
+    X = f32(inp_gpu.X)
+    Wr, b = f32(inp_gpu.Wr), f32(inp_gpu.bias)
+    W13 = [f32(w) for w in w13]
+    W2 = [f32(w) for w in w2]
+    SH = [(f32(a), f32(c)) for a, c in shared]
+
+    def run(S):
+        t0 = time.perf_counter()
+        oracle.layer_share(X[:S], Wr, b, cfg.k, inp_gpu.placement, 0, W13, W2, shared=SH,
+                           with_coact=cfg.coact)
+        return time.perf_counter() - t0
+
+    S0 = 16
+    t0 = run(S0)
+    S = int(min(T_full, max(S0, S0 * 12.0 / max(t0, 1e-6))))
+    t = run(S)
+    return {"value": S / t, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "first %d of the %d tokens of the same batch through the whole share "
+                      "(fp64 C loops), %.1f s" % (S, T_full, t)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mixtral_8x7b:prefill")
+    ap.add_argument("--decode", default="decode", help="regime reported beside the headline ('' = none)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU's share of the layer; --gpus %d is not supported "
+              "(multi-GPU expert parallelism is design-only in this build)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    moe.load_library()
+    name, regime = args.workload.split(":")
+    cfg = synth.CONFIGS[name]
+    T = cfg.T(regime)
+
+    inp, share, weights = make_share(cfg, T)
+    ms, phases, wall = time_share(share, args.steps, args.warmup)
+    N, active, flops, fbytes, sizes = ffn_work(share, cfg)
+    t_ffn = phases["grouped_ffn"] * 1e-3
+    achieved = flops / t_ffn
+    out = {
+        "metric": METRIC,
+        "value": T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": "%s-shaped MoE layer share, %s batch T=%d: d=%d, E=%d routed experts, "
+                        "top-%d, SwiGLU f=%d, %d of %d experts on this GPU (G=%d), Zipf s=%s"
+                        % (name, regime, T, cfg.d, cfg.E, cfg.k, cfg.f, share.n_local, cfg.E,
+                           cfg.G, cfg.zipf),
+            "T": T, "d": cfg.d, "E": cfg.E, "k": cfg.k, "f": cfg.f, "G": cfg.G,
+            "local_experts": share.n_local, "rows_here": N, "group_rows": sizes, "seed": 0,
+        },
+        "roofline": {
+            "kernel": "moe_grouped_ffn (grouped_gemm_kernel<swiglu> + grouped_gemm_kernel<plain>)",
+            "bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK_BF16_FLOPS / 1e12,
+            "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_FLOPS, "traffic": None,
+            "algorithmic_flops_per_launch": flops, "avg_launch_us": t_ffn * 1e6,
+        },
+        "phases_us": {k: v * 1e3 for k, v in phases.items()},
+    }
+    if args.decode and args.decode in dict(cfg.regimes) and args.decode != regime:
+        Td = cfg.T(args.decode)
+        dinp, dshare, _ = make_share(cfg, Td, weights=weights)
+        dms, dph, _ = time_share(dshare, max(args.steps * 5, 50), args.warmup * 2)
+        dN, dact, dfl, dby, dsizes = ffn_work(dshare, cfg)
+        dt = dph["grouped_ffn"] * 1e-3
+        out["decode"] = {
+            "T": Td, "tokens_per_s": Td / (dms * 1e-3), "ms_per_step": dms, "rows_here": dN,
+            "active_experts": dact,
+            "roofline": {"kernel": "moe_grouped_ffn", "bound": "hbm",
+                         "achieved": dby / dt / 1e9, "peak": PEAK_HBM_BYTES / 1e9, "unit": "GB/s",
+                         "frac": dby / dt / PEAK_HBM_BYTES, "traffic": None,
+                         "algorithmic_bytes_per_launch": dby, "avg_launch_us": dt * 1e6},
+            "phases_us": {k: v * 1e3 for k, v in dph.items()},
+        }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, inp, *weights, T)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,199 @@
+/*
+ * moe.h -- C ABI of the MI355X (gfx950) library for one GPU's share of one
+ * expert-parallel MoE layer, the layer whose routing statistics Director
+ * (arXiv 2607.08782) turns into expert placements.
+ *
+ * The share runs five steps, one entry point each, all enqueued on the
+ * caller's HIP stream:
+ *   moe_route_topk        gate scores and top-k routing            (Sec. II-A)
+ *   moe_expert_histogram  per-expert workload counts W, co-activation
+ *                                                     (Sec. VI-A; Sec. I)
+ *   moe_permute           packaging of tokens for the experts placed on this
+ *                         GPU, with per-GPU send counts (Sec. II-B; Eq. 1, 3)
+ *   moe_grouped_ffn       the experts' FFNs over ragged groups of rows
+ *                                                              (Sec. II-A)
+ *   moe_combine           gate-weighted sum of expert outputs  (Sec. II-A)
+ *
+ * Conventions for every entry point
+ *   - Pointers named "device" point to caller-owned device memory; pointers
+ *     named "host" point to host memory that is read during the call and not
+ *     kept.  The library allocates nothing and never synchronises the
+ *     stream; outputs are valid once the stream reaches the end of the call.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   - Matrices are row-major and densely packed.  Element type codes:
+ *     MOE_F32 (float) and MOE_BF16 (bfloat16, round-to-nearest-even stored).
+ *     Gate scores, logits and gates are always float; indices int32.
+ *   - Arguments are validated before anything is enqueued.  A non-zero
+ *     status means nothing was enqueued, except MOE_ERR_DEVICE, which
+ *     reports a HIP launch error (the stream state is then unspecified).
+ *   - Entry points are stateless and reentrant; concurrent calls on
+ *     different streams must use different output and workspace buffers.
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* element types */
+#define MOE_F32  0
+#define MOE_BF16 1
+
+/* status codes */
+#define MOE_OK            0
+#define MOE_ERR_ARG       1   /* null pointer, negative size, k out of range, bad dtype/flags */
+#define MOE_ERR_PLACEMENT 2   /* an expert with no host GPU, dev >= G, or more than c_max local experts */
+#define MOE_ERR_SHAPE     3   /* unsupported d or f, cap_rows or workspace too small */
+#define MOE_ERR_DEVICE    4   /* a HIP launch failed */
+
+/* flags of moe_route_topk */
+#define MOE_RENORM    1   /* gates = softmax over the k selected logits (else: full softmax, restricted) */
+#define MOE_LOGITS_IN 2   /* skip the gate GEMM: `logits` is an input holding T*E scores */
+
+/* limits */
+#define MOE_MAX_E      256   /* experts per layer */
+#define MOE_MAX_K      16    /* experts per token */
+#define MOE_MAX_G      64    /* GPUs in the placement map */
+#define MOE_MAX_GROUPS 128   /* local expert groups per moe_grouped_ffn call */
+
+/* Human-readable name of a status code (static string). */
+const char* moe_status_string(int status);
+
+/*
+ * moe_route_topk -- gate scores and top-k routing (Sec. II-A: the gating
+ * network scores every expert for each token and the token goes to the k
+ * best; the gate is replicated on every GPU, Sec. II-B).
+ *
+ *   logits[t][e] = sum_i x[t][i] * w_router[e][i] + bias[e]     (fp32 accumulate)
+ *   topk_idx[t][r] = r-th best expert of token t: descending logit; equal
+ *                    logits (-0.0 == +0.0) go to the lower expert index
+ *   topk_gate[t][r] = exp(l_r - l_0) / sum_{r'<k} exp(l_r' - l_0)  with MOE_RENORM,
+ *                     else exp(l_r - l_0) / sum_{e<E} exp(l_e - l_0)
+ *
+ * x         device [T][d] of `dtype`        (unused with MOE_LOGITS_IN; may be NULL then)
+ * w_router  device [E][d] of `dtype`        (unused with MOE_LOGITS_IN)
+ * bias      device [E] float, nullable (= 0)
+ * logits    device [T][E] float: output, or input with MOE_LOGITS_IN; nullable
+ *           otherwise (then the scores are not stored)
+ * topk_idx  device [T][k] int32 output;  topk_gate  device [T][k] float output
+ * Requires 1 <= E <= MOE_MAX_E, 1 <= k <= min(E, MOE_MAX_K), T >= 0,
+ * d >= 1 and, for MOE_BF16, d % 8 == 0.  Logits must be finite.
+ */
+int moe_route_topk(const void* x, int dtype, const void* w_router, const float* bias,
+                   int64_t T, int d, int E, int k, int flags,
+                   float* logits, int32_t* topk_idx, float* topk_gate, void* stream);
+
+/*
+ * moe_expert_histogram -- per-expert workload counts (Sec. VI-A: W_{j,i}
+ * counts tokens routed to expert i; this share routes all T tokens, so
+ * counts[e] is the inner sum of Eq. 1) and co-activation counts (the signal
+ * for co-locating experts activated together, Sec. I).
+ *
+ *   counts[e]   = #{(t, r) : topk_idx[t][r] == e}
+ *   coact[a][b] = #{t : a and b both among topk_idx[t][0..k-1]}   (diag = counts)
+ *
+ * topk_idx  device [T][k] int32, values in [0, E), distinct within a row
+ * counts    device [E] int32 output (overwritten)
+ * coact     device [E][E] int32 output, nullable (not computed)
+ * Results are exact integers and independent of scheduling.
+ */
+int moe_expert_histogram(const int32_t* topk_idx, int64_t T, int k, int E,
+                         int32_t* counts, int32_t* coact, void* stream);
+
+/* Workspace bytes moe_permute needs for T tokens, k and E. */
+size_t moe_permute_ws_bytes(int64_t T, int k, int E);
+
+/*
+ * moe_permute -- package the tokens for the experts placed on GPU `dev`
+ * (Sec. II-B: tokens are packaged and sent to the GPUs hosting their
+ * experts; Sec. VI-A: placement x[e][j], every expert hosted at least once,
+ * Eq. 6d, at most C_max experts per GPU, Eq. 6e).
+ *
+ * placement  HOST [E][G] uint8, x[e][j] = placement[e*G + j] != 0
+ * Local slot s = the s-th expert, by ascending id, with x[e][dev] = 1;
+ * n_local = number of local slots.  An expert with n_e hosts splits its
+ * tokens (ascending token order, c_e = counts[e] of them) into contiguous
+ * blocks: its q-th host by ascending GPU id serves ranks
+ * [floor(q*c_e/n_e), floor((q+1)*c_e/n_e)).  (The paper allows replicas but
+ * leaves the split open; this is the rule the library fixes.)
+ *
+ * Outputs (rows are grouped by slot, ascending token order inside a group):
+ *   group_offsets device [n_local+1] int32: exclusive prefix sum of rows per slot;
+ *                 N = group_offsets[n_local] rows are written
+ *   x_perm        device [cap_rows][d] of `dtype`: x_perm[p] = x[row_token[p]]
+ *   row_token     device [cap_rows] int32;  row_gate  device [cap_rows] float
+ *   token_row     device [T][k] int32: row of assignment (t, r) here, or -1
+ *   send_counts   device [G] int32, nullable: rows each GPU's hosts take,
+ *                 i.e. Eq. 3's D_{dev,j} / d; equals Eq. 1's lambda_j when
+ *                 no expert is replicated
+ * counts  device [E] int32 from moe_expert_histogram on the same topk_idx.
+ * c_max   0 = unchecked, else MOE_ERR_PLACEMENT if n_local > c_max.
+ * ws      device workspace of at least moe_permute_ws_bytes(T, k, E) bytes,
+ *         256-byte aligned.
+ * Requires cap_rows >= T * min(k, n_local), G <= MOE_MAX_G, and for
+ * MOE_BF16 d % 8 == 0.  Rows past N are left untouched.
+ */
+int moe_permute(const void* x, int dtype, const int32_t* topk_idx, const float* topk_gate,
+                const int32_t* counts, int64_t T, int d, int k, int E,
+                const uint8_t* placement, int G, int dev, int c_max,
+                void* x_perm, int64_t cap_rows, int32_t* group_offsets,
+                int32_t* row_token, float* row_gate, int32_t* token_row,
+                int32_t* send_counts, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes moe_grouped_ffn needs. */
+size_t moe_grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_groups);
+
+/*
+ * moe_grouped_ffn -- every local expert's FFN on its group of rows
+ * (Sec. II-A: experts are FFN sub-networks).  Experts are SwiGLU:
+ *
+ *   for each slot s and row p in [group_offsets[s], group_offsets[s+1]):
+ *     a = W1_s x_perm[p],  b = W3_s x_perm[p]               (f values each)
+ *     h = SiLU(a) * b,     SiLU(a) = a / (1 + exp(-a))
+ *     y_perm[p] = W2_s h
+ *
+ * x_perm         device [cap_rows][d] of `dtype`
+ * group_offsets  device [n_groups+1] int32, non-decreasing, offsets[0] = 0,
+ *                offsets[n_groups] <= cap_rows (read on the device only)
+ * w13            HOST array of n_groups device pointers; w13[s] is [2f][d]:
+ *                rows 0..f-1 are W1_s (gate), rows f..2f-1 are W3_s (up)
+ * w2             HOST array of n_groups device pointers; w2[s] is [d][f]
+ * y_perm         device [cap_rows][d] of `dtype` output (rows past
+ *                offsets[n_groups] untouched)
+ * ws             device workspace, moe_grouped_ffn_ws_bytes(...) bytes,
+ *                256-byte aligned
+ * For MOE_BF16 the products accumulate in fp32 and h is rounded to bf16
+ * before the second product.  Requires 1 <= n_groups <= MOE_MAX_GROUPS and
+ * for MOE_BF16 d % 64 == 0 and f % 64 == 0.
+ * A shared (always-on) expert is the call with x_perm = x, one group and
+ * group_offsets = {0, T}.
+ */
+int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets, int n_groups,
+                    const void* const* w13, const void* const* w2, int d, int f,
+                    int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * moe_combine -- gate-weighted sum of the experts' outputs (Sec. II-A) back
+ * in token order (the return trip of Sec. II-B), plus shared experts with
+ * weight 1:
+ *
+ *   y[t] = sum_{r ascending, token_row[t][r] >= 0} topk_gate[t][r] * y_perm[token_row[t][r]]
+ *          + y_shared[t]
+ *
+ * y_perm    device [rows][d] of `dtype`;  token_row device [T][k] int32
+ * topk_gate device [T][k] float;  y_shared device [T][d] of `dtype`, nullable
+ * y         device [T][d] of `dtype` output (fp32 accumulation, then stored).
+ * Tokens with no local assignment get y_shared[t] (or 0).
+ */
+int moe_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* topk_gate,
+                const void* y_shared, int64_t T, int d, int k, void* y, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H */

@@ -1,0 +1,148 @@
+// C ABI entry points: argument validation, placement map -> slot tables,
+// then the launches of each step on the caller's stream.  Nothing here
+// allocates device memory or synchronises.
+#include <string.h>
+
+#include "common.h"
+
+namespace {
+
+using namespace moe;
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* moe_status_string(int status) {
+    switch (status) {
+        case MOE_OK: return "ok";
+        case MOE_ERR_ARG: return "invalid argument";
+        case MOE_ERR_PLACEMENT: return "invalid placement map";
+        case MOE_ERR_SHAPE: return "unsupported shape, capacity or workspace size";
+        case MOE_ERR_DEVICE: return "HIP launch error";
+        default: return "unknown status";
+    }
+}
+
+int moe_route_topk(const void* x, int dtype, const void* w_router, const float* bias, int64_t T,
+                   int d, int E, int k, int flags, float* logits, int32_t* topk_idx,
+                   float* topk_gate, void* stream) {
+    if (T < 0 || E < 1 || E > MOE_MAX_E || k < 1 || k > MOE_MAX_K || k > E) return MOE_ERR_ARG;
+    if (flags & ~(MOE_RENORM | MOE_LOGITS_IN)) return MOE_ERR_ARG;
+    if (T > (int64_t)0x7fffffff * 16) return MOE_ERR_ARG;
+    if (T > 0 && (!topk_idx || !topk_gate)) return MOE_ERR_ARG;
+    if (flags & MOE_LOGITS_IN) {
+        if (T > 0 && !logits) return MOE_ERR_ARG;
+    } else {
+        if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
+        if (d < 1) return MOE_ERR_ARG;
+        if (T > 0 && (!x || !w_router)) return MOE_ERR_ARG;
+        if (dtype == MOE_BF16) {
+            if (d % 8) return MOE_ERR_SHAPE;
+            if (!aligned16(x) || !aligned16(w_router)) return MOE_ERR_ARG;
+        }
+    }
+    return launch_route_topk(x, dtype, w_router, bias, T, d, E, k, flags, logits, topk_idx,
+                             topk_gate, (hipStream_t)stream);
+}
+
+int moe_expert_histogram(const int32_t* topk_idx, int64_t T, int k, int E, int32_t* counts,
+                         int32_t* coact, void* stream) {
+    if (T < 0 || E < 1 || E > MOE_MAX_E || k < 1 || k > MOE_MAX_K || k > E) return MOE_ERR_ARG;
+    if (!counts || (T > 0 && !topk_idx)) return MOE_ERR_ARG;
+    return launch_histogram(topk_idx, T, k, E, counts, coact, (hipStream_t)stream);
+}
+
+size_t moe_permute_ws_bytes(int64_t T, int k, int E) {
+    if (T < 0 || k < 1 || E < 1) return 0;
+    return permute_ws_bytes(T, k, E);
+}
+
+int moe_permute(const void* x, int dtype, const int32_t* topk_idx, const float* topk_gate,
+                const int32_t* counts, int64_t T, int d, int k, int E, const uint8_t* placement,
+                int G, int dev, int c_max, void* x_perm, int64_t cap_rows,
+                int32_t* group_offsets, int32_t* row_token, float* row_gate, int32_t* token_row,
+                int32_t* send_counts, void* ws, size_t ws_bytes, void* stream) {
+    if (T < 0 || d < 0 || E < 1 || E > MOE_MAX_E || k < 1 || k > MOE_MAX_K || k > E)
+        return MOE_ERR_ARG;
+    if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
+    if (T * (int64_t)k > 0x7fffffff) return MOE_ERR_ARG;
+    if (!placement || !group_offsets || !counts || cap_rows < 0) return MOE_ERR_ARG;
+    if (G < 1 || G > MOE_MAX_G || dev < 0 || dev >= G) return MOE_ERR_PLACEMENT;
+    if (T > 0 && (!topk_idx || !topk_gate || !token_row)) return MOE_ERR_ARG;
+
+    PermuteTables tab;
+    memset(&tab, 0, sizeof(tab));
+    for (int e = 0; e < MOE_MAX_E; ++e) tab.slot_of[e] = -1;
+    int n_local = 0;
+    for (int e = 0; e < E; ++e) {
+        uint64_t h = 0;
+        for (int j = 0; j < G; ++j)
+            if (placement[(int64_t)e * G + j]) h |= 1ull << j;
+        if (!h) return MOE_ERR_PLACEMENT;
+        tab.hosts[e] = h;
+        if ((h >> dev) & 1ull) {
+            if (n_local >= MOE_MAX_GROUPS) return MOE_ERR_PLACEMENT;
+            tab.slot_of[e] = (int16_t)n_local;
+            tab.expert_of_slot[n_local] = (int16_t)e;
+            ++n_local;
+        }
+    }
+    if (c_max > 0 && n_local > c_max) return MOE_ERR_PLACEMENT;
+    const int64_t need_rows = T * (int64_t)(k < n_local ? k : n_local);
+    if (cap_rows < need_rows) return MOE_ERR_SHAPE;
+    if (dtype == MOE_BF16 && d % 8) return MOE_ERR_SHAPE;
+    if (!ws || ws_bytes < permute_ws_bytes(T, k, E) || ((uintptr_t)ws & 255u)) return MOE_ERR_SHAPE;
+    if (need_rows > 0 && (!row_token || !row_gate || (d > 0 && (!x || !x_perm))))
+        return MOE_ERR_ARG;
+    return launch_permute(x, dtype, topk_idx, topk_gate, counts, T, d, k, E, tab, n_local, G, dev,
+                          x_perm, cap_rows, group_offsets, row_token, row_gate, token_row,
+                          send_counts, ws, (hipStream_t)stream);
+}
+
+size_t moe_grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_groups) {
+    if (cap_rows < 0 || d < 1 || f < 1) return 0;
+    return grouped_ffn_ws_bytes(dtype, cap_rows, d, f, n_groups);
+}
+
+int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets, int n_groups,
+                    const void* const* w13, const void* const* w2, int d, int f, int64_t cap_rows,
+                    void* y_perm, void* ws, size_t ws_bytes, void* stream) {
+    if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
+    if (n_groups < 1 || n_groups > MOE_MAX_GROUPS || d < 1 || f < 1 || cap_rows < 0)
+        return MOE_ERR_ARG;
+    if (cap_rows > 0x7fffffff) return MOE_ERR_ARG;
+    if (!group_offsets || !w13 || !w2) return MOE_ERR_ARG;
+    for (int s = 0; s < n_groups; ++s)
+        if (!w13[s] || !w2[s]) return MOE_ERR_ARG;
+    if (cap_rows > 0 && (!x_perm || !y_perm)) return MOE_ERR_ARG;
+    if (dtype == MOE_BF16) {
+        if (d % 64 || f % 64) return MOE_ERR_SHAPE;
+        if (!aligned16(x_perm) || !aligned16(y_perm)) return MOE_ERR_ARG;
+        for (int s = 0; s < n_groups; ++s)
+            if (!aligned16(w13[s]) || !aligned16(w2[s])) return MOE_ERR_ARG;
+    }
+    if (cap_rows > 0 &&
+        (!ws || ws_bytes < grouped_ffn_ws_bytes(dtype, cap_rows, d, f, n_groups) ||
+         ((uintptr_t)ws & 255u)))
+        return MOE_ERR_SHAPE;
+    return launch_grouped_ffn(x_perm, dtype, group_offsets, n_groups, w13, w2, d, f, cap_rows,
+                              y_perm, ws, (hipStream_t)stream);
+}
+
+int moe_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* topk_gate,
+                const void* y_shared, int64_t T, int d, int k, void* y, void* stream) {
+    if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
+    if (T < 0 || d < 1 || k < 1 || k > MOE_MAX_K) return MOE_ERR_ARG;
+    if (T > 0 && (!token_row || !topk_gate || !y)) return MOE_ERR_ARG;
+    const int V = dtype == MOE_BF16 ? 8 : 4;
+    if (d % V == 0 && (!aligned16(y) || (y_perm && !aligned16(y_perm)) ||
+                       (y_shared && !aligned16(y_shared))))
+        return MOE_ERR_ARG;
+    return launch_combine(y_perm, dtype, token_row, topk_gate, y_shared, T, d, k, y,
+                          (hipStream_t)stream);
+}
+
+}  // extern "C"

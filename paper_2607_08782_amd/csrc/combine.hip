@@ -1,0 +1,118 @@
+// Gate-weighted sum of the selected experts' outputs (Sec. II-A of the
+// Director paper), gathered back into token order (the return trip of
+// Sec. II-B), plus always-on shared experts with weight 1.
+//
+// Bandwidth-bound gather: each thread owns one 16-byte chunk of one token's
+// output row, reads the k expert rows it needs (skipping assignments placed
+// on other GPUs), accumulates in fp32 in ascending r, and stores once.
+#include "common.h"
+
+namespace moe {
+namespace {
+
+constexpr int COMBINE_THREADS = 256;
+
+template <typename Elem, int V>
+struct Vec;
+
+template <>
+struct Vec<bf16_t, 8> {
+    typedef uint4 type;
+    static __device__ __forceinline__ void load(const bf16_t* p, float* v) {
+        const uint4 u = *(const uint4*)p;
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[2 * i] = __uint_as_float(w[i] << 16);
+            v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+        }
+    }
+    static __device__ __forceinline__ void store(bf16_t* p, const float* v) {
+        uint4 u;
+        u.x = pack_bf16x2(v[0], v[1]);
+        u.y = pack_bf16x2(v[2], v[3]);
+        u.z = pack_bf16x2(v[4], v[5]);
+        u.w = pack_bf16x2(v[6], v[7]);
+        *(uint4*)p = u;
+    }
+};
+
+template <>
+struct Vec<float, 4> {
+    static __device__ __forceinline__ void load(const float* p, float* v) {
+        const float4 u = *(const float4*)p;
+        v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+    }
+    static __device__ __forceinline__ void store(float* p, const float* v) {
+        *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+    }
+};
+
+template <>
+struct Vec<bf16_t, 1> {
+    static __device__ __forceinline__ void load(const bf16_t* p, float* v) { v[0] = bf16_to_f32(*p); }
+    static __device__ __forceinline__ void store(bf16_t* p, const float* v) { *p = f32_to_bf16(v[0]); }
+};
+
+template <>
+struct Vec<float, 1> {
+    static __device__ __forceinline__ void load(const float* p, float* v) { v[0] = *p; }
+    static __device__ __forceinline__ void store(float* p, const float* v) { *p = v[0]; }
+};
+
+template <typename Elem, int V>
+__global__ __launch_bounds__(COMBINE_THREADS) void combine_kernel(
+    const Elem* __restrict__ y_perm, const int32_t* __restrict__ token_row,
+    const float* __restrict__ gate, const Elem* __restrict__ y_shared, int64_t T, int d, int k,
+    int chunks_per_row, Elem* __restrict__ y) {
+    const int64_t gid = (int64_t)blockIdx.x * COMBINE_THREADS + threadIdx.x;
+    const int64_t t = gid / chunks_per_row;
+    const int c = (int)(gid - t * chunks_per_row);
+    if (t >= T) return;
+    const int col = c * V;
+    float acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = 0.f;
+    for (int r = 0; r < k; ++r) {
+        const int32_t p = token_row[t * k + r];
+        if (p < 0) continue;
+        const float g = gate[t * k + r];
+        float v[V];
+        Vec<Elem, V>::load(y_perm + (int64_t)p * d + col, v);
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] = fmaf(g, v[i], acc[i]);
+    }
+    if (y_shared) {
+        float v[V];
+        Vec<Elem, V>::load(y_shared + t * d + col, v);
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] += v[i];
+    }
+    Vec<Elem, V>::store(y + t * d + col, acc);
+}
+
+template <typename Elem, int V>
+int launch_v(const void* y_perm, const int32_t* token_row, const float* gate, const void* y_shared,
+             int64_t T, int d, int k, void* y, hipStream_t s) {
+    const int chunks = d / V;
+    const int64_t blocks = ceil_div(T * chunks, COMBINE_THREADS);
+    hipLaunchKernelGGL((combine_kernel<Elem, V>), dim3((unsigned)blocks), dim3(COMBINE_THREADS), 0,
+                       s, (const Elem*)y_perm, token_row, gate, (const Elem*)y_shared, T, d, k,
+                       chunks, (Elem*)y);
+    return launch_status();
+}
+
+}  // namespace
+
+int launch_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* gate,
+                   const void* y_shared, int64_t T, int d, int k, void* y, hipStream_t s) {
+    if (T == 0 || d == 0) return MOE_OK;
+    if (dtype == MOE_BF16) {
+        if (d % 8 == 0) return launch_v<bf16_t, 8>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
+        return launch_v<bf16_t, 1>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
+    }
+    if (d % 4 == 0) return launch_v<float, 4>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
+    return launch_v<float, 1>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
+}
+
+}  // namespace moe

@@ -1,0 +1,78 @@
+// Internal helpers of the HIP library (gfx950 only).  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "moe.h"
+
+namespace moe {
+
+// Element storage types: bf16 is kept as its 16-bit pattern.
+typedef uint16_t bf16_t;
+
+// MFMA operand / accumulator vector types.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+    return __uint_as_float(((uint32_t)h) << 16);
+}
+
+// fp32 -> bf16, round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x0040u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+__device__ __forceinline__ float silu(float a) {
+    return a / (1.0f + __expf(-a));
+}
+
+__host__ __device__ constexpr int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Launch-error check shared by the host wrappers.
+inline int launch_status() {
+    hipError_t e = hipGetLastError();
+    return e == hipSuccess ? MOE_OK : MOE_ERR_DEVICE;
+}
+
+// ---------------------------------------------------------------------------
+// Internal launchers (one translation unit each); arguments already validated.
+// ---------------------------------------------------------------------------
+int launch_route_topk(const void* x, int dtype, const void* w, const float* bias, int64_t T, int d,
+                      int E, int k, int flags, float* logits, int32_t* idx, float* gate,
+                      hipStream_t s);
+
+int launch_histogram(const int32_t* idx, int64_t T, int k, int E, int32_t* counts, int32_t* coact,
+                     hipStream_t s);
+
+struct PermuteTables {
+    uint64_t hosts[MOE_MAX_E];          // bit j set iff GPU j hosts expert e
+    int16_t slot_of[MOE_MAX_E];         // local slot of expert e, or -1
+    int16_t expert_of_slot[MOE_MAX_GROUPS];
+};
+
+int launch_permute(const void* x, int dtype, const int32_t* idx, const float* gate,
+                   const int32_t* counts, int64_t T, int d, int k, int E, const PermuteTables& tab,
+                   int n_local, int G, int dev, void* x_perm, int64_t cap_rows,
+                   int32_t* group_offsets, int32_t* row_token, float* row_gate, int32_t* token_row,
+                   int32_t* send_counts, void* ws, hipStream_t s);
+size_t permute_ws_bytes(int64_t T, int k, int E);
+
+int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, int n_groups,
+                       const void* const* w13, const void* const* w2, int d, int f,
+                       int64_t cap_rows, void* y_perm, void* ws, hipStream_t s);
+size_t grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_groups);
+
+int launch_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* gate,
+                   const void* y_shared, int64_t T, int d, int k, void* y, hipStream_t s);
+
+}  // namespace moe

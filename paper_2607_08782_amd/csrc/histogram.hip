@@ -1,0 +1,97 @@
+// Per-expert workload counts and co-activation counts (Sec. VI-A of the
+// Director paper: W counts the tokens routed to each expert and drives the
+// per-GPU load of Eq. 1; co-activation is the signal for co-locating experts
+// that fire together, Sec. I).
+//
+// Integer atomics only, so the result does not depend on scheduling: each
+// workgroup accumulates in LDS, then adds its non-zero bins to global memory.
+#include "common.h"
+
+namespace moe {
+namespace {
+
+constexpr int HIST_THREADS = 256;
+constexpr int LDS_COACT_MAX_E = 128;     // E*E int32 bins fit in 64 KiB of LDS
+
+__global__ void zero_i32_kernel(int32_t* __restrict__ p, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = 0;
+}
+
+template <bool COACT, bool LDS_COACT>
+__global__ __launch_bounds__(HIST_THREADS) void histogram_kernel(
+    const int32_t* __restrict__ idx, int64_t T, int k, int E, int32_t* __restrict__ counts,
+    int32_t* __restrict__ coact) {
+    __shared__ int32_t c_lds[MOE_MAX_E];
+    extern __shared__ int32_t co_lds[];          // [E][E] when LDS_COACT
+    for (int i = threadIdx.x; i < E; i += HIST_THREADS) c_lds[i] = 0;
+    if (LDS_COACT)
+        for (int i = threadIdx.x; i < E * E; i += HIST_THREADS) co_lds[i] = 0;
+    __syncthreads();
+
+    for (int64_t t = (int64_t)blockIdx.x * HIST_THREADS + threadIdx.x; t < T;
+         t += (int64_t)gridDim.x * HIST_THREADS) {
+        const int32_t* row = idx + t * k;
+        int sel[MOE_MAX_K];
+#pragma unroll
+        for (int r = 0; r < MOE_MAX_K; ++r) {
+            // out-of-range indices are ignored rather than written out of bounds
+            if (r < k) sel[r] = row[r];
+            if (r < k && (unsigned)sel[r] >= (unsigned)E) sel[r] = -1;
+        }
+#pragma unroll
+        for (int r = 0; r < MOE_MAX_K; ++r) {
+            if (r >= k) break;
+            if (sel[r] < 0) continue;
+            atomicAdd(&c_lds[sel[r]], 1);
+            if (COACT) {
+#pragma unroll
+                for (int q = 0; q < MOE_MAX_K; ++q) {
+                    if (q >= k) break;
+                    if (sel[q] < 0) continue;
+                    if (LDS_COACT) atomicAdd(&co_lds[sel[r] * E + sel[q]], 1);
+                    else atomicAdd(&coact[(int64_t)sel[r] * E + sel[q]], 1);
+                }
+            }
+        }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < E; i += HIST_THREADS)
+        if (c_lds[i]) atomicAdd(&counts[i], c_lds[i]);
+    if (LDS_COACT)
+        for (int i = threadIdx.x; i < E * E; i += HIST_THREADS)
+            if (co_lds[i]) atomicAdd(&coact[i], co_lds[i]);
+}
+
+}  // namespace
+
+int launch_histogram(const int32_t* idx, int64_t T, int k, int E, int32_t* counts, int32_t* coact,
+                     hipStream_t s) {
+    const int64_t nbins = (int64_t)E + (coact ? (int64_t)E * E : 0);
+    hipLaunchKernelGGL(zero_i32_kernel, dim3((unsigned)ceil_div(E, 256)), dim3(256), 0, s, counts,
+                       (int64_t)E);
+    if (coact)
+        hipLaunchKernelGGL(zero_i32_kernel, dim3((unsigned)ceil_div((int64_t)E * E, 256)),
+                           dim3(256), 0, s, coact, (int64_t)E * E);
+    (void)nbins;
+    if (T == 0) return launch_status();
+    int64_t blocks = ceil_div(T, HIST_THREADS);
+    if (!coact) {
+        if (blocks > 512) blocks = 512;
+        hipLaunchKernelGGL((histogram_kernel<false, false>), dim3((unsigned)blocks),
+                           dim3(HIST_THREADS), 0, s, idx, T, k, E, counts, coact);
+    } else if (E <= LDS_COACT_MAX_E) {
+        if (blocks > 32) blocks = 32;
+        const size_t lds = (size_t)E * E * sizeof(int32_t);
+        hipLaunchKernelGGL((histogram_kernel<true, true>), dim3((unsigned)blocks),
+                           dim3(HIST_THREADS), lds, s, idx, T, k, E, counts, coact);
+    } else {
+        if (blocks > 512) blocks = 512;
+        hipLaunchKernelGGL((histogram_kernel<true, false>), dim3((unsigned)blocks),
+                           dim3(HIST_THREADS), 0, s, idx, T, k, E, counts, coact);
+    }
+    return launch_status();
+}
+
+}  // namespace moe

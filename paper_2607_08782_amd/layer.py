@@ -1,0 +1,136 @@
+"""One GPU's share of one MoE layer, run through the five C-ABI calls.
+
+`LayerShare` owns the device buffers of one share (allocated once with
+torch) and enqueues, on the current stream:
+    moe_route_topk -> moe_expert_histogram -> moe_permute
+    -> moe_grouped_ffn (routed experts) [-> moe_grouped_ffn (shared experts)]
+    -> moe_combine
+with no host synchronisation in between.  The expert placement can be
+swapped between batches (`set_placement`) by re-pointing the weight table;
+nothing is reallocated.
+"""
+from __future__ import annotations
+
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+from . import moe
+
+
+def concat_shared(shared: Sequence[Tuple[torch.Tensor, torch.Tensor]]):
+    """Lay several always-on SwiGLU experts out as one wider expert.
+
+    For experts u with W13_u = [G_u; U_u] and W2_u, the sum over u of
+    W2_u (SiLU(G_u x) * U_u x) equals the single expert with gate rows
+    [G_0; G_1; ...], up rows [U_0; U_1; ...] and W2 = [W2_0 | W2_1 | ...].
+    """
+    if not shared:
+        return None
+    if len(shared) == 1:
+        return shared[0][0].contiguous(), shared[0][1].contiguous()
+    gates, ups, downs = [], [], []
+    for w13, w2 in shared:
+        f = w13.shape[0] // 2
+        gates.append(w13[:f])
+        ups.append(w13[f:])
+        downs.append(w2)
+    return torch.cat(gates + ups, 0).contiguous(), torch.cat(downs, 1).contiguous()
+
+
+class LayerShare:
+    def __init__(self, X: torch.Tensor, Wr: torch.Tensor, bias: Optional[torch.Tensor], k: int,
+                 placement: np.ndarray, dev: int, w13: Sequence[torch.Tensor],
+                 w2: Sequence[torch.Tensor], shared=(), renorm: bool = True,
+                 coact: bool = False, want_logits: bool = True, cap_rows: Optional[int] = None):
+        self.device = X.device
+        self.X = X
+        self.Wr = Wr
+        self.bias = bias
+        self.T, self.d = X.shape
+        self.E = Wr.shape[0]
+        self.k = k
+        self.dev = dev
+        self.renorm = renorm
+        self.want_coact = coact
+        self.placement = np.ascontiguousarray(placement, dtype=np.uint8)
+        self.G = self.placement.shape[1]
+        self.n_local = int(self.placement[:, dev].sum())
+        self.cap_rows = cap_rows if cap_rows is not None else self.T * min(k, self.n_local)
+        T, d, E, dt = self.T, self.d, self.E, X.dtype
+        dv = self.device
+        self.logits = torch.empty((T, E), dtype=torch.float32, device=dv) if want_logits else None
+        self.topk_idx = torch.empty((T, k), dtype=torch.int32, device=dv)
+        self.topk_gate = torch.empty((T, k), dtype=torch.float32, device=dv)
+        self.counts = torch.empty((E,), dtype=torch.int32, device=dv)
+        self.coact = torch.empty((E, E), dtype=torch.int32, device=dv) if coact else None
+        cap = max(self.cap_rows, 1)
+        self.perm = {
+            "x_perm": torch.empty((cap, d), dtype=dt, device=dv),
+            "group_offsets": torch.empty((self.n_local + 1,), dtype=torch.int32, device=dv),
+            "row_token": torch.empty((cap,), dtype=torch.int32, device=dv),
+            "row_gate": torch.empty((cap,), dtype=torch.float32, device=dv),
+            "token_row": torch.empty((T, k), dtype=torch.int32, device=dv),
+            "send_counts": torch.empty((self.G,), dtype=torch.int32, device=dv),
+        }
+        self.ws_perm = moe.workspace(moe.moe_permute_ws_bytes(T, k, E), dv)
+        self.y_perm = torch.empty((cap, d), dtype=dt, device=dv)
+        self.weights = moe.WeightTable(w13, w2) if self.n_local else None
+        self.f = self.weights.f if self.weights else (w13[0].shape[0] // 2 if len(w13) else 0)
+        dcode = moe.MOE_BF16 if dt == torch.bfloat16 else moe.MOE_F32
+        self.ws_ffn = moe.workspace(
+            moe.moe_grouped_ffn_ws_bytes(dcode, self.cap_rows, d, max(self.f, 1), max(self.n_local, 1)), dv)
+        sh = concat_shared(list(shared))
+        if sh is not None:
+            self.shared_weights = moe.WeightTable([sh[0]], [sh[1]])
+            self.shared_offsets = torch.tensor([0, T], dtype=torch.int32, device=dv)
+            self.y_shared = torch.empty((max(T, 1), d), dtype=dt, device=dv)
+            self.ws_shared = moe.workspace(
+                moe.moe_grouped_ffn_ws_bytes(dcode, T, d, self.shared_weights.f, 1), dv)
+        else:
+            self.shared_weights = None
+            self.y_shared = None
+        self.y = torch.empty((max(T, 1), d), dtype=dt, device=dv)
+
+    def set_placement(self, placement: np.ndarray, w13: Sequence[torch.Tensor],
+                      w2: Sequence[torch.Tensor]):
+        """Swap the expert placement between batches (same number of local slots)."""
+        placement = np.ascontiguousarray(placement, dtype=np.uint8)
+        n_local = int(placement[:, self.dev].sum())
+        if n_local != self.n_local:
+            raise ValueError("the new placement must keep %d local slots" % self.n_local)
+        self.placement = placement
+        self.weights = moe.WeightTable(w13, w2)
+
+    def set_inputs(self, X: torch.Tensor, bias: Optional[torch.Tensor] = None):
+        if tuple(X.shape) != (self.T, self.d) or X.dtype != self.X.dtype:
+            raise ValueError("X must keep shape and dtype")
+        self.X = X
+        if bias is not None:
+            self.bias = bias
+
+    def route(self, logits_in: Optional[torch.Tensor] = None):
+        if logits_in is not None:
+            moe.moe_route_topk(None, None, None, self.k, renorm=self.renorm, logits=logits_in,
+                               logits_in=True, topk_idx=self.topk_idx, topk_gate=self.topk_gate)
+        else:
+            moe.moe_route_topk(self.X, self.Wr, self.bias, self.k, renorm=self.renorm,
+                               logits=self.logits, want_logits=self.logits is not None,
+                               topk_idx=self.topk_idx, topk_gate=self.topk_gate)
+
+    def run(self, logits_in: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """Enqueue the whole share on the current stream; returns y [T, d]."""
+        self.route(logits_in)
+        moe.moe_expert_histogram(self.topk_idx, self.E, counts=self.counts, coact=self.coact)
+        moe.moe_permute(self.X, self.topk_idx, self.topk_gate, self.counts, self.placement,
+                        self.dev, E=self.E, cap_rows=self.cap_rows, out=self.perm, ws=self.ws_perm)
+        if self.weights is not None:
+            moe.moe_grouped_ffn(self.perm["x_perm"], self.perm["group_offsets"], self.weights,
+                                cap_rows=self.cap_rows, y_perm=self.y_perm, ws=self.ws_ffn)
+        if self.shared_weights is not None:
+            moe.moe_grouped_ffn(self.X, self.shared_offsets, self.shared_weights, cap_rows=self.T,
+                                y_perm=self.y_shared, ws=self.ws_shared)
+        moe.moe_combine(self.y_perm, self.perm["token_row"], self.topk_gate, self.y_shared,
+                        T=self.T, d=self.d, y=self.y)
+        return self.y

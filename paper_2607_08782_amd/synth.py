@@ -181,7 +181,8 @@ def make_layer(cfg: LayerConfig, T: int, seed: int = 0, device="cpu", batch: int
                dev: int = 0, experts: str = "local") -> LayerInputs:
     """All inputs of one layer share: hidden states of batch `batch`, the router,
     the Zipf bias and placement of that batch's popularity epoch, and the
-    weights of the experts hosted on `dev` (or of every expert)."""
+    weights of the experts hosted on `dev` (experts="local"), of every expert
+    ("all") or of none ("none")."""
     epoch = batch // cfg.drift_every if cfg.drift_every else 0
     pi = popularity_perm(cfg, seed, epoch)
     X = normal((T, cfg.d), seed, "X", batch, 1.0, device, cfg.torch_dtype)
@@ -189,7 +190,7 @@ def make_layer(cfg: LayerConfig, T: int, seed: int = 0, device="cpu", batch: int
     bias = torch.from_numpy(zipf_bias(cfg, pi)).to(device)
     placement = placement_map(cfg, pi)
     local = [int(e) for e in np.nonzero(placement[:, dev])[0]]
-    which = local if experts == "local" else list(range(cfg.E))
+    which = {"local": local, "none": [], "all": list(range(cfg.E))}[experts]
     w13, w2 = [], []
     for e in which:
         a, b = expert_weights(cfg, e, seed, device)

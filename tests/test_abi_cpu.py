@@ -1,0 +1,146 @@
+"""Host-side checks of the C ABI that need no GPU.
+
+The library must load and export every entry point include/moe.h declares,
+and every validation error must be returned before anything touches HIP
+(these calls use argument combinations that fail validation, so no kernel is
+ever launched and no device pointer is ever dereferenced).
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2607_08782_amd import moe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(moe.LIB_PATH):
+        from paper_2607_08782_amd import build
+        build.build()
+    return moe.load_library()
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+char\*|int|size_t)\s+(moe_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_five_steps():
+    names = _declared()
+    for n in ("moe_route_topk", "moe_expert_histogram", "moe_permute", "moe_grouped_ffn",
+              "moe_combine"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert set(_declared()) == set(moe.EXPORTS)
+
+
+def test_status_strings(lib):
+    for code in range(5):
+        assert moe.status_string(code) != "unknown status"
+    assert moe.status_string(99) == "unknown status"
+
+
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation
+
+
+def test_route_topk_validation(lib):
+    f = lib.moe_route_topk
+    ok = dict(x=FAKE, dtype=1, w=FAKE, b=None, T=4, d=64, E=8, k=2, flags=1, lg=FAKE, idx=FAKE,
+              gate=FAKE)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["x"], a["dtype"], a["w"], a["b"], a["T"], a["d"], a["E"], a["k"], a["flags"],
+                 a["lg"], a["idx"], a["gate"], None)
+    assert call(k=0) == moe.MOE_ERR_ARG
+    assert call(k=9) == moe.MOE_ERR_ARG            # k > E
+    assert call(E=300, k=2) == moe.MOE_ERR_ARG      # E > MOE_MAX_E
+    assert call(E=64, k=17) == moe.MOE_ERR_ARG      # k > MOE_MAX_K
+    assert call(T=-1) == moe.MOE_ERR_ARG
+    assert call(dtype=7) == moe.MOE_ERR_ARG
+    assert call(flags=8) == moe.MOE_ERR_ARG
+    assert call(idx=None) == moe.MOE_ERR_ARG
+    assert call(x=None) == moe.MOE_ERR_ARG
+    assert call(d=12) == moe.MOE_ERR_SHAPE          # bf16 rows must be 16-byte multiples
+    assert call(x=ctypes.c_void_p(0x1002)) == moe.MOE_ERR_ARG   # misaligned bf16 rows
+    assert call(flags=3, lg=None) == moe.MOE_ERR_ARG             # logits-in without logits
+
+
+def test_histogram_validation(lib):
+    f = lib.moe_expert_histogram
+    assert f(FAKE, 4, 0, 8, FAKE, None, None) == moe.MOE_ERR_ARG
+    assert f(FAKE, 4, 2, 0, FAKE, None, None) == moe.MOE_ERR_ARG
+    assert f(FAKE, 4, 2, 8, None, None, None) == moe.MOE_ERR_ARG
+    assert f(None, 4, 2, 8, FAKE, None, None) == moe.MOE_ERR_ARG
+
+
+def _permute(lib, placement, T=10, k=2, E=4, cap=None, ws_bytes=None, dev=0, c_max=0, d=64,
+             dtype=1):
+    pl = np.ascontiguousarray(placement, np.uint8)
+    G = pl.shape[1]
+    if cap is None:
+        cap = T * k
+    if ws_bytes is None:
+        ws_bytes = lib.moe_permute_ws_bytes(T, k, E)
+    return lib.moe_permute(FAKE, dtype, FAKE, FAKE, FAKE, T, d, k, E,
+                           pl.ctypes.data_as(ctypes.c_void_p), G, dev, c_max, FAKE, cap, FAKE,
+                           FAKE, FAKE, FAKE, FAKE, ctypes.c_void_p(0x100000), ws_bytes, None)
+
+
+def test_permute_placement_and_capacity_validation(lib):
+    pl = np.array([[1, 0], [0, 1], [1, 1], [0, 0]])     # expert 3 has no host
+    assert _permute(lib, pl) == moe.MOE_ERR_PLACEMENT
+    pl[3, 1] = 1
+    assert _permute(lib, pl, dev=2) == moe.MOE_ERR_PLACEMENT          # dev >= G
+    assert _permute(lib, pl, c_max=1) == moe.MOE_ERR_PLACEMENT        # 2 local experts > c_max
+    assert _permute(lib, pl, cap=10 * 2 - 1) == moe.MOE_ERR_SHAPE     # cap < T*min(k, n_local)
+    assert _permute(lib, pl, ws_bytes=16) == moe.MOE_ERR_SHAPE
+    assert _permute(lib, pl, d=12) == moe.MOE_ERR_SHAPE
+    assert _permute(lib, pl, k=0) == moe.MOE_ERR_ARG
+    assert _permute(lib, pl, dtype=5) == moe.MOE_ERR_ARG
+    big = np.ones((4, 65), np.uint8)
+    assert _permute(lib, big) == moe.MOE_ERR_PLACEMENT                # G > MOE_MAX_G
+
+
+def test_grouped_ffn_validation(lib):
+    f = lib.moe_grouped_ffn
+    arr = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    null_arr = (ctypes.c_void_p * 2)(0x1000, None)
+    P = ctypes.cast(arr, ctypes.c_void_p)
+
+    def call(dtype=1, n=2, d=128, f_=64, cap=16, w13=P, ws=0x100000, ws_bytes=1 << 30):
+        return f(FAKE, dtype, FAKE, n, w13, P, d, f_, cap, FAKE, ctypes.c_void_p(ws), ws_bytes, None)
+    assert call(n=0) == moe.MOE_ERR_ARG
+    assert call(n=129) == moe.MOE_ERR_ARG
+    assert call(d=100) == moe.MOE_ERR_SHAPE
+    assert call(f_=96) == moe.MOE_ERR_SHAPE
+    assert call(ws_bytes=10) == moe.MOE_ERR_SHAPE
+    assert call(ws=0x100010) == moe.MOE_ERR_SHAPE        # workspace not 256-byte aligned
+    assert call(w13=ctypes.cast(null_arr, ctypes.c_void_p)) == moe.MOE_ERR_ARG
+    assert call(dtype=3) == moe.MOE_ERR_ARG
+
+
+def test_combine_validation(lib):
+    f = lib.moe_combine
+    assert f(FAKE, 1, FAKE, FAKE, None, 4, 64, 0, FAKE, None) == moe.MOE_ERR_ARG
+    assert f(FAKE, 1, FAKE, FAKE, None, 4, 0, 2, FAKE, None) == moe.MOE_ERR_ARG
+    assert f(FAKE, 1, None, FAKE, None, 4, 64, 2, FAKE, None) == moe.MOE_ERR_ARG
+    assert f(FAKE, 1, FAKE, FAKE, None, 4, 64, 2, ctypes.c_void_p(0x1008), None) == moe.MOE_ERR_ARG
+
+
+def test_workspace_sizes(lib):
+    a = lib.moe_permute_ws_bytes(1000, 4, 60)
+    b = lib.moe_permute_ws_bytes(2000, 4, 60)
+    assert 0 < a < b
+    assert lib.moe_grouped_ffn_ws_bytes(1, 100, 256, 128, 4) >= 100 * 128 * 2
+    assert lib.moe_grouped_ffn_ws_bytes(0, 100, 256, 128, 4) >= 100 * 128 * 4

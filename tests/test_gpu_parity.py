@@ -1,0 +1,198 @@
+"""HIP path vs the CPU oracle, on the GPU (marked `gpu`).
+
+Small shapes check every output element and span several tiles with ragged
+tails; the model-shaped layer shares check routing bit for bit at full size
+and the FFN / combined outputs on sampled rows and tokens.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_08782_amd import moe, synth
+from paper_2607_08782_amd.layer import LayerShare
+
+from parity import (Case, check_end_to_end_routing, check_ffn_and_combine, check_logits,
+                    check_routing, close, np32, say, OUT_TOL)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    moe.load_library()          # fails loudly if the HIP library is not built
+    yield
+
+
+SMALL = {
+    "tiny_fp32": (synth.CONFIGS["tiny_fp32"], 64),
+    "bf16_ragged_replicas": (synth.custom_config(d=256, E=16, k=4, f=384, G=3, replicas=2,
+                                                 zipf=1.2), 300),
+    "bf16_two_shared": (synth.custom_config(d=128, E=12, k=3, f=192, shared_f=(128, 64), G=2,
+                                            replicas=1, zipf=1.0), 200),
+    "bf16_k1": (synth.custom_config(d=64, E=8, k=1, f=64, G=1), 130),
+    "bf16_k_eq_E": (synth.custom_config(d=64, E=8, k=8, f=128, G=2), 70),
+    "bf16_E128_coact": (synth.custom_config(d=128, E=128, k=8, f=64, G=9, replicas=2, zipf=1.5,
+                                            coact=True), 257),
+    "bf16_T1": (synth.custom_config(d=128, E=8, k=2, f=128, G=2), 1),
+    "fp32_ragged": (synth.custom_config(dtype="f32", d=72, E=6, k=2, f=40, shared_f=(24,), G=2,
+                                        replicas=1, zipf=1.0), 77),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_small_shapes_every_element(name):
+    cfg, T = SMALL[name]
+    say("[case]", name, cfg, "T=%d" % T)
+    case = Case(cfg, T)
+    ref_logits, _ = check_logits(case)
+    idx, gate, pm = check_routing(case, ref_logits)
+    check_ffn_and_combine(case, idx, gate, pm, sample=None)
+    check_end_to_end_routing(case, ref_logits)
+
+
+FULL = [
+    ("mixtral_8x7b", "prefill"), ("mixtral_8x7b", "decode"),
+    ("deepseek_v2_lite", "prefill"), ("deepseek_v2_lite", "decode"),
+    ("qwen15_moe_a27b", "batch"),
+    ("qwen3_30b_a3b", "decode"), ("qwen3_30b_a3b", "prefill"),
+]
+
+
+@pytest.mark.parametrize("name,regime", FULL)
+def test_model_shaped_layer_share(name, regime):
+    cfg = synth.CONFIGS[name]
+    T = cfg.T(regime)
+    say("[case]", name, regime, "T=%d" % T)
+    case = Case(cfg, T)
+    ref_logits, _ = check_logits(case)
+    idx, gate, pm = check_routing(case, ref_logits)
+    say("  rows here", pm["rows"], "send_counts", pm["send_counts"].tolist())
+    worst = check_ffn_and_combine(case, idx, gate, pm, sample=6)
+    differ = check_end_to_end_routing(case, ref_logits)
+    say("  worst rel err %.2e, top-k sets differing from the oracle: %.4f" % (worst, differ))
+
+
+def test_drift_sequence_swaps_placement_without_reallocating():
+    """Qwen1.5-MoE-shaped share: popularity re-ranked every 4 batches, placement
+    swapped between batches by re-pointing the weight table."""
+    cfg = synth.CONFIGS["qwen15_moe_a27b"]
+    T = cfg.T("batch")
+    base = Case(cfg, T, batch=0)
+    share = base.share
+    ptr_before = share.perm["x_perm"].data_ptr()
+    for b in (0, 3, 4, 9, 15):
+        say("[case] drift batch", b)
+        inp = synth.make_layer(cfg, T, seed=0, device="cuda", batch=b)
+        share.set_inputs(inp.X, inp.bias)
+        share.set_placement(inp.placement, inp.w13, inp.w2)
+        case = Case.__new__(Case)
+        case.cfg, case.T, case.inp, case.share = cfg, T, inp, share
+        case.X, case.Wr, case.b, case._w = np32(inp.X), np32(inp.Wr), np32(inp.bias), {}
+        ref_logits, _ = check_logits(case)
+        idx, gate, pm = check_routing(case, ref_logits)
+        check_ffn_and_combine(case, idx, gate, pm, sample=3, seed=b)
+    assert share.perm["x_perm"].data_ptr() == ptr_before
+
+
+def _share(cfg, T, logits=None, placement=None, dev=0):
+    inp = synth.make_layer(cfg, T, seed=1, device="cuda")
+    pl = inp.placement if placement is None else placement
+    local = [int(e) for e in np.nonzero(pl[:, dev])[0]]
+    ws = [synth.expert_weights(cfg, e, 1, "cuda") for e in local]
+    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, pl, dev, [a for a, _ in ws],
+                       [b for _, b in ws], shared=inp.shared)
+    return inp, share
+
+
+def test_empty_batch():
+    cfg = synth.custom_config(d=64, E=8, k=2, f=64, G=2)
+    inp, share = _share(cfg, 0)
+    share.run()
+    torch.cuda.synchronize()
+    assert share.perm["group_offsets"].cpu().numpy().tolist() == [0] * (share.n_local + 1)
+    assert share.perm["send_counts"].cpu().numpy().tolist() == [0, 0]
+    assert share.counts.cpu().numpy().tolist() == [0] * 8
+
+
+def test_ties_all_equal_and_signed_zero_logits():
+    cfg = synth.custom_config(d=64, E=8, k=3, f=64, G=1)
+    T = 70
+    inp, share = _share(cfg, T)
+    L = np.full((T, 8), 0.75, np.float32)
+    L[1] = [0.0, -0.0, 0.0, -0.0, -1.0, 0.0, -0.0, -2.0]
+    L[2] = [-0.0, 1.0, -0.0, 1.0, 0.0, 1.0, 0.0, 3.0]
+    share.run(logits_in=torch.from_numpy(L).cuda())
+    torch.cuda.synchronize()
+    gidx = share.topk_idx.cpu().numpy()
+    assert gidx[0].tolist() == [0, 1, 2] and gidx[5].tolist() == [0, 1, 2]
+    assert gidx[1].tolist() == [0, 1, 2]
+    assert gidx[2].tolist() == [7, 1, 3]
+    oidx, og = oracle.topk(L, 3)
+    np.testing.assert_array_equal(gidx, oidx)
+    close(np32(share.topk_gate), og, 1e-5, "gates")
+
+
+def test_every_token_to_one_expert_and_a_gpu_with_no_rows():
+    cfg = synth.custom_config(d=128, E=8, k=2, f=128, G=2)
+    T = 150
+    pl = np.zeros((8, 2), np.uint8)
+    pl[:4, 0] = 1
+    pl[4:, 1] = 1
+    L = np.zeros((T, 8), np.float32)
+    L[:, 1] = 5.0
+    L[:, 2] = 4.0                                # every token: experts 1, 2 (both on GPU 0)
+    for dev, expect_rows in ((0, 2 * T), (1, 0)):
+        inp, share = _share(cfg, T, placement=pl, dev=dev)
+        share.run(logits_in=torch.from_numpy(L).cuda())
+        torch.cuda.synchronize()
+        go = share.perm["group_offsets"].cpu().numpy()
+        assert go[-1] == expect_rows
+        assert share.perm["send_counts"].cpu().numpy().tolist() == [2 * T, 0]
+        if dev == 1:
+            np.testing.assert_array_equal(share.perm["token_row"].cpu().numpy(), -1)
+            np.testing.assert_array_equal(np32(share.y), 0.0)
+        else:
+            idx, gate = oracle.topk(L, 2)
+            pm = oracle.permute(np32(inp.X), idx, gate, 8, pl, 0)
+            np.testing.assert_array_equal(go, pm["group_offsets"])
+
+
+def test_gpu_hosting_no_expert_returns_shared_output_only():
+    cfg = synth.custom_config(d=128, E=4, k=2, f=64, shared_f=(128,), G=2)
+    pl = np.zeros((4, 2), np.uint8)
+    pl[:, 0] = 1
+    inp, share = _share(cfg, 90, placement=pl, dev=1)
+    assert share.n_local == 0
+    share.run()
+    torch.cuda.synchronize()
+    ys = oracle.expert_ffn(np32(inp.X), np32(inp.shared[0][0]), np32(inp.shared[0][1]))
+    close(np32(share.y), ys, OUT_TOL["bf16"], "shared-only y")
+
+
+def test_repeated_runs_are_bitwise_identical():
+    cfg = synth.custom_config(d=256, E=16, k=4, f=256, G=3, replicas=2, zipf=1.2, coact=True)
+    inp, share = _share(cfg, 500)
+    share.coact = torch.empty((16, 16), dtype=torch.int32, device="cuda")
+    outs = []
+    for _ in range(3):
+        share.run()
+        torch.cuda.synchronize()
+        outs.append([share.y.clone(), share.coact.clone(), share.perm["row_token"].clone()])
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            assert torch.equal(a, b)
+
+
+def test_doubling_w2_doubles_expert_outputs_exactly():
+    cfg = synth.custom_config(d=128, E=8, k=2, f=192, G=2)
+    inp, share = _share(cfg, 200)
+    share.run()
+    torch.cuda.synchronize()
+    y1 = share.y_perm.clone()
+    N = int(share.perm["group_offsets"][-1])
+    share.set_placement(share.placement, share.weights.w13, [2 * w for w in share.weights.w2])
+    share.run()
+    torch.cuda.synchronize()
+    assert torch.equal(share.y_perm[:N], 2 * y1[:N])
