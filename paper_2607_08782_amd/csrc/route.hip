@@ -2,10 +2,9 @@
 // network scores each expert for every token and the token is sent to the k
 // best; the gate is replicated on every GPU, Sec. II-B).
 //
-// One workgroup of 256 threads owns 64 tokens:
-//   phase 1  scores for the 64 tokens x all E experts into LDS
-//            bf16: MFMA 16x16x32 (four waves x 16 tokens, router rows staged
-//            through LDS once per workgroup and K step);
+// Each workgroup owns a block of tokens:
+//   phase 1  scores for its tokens x all E experts into LDS
+//            bf16: MFMA 16x16x32, K split over 16 waves, fixed-order reduction;
 //            f32:  plain FMA loops;  logits-in: copied from global memory
 //   phase 2  bias added, scores written back coalesced (if requested)
 //   phase 3  one thread per token: insertion top-k over the LDS row, gates.
@@ -16,9 +15,8 @@ namespace {
 
 constexpr int ROUTE_TOKENS = 64;
 constexpr int ROUTE_THREADS = 256;
-constexpr int ROUTE_BK = 32;          // K per MFMA 16x16x32 step
 
-enum RouteMode { MODE_BF16 = 0, MODE_F32 = 1, MODE_LOGITS_IN = 2 };
+enum RouteMode { MODE_F32 = 1, MODE_LOGITS_IN = 2 };
 
 // "a ranks before b": larger score, or equal score and lower expert index.
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
@@ -70,72 +68,139 @@ __device__ void topk_row(const float* s, int E, int k, bool renorm, int32_t* idx
     }
 }
 
-template <int MODE, int KM>
-__global__ __launch_bounds__(ROUTE_THREADS) void route_kernel(
-    const void* __restrict__ xv, const void* __restrict__ wv, const float* __restrict__ bias,
+// Bias, optional score store and top-k for the `nt` tokens whose scores sit in
+// S[r * ldS + e] (LDS), one thread per token.
+template <int KM>
+__device__ __forceinline__ void finish_tokens(float* S, int ldS, int nt, int64_t t0, int E, int k,
+                                              int renorm, const float* __restrict__ bias,
+                                              bool add_bias, float* __restrict__ logits,
+                                              int32_t* __restrict__ idx, float* __restrict__ gate) {
+    const int tid = threadIdx.x, nthr = blockDim.x;
+    if (add_bias) {
+        for (int c = tid; c < nt * E; c += nthr) {
+            const int r = c / E, e = c % E;
+            float v = S[r * ldS + e];
+            if (bias) v += bias[e];
+            S[r * ldS + e] = v;
+            if (logits) logits[(t0 + r) * E + e] = v;
+        }
+        __syncthreads();
+    }
+    if (tid < nt) {
+        const int64_t t = t0 + tid;
+        topk_row<KM>(S + tid * ldS, E, k, renorm != 0, idx + t * k, gate + t * k);
+    }
+}
+
+// bf16 gate scores on MFMA 16x16x32.  A workgroup of 16 waves owns 16*RT
+// tokens; wave w takes the K steps w, w+16, w+32, ... (32 elements each) for
+// all RT token tiles and up to NTM expert tiles, with operand fragments loaded
+// straight from global memory (the router matrix stays L2-resident); the
+// 16 waves per workgroup hide the load latency.  Partial scores are reduced in LDS in a fixed order
+// (four slices, each summed over its four waves in turn, then the slices in
+// turn), so the scores are deterministic.
+constexpr int RB_WAVES = 16;
+constexpr int RB_THREADS = RB_WAVES * 64;
+
+template <int RT, int NTM, int KM>
+__global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, const float* __restrict__ bias,
     int64_t T, int d, int E, int k, int renorm, float* __restrict__ logits,
     int32_t* __restrict__ idx, float* __restrict__ gate) {
     extern __shared__ float smem[];
+    constexpr int ROWS = 16 * RT;
     const int E_pad = (E + 15) & ~15;
-    const int ldS = E_pad + 1;                   // odd stride: conflict-free row scans
-    float* S = smem;                             // [64][ldS] scores
-    bf16_t* Wst = (bf16_t*)(smem + ROUTE_TOKENS * ldS);   // [E_pad][ROUTE_BK] router slice (bf16)
+    const int ldS = E_pad + 1;
+    const int slice = ROWS * ldS;                     // floats per partial-score slice
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t t0 = (int64_t)blockIdx.x * ROWS;
+    const int nt = (int)((T - t0) < ROWS ? (T - t0) : ROWS);
+    const int NT = E_pad / 16;
+    const int row = lane & 15, kq = (lane >> 4) * 8;
 
+    const bf16_t* xbase = X + (t0 + row) * d + kq;       // token row `row` of tile 0
+    const bf16_t* wbase = W + (int64_t)row * d + kq;     // expert row `row` of tile 0
+    f32x4 acc[RT][NTM];
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int j = 0; j < NTM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nsteps = (d + 31) / 32;
+    for (int step = wave; step < nsteps; step += RB_WAVES) {
+        const int k0 = step * 32;
+        const bool kin = k0 + kq < d;
+        bf16x8 a[RT];
+#pragma unroll
+        for (int i = 0; i < RT; ++i) {
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (kin && i * 16 + row < nt) v = *(const uint4*)(xbase + (int64_t)i * 16 * d + k0);
+            a[i] = __builtin_bit_cast(bf16x8, v);
+        }
+#pragma unroll
+        for (int jc = 0; jc < NTM; jc += 4) {
+            if (jc >= NT) break;
+            bf16x8 b[4];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int j = jc + jj;
+                uint4 v = make_uint4(0, 0, 0, 0);
+                if (kin && j < NT && j * 16 + row < E)
+                    v = *(const uint4*)(wbase + (int64_t)j * 16 * d + k0);
+                b[jj] = __builtin_bit_cast(bf16x8, v);
+            }
+#pragma unroll
+            for (int i = 0; i < RT; ++i)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+                    if (jc + jj < NT)
+                        acc[i][jc + jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            a[i], b[jj], acc[i][jc + jj], 0, 0, 0);
+        }
+    }
+
+    // fixed-order reduction: slice g = wave & 3 receives waves g, g+4, g+8, g+12 in turn
+    const int g = wave & 3, q = wave >> 2;
+    float* Sg = smem + g * slice;
+    for (int pass = 0; pass < 4; ++pass) {
+        if (q == pass) {
+#pragma unroll
+            for (int i = 0; i < RT; ++i)
+#pragma unroll
+                for (int j = 0; j < NTM; ++j) {
+                    if (j >= NT) continue;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        float* dst = Sg + (i * 16 + (lane >> 4) * 4 + r) * ldS + j * 16 + (lane & 15);
+                        *dst = pass == 0 ? acc[i][j][r] : *dst + acc[i][j][r];
+                    }
+                }
+        }
+        __syncthreads();
+    }
+    for (int c = tid; c < ROWS * E_pad; c += RB_THREADS) {
+        const int r = c / E_pad, e = c % E_pad;
+        const int o = r * ldS + e;
+        smem[o] = ((smem[o] + smem[slice + o]) + smem[2 * slice + o]) + smem[3 * slice + o];
+    }
+    __syncthreads();
+    finish_tokens<KM>(smem, ldS, nt, t0, E, k, renorm, bias, true, logits, idx, gate);
+}
+
+// fp32 scores (plain FMA loops) or scores handed in (MOE_LOGITS_IN): 64 tokens
+// per workgroup of 256 threads.
+template <int MODE, int KM>
+__global__ __launch_bounds__(ROUTE_THREADS) void route_simple_kernel(
+    const float* __restrict__ X, const float* __restrict__ W, const float* __restrict__ bias,
+    int64_t T, int d, int E, int k, int renorm, float* __restrict__ logits,
+    int32_t* __restrict__ idx, float* __restrict__ gate) {
+    extern __shared__ float smem[];
+    const int ldS = ((E + 15) & ~15) + 1;
+    float* S = smem;
     const int tid = threadIdx.x;
     const int64_t t0 = (int64_t)blockIdx.x * ROUTE_TOKENS;
     const int nt = (int)((T - t0) < ROUTE_TOKENS ? (T - t0) : ROUTE_TOKENS);
-
-    if (MODE == MODE_BF16) {
-        const bf16_t* X = (const bf16_t*)xv;
-        const bf16_t* W = (const bf16_t*)wv;
-        const int wave = tid >> 6, lane = tid & 63;
-        const int row = lane & 15;                 // token row of this lane's A fragment
-        const int kq = (lane >> 4) * 8;            // K offset of this lane inside the 32-step
-        const int64_t trow = t0 + wave * 16 + row;
-        const bool row_ok = (wave * 16 + row) < nt;
-        const int NT = E_pad / 16;                 // expert tiles (<= 16)
-        f32x4 acc[16];
-#pragma unroll
-        for (int j = 0; j < 16; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-        for (int k0 = 0; k0 < d; k0 += ROUTE_BK) {
-            // stage W[0:E_pad, k0:k0+32] in LDS, 16 bytes per thread per pass
-            const int chunks = E_pad * (ROUTE_BK / 8);
-            for (int c = tid; c < chunks; c += ROUTE_THREADS) {
-                const int e = c >> 2, kc = (c & 3) * 8;
-                uint4 v = make_uint4(0, 0, 0, 0);
-                if (e < E && k0 + kc < d) v = *(const uint4*)(W + (int64_t)e * d + k0 + kc);
-                *(uint4*)(Wst + e * ROUTE_BK + kc) = v;
-            }
-            uint4 av = make_uint4(0, 0, 0, 0);
-            if (row_ok && k0 + kq < d) av = *(const uint4*)(X + trow * d + k0 + kq);
-            __syncthreads();
-            const bf16x8 a = __builtin_bit_cast(bf16x8, av);
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                if (j < NT) {
-                    const uint4 bv = *(const uint4*)(Wst + (j * 16 + row) * ROUTE_BK + kq);
-                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        a, __builtin_bit_cast(bf16x8, bv), acc[j], 0, 0, 0);
-                }
-            }
-            __syncthreads();
-        }
-        // C fragment: lane holds rows 4*(lane/16)+i, column lane%16
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            if (j < NT) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int r = wave * 16 + (lane >> 4) * 4 + i;
-                    S[r * ldS + j * 16 + (lane & 15)] = acc[j][i];
-                }
-            }
-        }
-        __syncthreads();
-    } else if (MODE == MODE_F32) {
-        const float* X = (const float*)xv;
-        const float* W = (const float*)wv;
+    if (MODE == MODE_F32) {
         for (int c = tid; c < ROUTE_TOKENS * E; c += ROUTE_THREADS) {
             const int r = c % ROUTE_TOKENS, e = c / ROUTE_TOKENS;
             float a = 0.f;
@@ -146,55 +211,51 @@ __global__ __launch_bounds__(ROUTE_THREADS) void route_kernel(
             }
             S[r * ldS + e] = a;
         }
-        __syncthreads();
     } else {
         for (int c = tid; c < nt * E; c += ROUTE_THREADS) {
             const int r = c / E, e = c % E;
             S[r * ldS + e] = logits[(t0 + r) * E + e];
         }
-        __syncthreads();
     }
-
-    if (MODE != MODE_LOGITS_IN) {
-        for (int c = tid; c < nt * E; c += ROUTE_THREADS) {
-            const int r = c / E, e = c % E;
-            float v = S[r * ldS + e];
-            if (bias) v += bias[e];
-            S[r * ldS + e] = v;
-            if (logits) logits[(t0 + r) * E + e] = v;
-        }
-        __syncthreads();
-    }
-
-    if (tid < nt) {
-        const int64_t t = t0 + tid;
-        topk_row<KM>(S + tid * ldS, E, k, renorm != 0, idx + t * k, gate + t * k);
-    }
+    __syncthreads();
+    finish_tokens<KM>(S, ldS, nt, t0, E, k, renorm, bias, MODE == MODE_F32, logits, idx, gate);
 }
 
-template <int MODE>
-int launch_mode(const void* x, const void* w, const float* bias, int64_t T, int d, int E, int k,
-                int renorm, float* logits, int32_t* idx, float* gate, hipStream_t s) {
+template <int KM>
+int launch_km(const void* x, int dtype, const void* w, const float* bias, int64_t T, int d,
+              int E, int k, int flags, float* logits, int32_t* idx, float* gate, hipStream_t s) {
+    const int renorm = (flags & MOE_RENORM) ? 1 : 0;
     const int E_pad = (E + 15) & ~15;
-    size_t lds = (size_t)ROUTE_TOKENS * (E_pad + 1) * sizeof(float);
-    if (MODE == MODE_BF16) lds += (size_t)E_pad * ROUTE_BK * sizeof(bf16_t);
-    const dim3 grid((unsigned)ceil_div(T, ROUTE_TOKENS));
-    const dim3 block(ROUTE_THREADS);
-#define MOE_ROUTE_LAUNCH(KM)                                                                    \
+    if (!(flags & MOE_LOGITS_IN) && dtype == MOE_BF16) {
+        const int rt = E_pad <= 64 ? 4 : (E_pad <= 128 ? 2 : 1);
+        const size_t lds = (size_t)4 * 16 * rt * (E_pad + 1) * sizeof(float);
+        const dim3 grid((unsigned)ceil_div(T, 16 * rt)), block(RB_THREADS);
+#define MOE_RB_LAUNCH(RT, NTM)                                                                  \
     do {                                                                                        \
         if (lds > 65536 &&                                                                      \
-            hipFuncSetAttribute((const void*)route_kernel<MODE, KM>,                            \
+            hipFuncSetAttribute((const void*)route_bf16_kernel<RT, NTM, KM>,                    \
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=        \
                 hipSuccess)                                                                     \
             return MOE_ERR_DEVICE;                                                              \
-        hipLaunchKernelGGL((route_kernel<MODE, KM>), grid, block, lds, s, x, w, bias, T, d, E,  \
-                           k, renorm, logits, idx, gate);                                       \
+        hipLaunchKernelGGL((route_bf16_kernel<RT, NTM, KM>), grid, block, lds, s,               \
+                           (const bf16_t*)x, (const bf16_t*)w, bias, T, d, E, k, renorm,        \
+                           logits, idx, gate);                                                  \
     } while (0)
-    if (k <= 2) MOE_ROUTE_LAUNCH(2);
-    else if (k <= 4) MOE_ROUTE_LAUNCH(4);
-    else if (k <= 8) MOE_ROUTE_LAUNCH(8);
-    else MOE_ROUTE_LAUNCH(16);
-#undef MOE_ROUTE_LAUNCH
+        if (rt == 4) MOE_RB_LAUNCH(4, 4);
+        else if (rt == 2) MOE_RB_LAUNCH(2, 8);
+        else MOE_RB_LAUNCH(1, 16);
+#undef MOE_RB_LAUNCH
+        return launch_status();
+    }
+    const size_t lds = (size_t)ROUTE_TOKENS * (E_pad + 1) * sizeof(float);
+    const dim3 grid((unsigned)ceil_div(T, ROUTE_TOKENS)), block(ROUTE_THREADS);
+    if (flags & MOE_LOGITS_IN)
+        hipLaunchKernelGGL((route_simple_kernel<MODE_LOGITS_IN, KM>), grid, block, lds, s, nullptr,
+                           nullptr, nullptr, T, d, E, k, renorm, logits, idx, gate);
+    else
+        hipLaunchKernelGGL((route_simple_kernel<MODE_F32, KM>), grid, block, lds, s,
+                           (const float*)x, (const float*)w, bias, T, d, E, k, renorm, logits,
+                           idx, gate);
     return launch_status();
 }
 
@@ -204,13 +265,10 @@ int launch_route_topk(const void* x, int dtype, const void* w, const float* bias
                       int E, int k, int flags, float* logits, int32_t* idx, float* gate,
                       hipStream_t s) {
     if (T == 0) return MOE_OK;
-    const int renorm = (flags & MOE_RENORM) ? 1 : 0;
-    if (flags & MOE_LOGITS_IN)
-        return launch_mode<MODE_LOGITS_IN>(nullptr, nullptr, nullptr, T, d, E, k, renorm, logits,
-                                           idx, gate, s);
-    if (dtype == MOE_BF16)
-        return launch_mode<MODE_BF16>(x, w, bias, T, d, E, k, renorm, logits, idx, gate, s);
-    return launch_mode<MODE_F32>(x, w, bias, T, d, E, k, renorm, logits, idx, gate, s);
+    if (k <= 2) return launch_km<2>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, s);
+    if (k <= 4) return launch_km<4>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, s);
+    if (k <= 8) return launch_km<8>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, s);
+    return launch_km<16>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, s);
 }
 
 }  // namespace moe
