@@ -112,7 +112,7 @@ def cpu_baseline(cfg, inp_gpu, w13, w2, shared, T_full):
 
     S0 = 16
     t0 = run(S0)
-    S = int(min(T_full, max(S0, S0 * 12.0 / max(t0, 1e-6))))
+    S = int(min(T_full, max(S0, S0 * 20.0 / max(t0, 1e-6))))
     t = run(S)
     return {"value": S / t, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
             "sample": "first %d of the %d tokens of the same batch through the whole share "

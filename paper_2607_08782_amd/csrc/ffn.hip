@@ -10,9 +10,10 @@
 // loads, LDS stores and MFMA fragment reads are all 16-byte vectors.
 //
 // Kernel shape (gfx950, wave64):
-//   workgroup 256 threads = 4 waves (2 x 2), macro tile 128 rows x 256 weight
-//   rows, K step 64, LDS double buffer (2 x 55 KiB), wave tile 64 x 128 on
-//   v_mfma_f32_32x32x16_bf16 (2 x 4 accumulator tiles).
+//   workgroup 512 threads = 8 waves (4 x 2, two per SIMD), macro tile 256 rows
+//   x 256 weight rows, K step 64, LDS double buffer (2 x 72 KiB), wave tile
+//   64 x 128 on v_mfma_f32_32x32x16_bf16 (2 x 4 accumulator tiles), fragment
+//   reads software-pipelined against the MFMAs.
 //   The grid is persistent (one workgroup per CU).  Tiles are ordered
 //   (group, n-tile, m-tile) and cut into eight contiguous chunks, one per XCD
 //   (workgroups are dispatched round-robin over the XCDs), so the workgroups
@@ -23,12 +24,19 @@
 namespace moe {
 namespace {
 
-constexpr int BM = 128;          // rows per tile
+constexpr int BM = 256;          // rows per tile
 constexpr int BNW = 256;         // weight rows per tile
 constexpr int BK = 64;           // K per stage
 constexpr int LDK = BK + 8;      // LDS row stride in elements (144 B: conflict-free reads)
-constexpr int GEMM_THREADS = 256;
+constexpr int WAVES_M = 4, WAVES_N = 2;
+constexpr int GEMM_THREADS = WAVES_M * WAVES_N * 64;
+constexpr int MS = BM / WAVES_M / 32;              // 32-row accumulator tiles per wave
+constexpr int NS = BNW / WAVES_N / 32;             // 32-column accumulator tiles per wave
+constexpr int ROWS_PER_PASS = GEMM_THREADS / 8;    // rows one pass of 16-byte loads covers
+constexpr int A_PER = BM / ROWS_PER_PASS;          // 16-byte loads per thread per stage (A)
+constexpr int B_PER = BNW / ROWS_PER_PASS;         // (B)
 constexpr int NUM_XCD = 8;
+constexpr uint32_t RSRC_WORD3 = 0x00020000;        // raw buffer: 32-bit data format
 
 struct GemmArgs {
     const bf16_t* w[MOE_MAX_GROUPS];   // per-group weight matrix, rows contiguous along K
@@ -44,11 +52,27 @@ struct GemmArgs {
 };
 
 // B-tile row of the jj-th 32-wide accumulator column block of wave column wn.
+// SwiGLU tiles hold 128 gate rows then the matching 128 up rows; a wave takes
+// the same columns from both halves, so gate and up meet in its registers.
 template <bool SWIGLU>
 __device__ __forceinline__ int b_sub_row(int wn, int jj) {
-    return SWIGLU ? ((jj >> 1) * 128 + wn * 64 + (jj & 1) * 32) : (wn * 128 + jj * 32);
+    if (SWIGLU) {
+        constexpr int HW = BNW / 2 / WAVES_N;
+        return jj < NS / 2 ? wn * HW + jj * 32 : BNW / 2 + wn * HW + (jj - NS / 2) * 32;
+    }
+    return wn * (BNW / WAVES_N) + jj * 32;
 }
 
+__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// Persistent grouped NT GEMM.  Per tile: operands stream through per-tile
+// buffer descriptors (rows past the group's end fall outside the descriptor and
+// read as zero), are staged through registers into a double-buffered LDS
+// stage, and MFMA fragments are double-buffered per 16-wide K sub-step, so the
+// LDS reads of sub-step q+1 (including across the stage barrier) overlap the
+// MFMAs of sub-step q.
 template <bool SWIGLU>
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs args) {
     __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LDK];
@@ -59,7 +83,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int wm = wave % WAVES_M, wn = wave / WAVES_M;
     const int n_groups = args.n_groups;
     const int BN_OUT = SWIGLU ? BNW / 2 : BNW;      // output columns per tile
 
@@ -84,6 +108,11 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
     const int t_end = min(t_begin + chunk, total);
     const int KT = args.K / BK;
     const int K = args.K;
+    const int kc = (tid & 7) * 8;
+    const int voff = ((tid >> 3) * K + kc) * 2;
+    const int vstep = ROWS_PER_PASS * K * 2;
+    const int frag_col = (lane >> 5) * 32;
+    const int frag_row = lane & 31;
 
     for (int L = t_begin + widx; L < t_end; L += nper) {
         if (tid == 0) {
@@ -105,110 +134,115 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
         const int rows_valid = min(BM, s_off[g + 1] - row0);
         const bf16_t* __restrict__ W = args.w[g];
 
-        // per-thread global source rows: A rows (tid>>3) + 32*i, B rows (tid>>3) + 32*i
-        const int kc = (tid & 7) * 8;
-        const bf16_t* aptr[4];
-        bool aok[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = (tid >> 3) + 32 * i;
-            aok[i] = r < rows_valid;
-            aptr[i] = args.a + (int64_t)(row0 + (aok[i] ? r : 0)) * K + kc;
-        }
-        const bf16_t* bptr[8];
-        bool bok[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int r = (tid >> 3) + 32 * i;
-            int col, wrow;
-            if (SWIGLU) {
-                col = n0 + (r & 127);
-                wrow = (r < 128 ? 0 : args.up_row) + col;
-            } else {
-                col = n0 + r;
-                wrow = col;
-            }
-            bok[i] = col < args.N;
-            bptr[i] = W + (int64_t)(bok[i] ? wrow : 0) * K + kc;
-        }
+        const __amdgpu_buffer_rsrc_t arsrc = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(args.a + (int64_t)row0 * K), (short)0, rows_valid * K * 2, RSRC_WORD3);
+        const int bvalid = min(BN_OUT, args.N - n0);
+        const int bup = SWIGLU ? args.up_row + n0 : n0;
+        const __amdgpu_buffer_rsrc_t brsrc_lo = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(W + (int64_t)n0 * K), (short)0, bvalid * K * 2, RSRC_WORD3);
+        const __amdgpu_buffer_rsrc_t brsrc_hi = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(W + (int64_t)bup * K), (short)0, bvalid * K * 2, RSRC_WORD3);
 
-        uint4 ra[4], rb[8];
+        uint4 ra[A_PER], rb[B_PER];
         auto gload = [&](int kt) {
-            const int k0 = kt * BK;
+            const int so = kt * BK * 2;
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                ra[i] = aok[i] ? *(const uint4*)(aptr[i] + k0) : make_uint4(0, 0, 0, 0);
+            for (int i = 0; i < A_PER; ++i) ra[i] = buffer_load16(arsrc, voff + i * vstep, so);
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
-                rb[i] = bok[i] ? *(const uint4*)(bptr[i] + k0) : make_uint4(0, 0, 0, 0);
+            for (int i = 0; i < B_PER; ++i) {
+                if (SWIGLU && i >= B_PER / 2)
+                    rb[i] = buffer_load16(brsrc_hi, voff + (i - B_PER / 2) * vstep, so);
+                else
+                    rb[i] = buffer_load16(brsrc_lo, voff + i * vstep, so);
+            }
         };
         auto sstore = [&](int buf) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                *(uint4*)&As[buf][((tid >> 3) + 32 * i) * LDK + kc] = ra[i];
+            for (int i = 0; i < A_PER; ++i)
+                *(uint4*)&As[buf][((tid >> 3) + ROWS_PER_PASS * i) * LDK + kc] = ra[i];
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
-                *(uint4*)&Bs[buf][((tid >> 3) + 32 * i) * LDK + kc] = rb[i];
+            for (int i = 0; i < B_PER; ++i)
+                *(uint4*)&Bs[buf][((tid >> 3) + ROWS_PER_PASS * i) * LDK + kc] = rb[i];
         };
 
-        f32x16 acc[2][4];
+        f32x16 acc[MS][NS];
 #pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
+        for (int mi = 0; mi < MS; ++mi)
 #pragma unroll
-            for (int jj = 0; jj < 4; ++jj)
+            for (int jj = 0; jj < NS; ++jj)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[mi][jj][r] = 0.f;
 
+        const bf16_t* a_lds0 = &As[0][(wm * (BM / WAVES_M) + frag_row) * LDK + frag_col];
+        const bf16_t* b_lds0 = &Bs[0][frag_row * LDK + frag_col];
+        bf16x8 fa0[MS], fb0[NS], fa1[MS], fb1[NS];
+        auto read = [&](int buf, int kk, bf16x8* fa, bf16x8* fb) {
+#pragma unroll
+            for (int mi = 0; mi < MS; ++mi)
+                fa[mi] = *(const bf16x8*)(a_lds0 + buf * BM * LDK + mi * 32 * LDK + kk * 8);
+#pragma unroll
+            for (int jj = 0; jj < NS; ++jj)
+                fb[jj] = *(const bf16x8*)(b_lds0 + buf * BNW * LDK + b_sub_row<SWIGLU>(wn, jj) * LDK +
+                                          kk * 8);
+        };
+        auto mfma = [&](const bf16x8* fa, const bf16x8* fb) {
+#pragma unroll
+            for (int mi = 0; mi < MS; ++mi)
+#pragma unroll
+                for (int jj = 0; jj < NS; ++jj)
+                    acc[mi][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mi], fb[jj],
+                                                                          acc[mi][jj], 0, 0, 0);
+        };
+
+        // The K permutation inside a stage (lane half h, sub-step kk -> K offset
+        // h*32 + kk*8) is the same for A and B, so the products sum over all K.
         gload(0);
         sstore(0);
+        gload(KT > 1 ? 1 : 0);
         __syncthreads();
-        const int frag_col = (lane >> 5) * 32;
-        const int frag_row = lane & 31;
-        for (int kt = 0; kt < KT; ++kt) {
-            const int buf = kt & 1;
-            if (kt + 1 < KT) gload(kt + 1);
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                bf16x8 af[2], bfr[4];
-#pragma unroll
-                for (int mi = 0; mi < 2; ++mi)
-                    af[mi] = *(const bf16x8*)&As[buf][(wm * 64 + mi * 32 + frag_row) * LDK +
-                                                      frag_col + kk * 8];
-#pragma unroll
-                for (int jj = 0; jj < 4; ++jj)
-                    bfr[jj] = *(const bf16x8*)&Bs[buf][(b_sub_row<SWIGLU>(wn, jj) + frag_row) * LDK +
-                                                       frag_col + kk * 8];
-#pragma unroll
-                for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-                    for (int jj = 0; jj < 4; ++jj)
-                        acc[mi][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[jj],
-                                                                              acc[mi][jj], 0, 0, 0);
+        read(0, 0, fa0, fb0);
+        for (int t = 0; t < KT; ++t) {
+            const int buf = t & 1;
+            __builtin_amdgcn_iglp_opt(1);
+            read(buf, 1, fa1, fb1);
+            mfma(fa0, fb0);
+            read(buf, 2, fa0, fb0);
+            mfma(fa1, fb1);
+            read(buf, 3, fa1, fb1);
+            mfma(fa0, fb0);
+            if (t + 1 < KT) {
+                sstore(buf ^ 1);
+                __syncthreads();
+                gload(t + 2 < KT ? t + 2 : KT - 1);
+                read(buf ^ 1, 0, fa0, fb0);
             }
-            if (kt + 1 < KT) sstore(buf ^ 1);
-            __syncthreads();
+            mfma(fa1, fb1);
         }
+        __syncthreads();
 
         // epilogue: accumulator element r of a 32x32 tile sits at
         // row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
         const int col_in = lane & 31;
 #pragma unroll
-        for (int mi = 0; mi < 2; ++mi) {
+        for (int mi = 0; mi < MS; ++mi) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int row_in = wm * 64 + mi * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+                const int row_in = wm * (BM / WAVES_M) + mi * 32 + (r >> 2) * 8 + (lane >> 5) * 4 +
+                                   (r & 3);
                 if (row_in >= rows_valid) continue;
                 bf16_t* orow = args.out + (int64_t)(row0 + row_in) * args.ldo;
                 if (SWIGLU) {
+                    constexpr int HW = BNW / 2 / WAVES_N;
 #pragma unroll
-                    for (int j = 0; j < 2; ++j) {
-                        const int col = n0 + wn * 64 + j * 32 + col_in;
-                        if (col < args.N) orow[col] = f32_to_bf16(silu(acc[mi][j][r]) * acc[mi][2 + j][r]);
+                    for (int j = 0; j < NS / 2; ++j) {
+                        const int col = n0 + wn * HW + j * 32 + col_in;
+                        if (col < args.N)
+                            orow[col] = f32_to_bf16(silu(acc[mi][j][r]) * acc[mi][NS / 2 + j][r]);
                     }
                 } else {
 #pragma unroll
-                    for (int jj = 0; jj < 4; ++jj) {
-                        const int col = n0 + wn * 128 + jj * 32 + col_in;
+                    for (int jj = 0; jj < NS; ++jj) {
+                        const int col = n0 + wn * (BNW / WAVES_N) + jj * 32 + col_in;
                         if (col < args.N) orow[col] = f32_to_bf16(acc[mi][jj][r]);
                     }
                 }
