@@ -49,6 +49,8 @@ struct GemmArgs {
     int ldo;
     int up_row;                        // SWIGLU: first row of W3 inside w[s] (= f)
     int n_tiles;                       // output-column tiles per group
+    int small_rows;                    // groups with at most this many rows are left to the
+                                       // split-K streaming kernel (no tiles here)
 };
 
 // B-tile row of the jj-th 32-wide accumulator column block of wave column wn.
@@ -94,7 +96,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
         s_tstart[0] = 0;
         for (int s = 0; s < n_groups; ++s) {
             const int rows = s_off[s + 1] - s_off[s];
-            acc += (int)ceil_div(rows > 0 ? rows : 0, BM) * args.n_tiles;
+            acc += rows > args.small_rows ? (int)ceil_div(rows, BM) * args.n_tiles : 0;
             s_tstart[s + 1] = acc;
         }
     }
@@ -252,6 +254,225 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 }
 
 // ---------------------------------------------------------------------------
+// Small groups (decode-sized, at most SMALL_ROWS rows): weight streaming with
+// split-K.  Here the weights dominate the traffic (each weight byte is used by
+// a handful of rows), so the aim is to read every weight byte once, from all
+// CUs at once.  Work item = (group, 64 weight rows, K chunk, 32 rows); one
+// wave per item, MFMA fragments loaded straight from global memory through
+// buffer descriptors (no LDS, no barriers), fp32 partial sums per K chunk.  A
+// second kernel adds the chunks in a fixed order (so results are
+// deterministic) and, for the gate/up product, applies SiLU(a) * b.
+// The split factor S is derived on the device from the group sizes; both
+// kernels derive the same plan from the same inputs.
+// ---------------------------------------------------------------------------
+constexpr int SMALL_ROWS = 64;
+constexpr int ST_M = 32;                 // rows per item
+constexpr int ST_N = 64;                 // weight rows per item
+constexpr int ST_THREADS = 256;
+constexpr int ST_WAVES_PER_CU = 8;
+constexpr int SPLIT_MAX = 32;
+constexpr int PART_FACTOR = 8;           // partial capacity = PART_FACTOR x bound on small rows
+
+struct StreamArgs {
+    const bf16_t* w[MOE_MAX_GROUPS];     // per group [N][K]
+    const int32_t* offsets;
+    const bf16_t* a;                     // [rows][K]
+    float* part;                         // [S][n_small][N]
+    bf16_t* out;                         // reduce output [rows][ldo]
+    int n_groups;
+    int K;
+    int N;                               // weight rows (2f for gate/up, d for down)
+    int ldo;
+    int part_rows;                       // capacity of `part` in rows (S * n_small <= part_rows)
+    int target_items;
+};
+
+struct StreamPlan {
+    int off[MOE_MAX_GROUPS + 1];
+    int qbase[MOE_MAX_GROUPS + 1];       // compact row base of each small group
+    int istart[MOE_MAX_GROUPS + 1];      // first work item of each group
+    int n_small, S, total, n_tiles;
+};
+
+__device__ void make_stream_plan(const StreamArgs& a, StreamPlan& P, int nthreads) {
+    for (int g = threadIdx.x; g <= a.n_groups; g += nthreads) P.off[g] = a.offsets[g];
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int nt = (int)ceil_div(a.N, ST_N);
+        const int KT = a.K / 64;
+        int rows_small = 0, base = 0;
+        for (int g = 0; g < a.n_groups; ++g) {
+            const int rows = P.off[g + 1] - P.off[g];
+            P.qbase[g] = rows_small;
+            if (rows > 0 && rows <= SMALL_ROWS) {
+                rows_small += rows;
+                base += (int)ceil_div(rows, ST_M) * nt;
+            }
+        }
+        P.qbase[a.n_groups] = rows_small;
+        int S = base > 0 ? (int)ceil_div(a.target_items, base) : 1;
+        S = min(S, SPLIT_MAX);
+        S = min(S, KT);
+        if (rows_small > 0) S = min(S, a.part_rows / rows_small);
+        S = max(S, 1);
+        int acc = 0;
+        for (int g = 0; g < a.n_groups; ++g) {
+            P.istart[g] = acc;
+            const int rows = P.off[g + 1] - P.off[g];
+            if (rows > 0 && rows <= SMALL_ROWS) acc += (int)ceil_div(rows, ST_M) * nt * S;
+        }
+        P.istart[a.n_groups] = acc;
+        P.n_small = rows_small;
+        P.S = S;
+        P.total = acc;
+        P.n_tiles = nt;
+    }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(ST_THREADS) void stream_gemm_kernel(StreamArgs args) {
+    __shared__ StreamPlan P;
+    make_stream_plan(args, P, ST_THREADS);
+    if (P.total == 0) return;
+    const int lane = threadIdx.x & 63;
+    const int waves = gridDim.x * (ST_THREADS / 64);
+    // XCD-aware: the waves of one XCD walk one contiguous chunk of items
+    const int wg_per_xcd = gridDim.x / NUM_XCD;
+    const int xcd = blockIdx.x % NUM_XCD;
+    const int wave_in_xcd = (blockIdx.x / NUM_XCD) * (ST_THREADS / 64) + (threadIdx.x >> 6);
+    const int waves_per_xcd = wg_per_xcd * (ST_THREADS / 64);
+    const int chunk = (P.total + NUM_XCD - 1) / NUM_XCD;
+    const int i_begin = xcd * chunk, i_end = min(i_begin + chunk, P.total);
+    (void)waves;
+    const int K = args.K, KT = K / 64, S = P.S, nt = P.n_tiles;
+    const int kq = (lane >> 5) * 32;                 // lane half -> K offset inside a 64-wide step
+    const int r32 = lane & 31;
+
+    for (int it = i_begin + wave_in_xcd; it < i_end; it += waves_per_xcd) {
+        int lo = 0, hi = args.n_groups - 1;          // group: last g with istart[g] <= it
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (P.istart[mid] <= it) lo = mid; else hi = mid - 1;
+        }
+        const int g = lo;
+        const int rows = P.off[g + 1] - P.off[g];
+        const int mt = (int)ceil_div(rows, ST_M);
+        int local = it - P.istart[g];
+        const int m = local % mt;
+        local /= mt;
+        const int c = local % S;
+        const int n = local / S;
+        const int n0 = n * ST_N;
+        const int row0 = P.off[g] + m * ST_M;
+        const int rows_valid = min(ST_M, rows - m * ST_M);
+        const int bvalid = min(ST_N, args.N - n0);
+        const int kt0 = (int)((int64_t)c * KT / S), kt1 = (int)((int64_t)(c + 1) * KT / S);
+
+        const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(args.a + (int64_t)row0 * K), (short)0, rows_valid * K * 2, RSRC_WORD3);
+        const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(args.w[g] + (int64_t)n0 * K), (short)0, bvalid * K * 2, RSRC_WORD3);
+        const int va = (r32 * K + kq) * 2;
+        const int vb0 = (r32 * K + kq) * 2;
+        const int vb1 = ((32 + r32) * K + kq) * 2;
+
+        f32x16 acc0, acc1;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) { acc0[r] = 0.f; acc1[r] = 0.f; }
+        uint4 a_cur[4], b0_cur[4], b1_cur[4], a_nxt[4], b0_nxt[4], b1_nxt[4];
+        auto load = [&](int kt, uint4* aa, uint4* bb0, uint4* bb1) {
+            const int so = kt * 128;
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                aa[kk] = buffer_load16(ar, va + kk * 16, so);
+                bb0[kk] = buffer_load16(br, vb0 + kk * 16, so);
+                bb1[kk] = buffer_load16(br, vb1 + kk * 16, so);
+            }
+        };
+        auto step = [&](const uint4* aa, const uint4* bb0, const uint4* bb1) {
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const bf16x8 af = __builtin_bit_cast(bf16x8, aa[kk]);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, __builtin_bit_cast(bf16x8, bb0[kk]),
+                                                               acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, __builtin_bit_cast(bf16x8, bb1[kk]),
+                                                               acc1, 0, 0, 0);
+            }
+        };
+        load(kt0, a_cur, b0_cur, b1_cur);
+        int kt = kt0;
+        for (; kt + 2 <= kt1; kt += 2) {
+            load(kt + 1, a_nxt, b0_nxt, b1_nxt);
+            step(a_cur, b0_cur, b1_cur);
+            if (kt + 2 < kt1) load(kt + 2, a_cur, b0_cur, b1_cur);
+            step(a_nxt, b0_nxt, b1_nxt);
+        }
+        if (kt < kt1) step(a_cur, b0_cur, b1_cur);
+
+        // partial store: element r of a 32x32 tile is row 8*(r/4) + 4*(lane/32) + r%4, col lane%32
+        float* prow = args.part + ((int64_t)c * P.n_small + P.qbase[g] + m * ST_M) * args.N + n0;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+            if (row >= rows_valid) continue;
+            float* pr = prow + (int64_t)row * args.N;
+            if (r32 < bvalid) pr[r32] = acc0[r];
+            if (32 + r32 < bvalid) pr[32 + r32] = acc1[r];
+        }
+    }
+}
+
+// Fixed-order sum of the K chunks; SWIGLU: out[p][j] = SiLU(sum gate_j) * sum up_j
+// with gate in partial columns [0, N/2) and up in [N/2, N).
+template <bool SWIGLU>
+__global__ __launch_bounds__(ST_THREADS) void split_reduce_kernel(StreamArgs args) {
+    __shared__ StreamPlan P;
+    make_stream_plan(args, P, ST_THREADS);
+    const int n_small = P.n_small;
+    if (n_small == 0) return;
+    const int S = P.S;
+    const int cols = SWIGLU ? args.N / 2 : args.N;
+    const int chunks = cols / 8;
+    const int64_t total = (int64_t)n_small * chunks;
+    for (int64_t i = (int64_t)blockIdx.x * ST_THREADS + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * ST_THREADS) {
+        const int q = (int)(i / chunks);
+        const int c8 = (int)(i - (int64_t)q * chunks) * 8;
+        int lo = 0, hi = args.n_groups - 1;          // group: last g with qbase[g] <= q
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (P.qbase[mid] <= q) lo = mid; else hi = mid - 1;
+        }
+        // skip forward over groups that hold no small rows (qbase does not advance there)
+        const int g = lo;                            // groups without small rows share qbase
+        const int p = P.off[g] + (q - P.qbase[g]);
+        float x[8], y[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) { x[e] = 0.f; y[e] = 0.f; }
+        for (int c = 0; c < S; ++c) {
+            const float* pr = args.part + ((int64_t)c * n_small + q) * args.N + c8;
+            const float4 v0 = *(const float4*)pr, v1 = *(const float4*)(pr + 4);
+            x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
+            x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
+            if (SWIGLU) {
+                const float4 u0 = *(const float4*)(pr + cols), u1 = *(const float4*)(pr + cols + 4);
+                y[0] += u0.x; y[1] += u0.y; y[2] += u0.z; y[3] += u0.w;
+                y[4] += u1.x; y[5] += u1.y; y[6] += u1.z; y[7] += u1.w;
+            }
+        }
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = SWIGLU ? silu(x[e]) * y[e] : x[e];
+        uint4 pk;
+        pk.x = pack_bf16x2(o[0], o[1]);
+        pk.y = pack_bf16x2(o[2], o[3]);
+        pk.z = pack_bf16x2(o[4], o[5]);
+        pk.w = pack_bf16x2(o[6], o[7]);
+        *(uint4*)(args.out + (int64_t)p * args.ldo + c8) = pk;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // fp32 path: plain FMA loops, one thread per output element.
 // ---------------------------------------------------------------------------
 struct PtrTable {
@@ -323,10 +544,19 @@ int num_cus() {
 
 }  // namespace
 
+static int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+static int64_t small_rows_bound(int64_t cap_rows, int n_groups) {
+    const int64_t b = (int64_t)n_groups * SMALL_ROWS;
+    return cap_rows < b ? cap_rows : b;
+}
+
 size_t grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_groups) {
-    (void)d; (void)n_groups;
-    const size_t esize = dtype == MOE_BF16 ? 2 : 4;
-    return (size_t)cap_rows * (size_t)f * esize + 256;
+    if (dtype != MOE_BF16) return (size_t)cap_rows * (size_t)f * 4 + 256;
+    const int64_t h = align256(cap_rows * (int64_t)f * 2);
+    const int64_t ncols = 2 * (int64_t)f > d ? 2 * (int64_t)f : d;
+    const int64_t part = (int64_t)PART_FACTOR * small_rows_bound(cap_rows, n_groups) * ncols * 4;
+    return (size_t)(h + part + 256);
 }
 
 int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, int n_groups,
@@ -349,8 +579,18 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
                            offsets, n_groups, t2, d, f, (float*)y_perm);
         return launch_status();
     }
-    const int grid = (num_cus() / NUM_XCD) * NUM_XCD;
+    const int cus = num_cus();
+    const int grid = (cus / NUM_XCD) * NUM_XCD;
     bf16_t* h = (bf16_t*)ws;
+    float* part = (float*)((char*)ws + align256(cap_rows * (int64_t)f * 2));
+    const int64_t rmax = small_rows_bound(cap_rows, n_groups);
+    const int sgrid = ((cus * ST_WAVES_PER_CU / (ST_THREADS / 64)) / NUM_XCD) * NUM_XCD;
+    const int64_t red_items = rmax * ((f > d ? f : d) / 8);
+    int rgrid = (int)ceil_div(red_items, ST_THREADS);
+    if (rgrid > 4096) rgrid = 4096;
+    if (rgrid < 1) rgrid = 1;
+
+    // gate/up product: big groups on the tiled kernel, small groups streamed
     GemmArgs a1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) a1.w[i] = i < n_groups ? (const bf16_t*)w13[i] : nullptr;
     a1.offsets = offsets;
@@ -362,7 +602,24 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a1.ldo = f;
     a1.up_row = f;
     a1.n_tiles = (int)ceil_div(f, BNW / 2);
+    a1.small_rows = SMALL_ROWS;
     hipLaunchKernelGGL(grouped_gemm_kernel<true>, dim3(grid), dim3(GEMM_THREADS), 0, s, a1);
+    StreamArgs s1;
+    for (int i = 0; i < MOE_MAX_GROUPS; ++i) s1.w[i] = a1.w[i];
+    s1.offsets = offsets;
+    s1.a = (const bf16_t*)x_perm;
+    s1.part = part;
+    s1.out = h;
+    s1.n_groups = n_groups;
+    s1.K = d;
+    s1.N = 2 * f;
+    s1.ldo = f;
+    s1.part_rows = (int)(PART_FACTOR * rmax);
+    s1.target_items = 2 * cus * ST_WAVES_PER_CU;
+    hipLaunchKernelGGL(stream_gemm_kernel, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
+    hipLaunchKernelGGL(split_reduce_kernel<true>, dim3(rgrid), dim3(ST_THREADS), 0, s, s1);
+
+    // down product
     GemmArgs a2 = a1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) a2.w[i] = i < n_groups ? (const bf16_t*)w2[i] : nullptr;
     a2.a = h;
@@ -373,6 +630,15 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a2.up_row = 0;
     a2.n_tiles = (int)ceil_div(d, BNW);
     hipLaunchKernelGGL(grouped_gemm_kernel<false>, dim3(grid), dim3(GEMM_THREADS), 0, s, a2);
+    StreamArgs s2 = s1;
+    for (int i = 0; i < MOE_MAX_GROUPS; ++i) s2.w[i] = a2.w[i];
+    s2.a = h;
+    s2.out = (bf16_t*)y_perm;
+    s2.K = f;
+    s2.N = d;
+    s2.ldo = d;
+    hipLaunchKernelGGL(stream_gemm_kernel, dim3(sgrid), dim3(ST_THREADS), 0, s, s2);
+    hipLaunchKernelGGL(split_reduce_kernel<false>, dim3(rgrid), dim3(ST_THREADS), 0, s, s2);
     return launch_status();
 }
 

@@ -196,3 +196,30 @@ def test_doubling_w2_doubles_expert_outputs_exactly():
     share.run()
     torch.cuda.synchronize()
     assert torch.equal(share.y_perm[:N], 2 * y1[:N])
+
+
+def test_group_sizes_around_the_streaming_threshold():
+    """Groups of 64 and fewer rows take the split-K streaming kernels, larger ones the
+    tiled kernel; sizes 64 / 65 / 1 / 0 / 200 / 33 check both sides of the boundary."""
+    sizes = [64, 65, 1, 0, 200, 33]
+    E = len(sizes)
+    cfg = synth.custom_config(d=256, E=E, k=1, f=192, G=1)
+    T = sum(sizes)
+    owner = np.repeat(np.arange(E), sizes)
+    np.random.default_rng(5).shuffle(owner)
+    L = np.zeros((T, E), np.float32)
+    L[np.arange(T), owner] = 1.0
+    inp, share = _share(cfg, T)
+    share.run(logits_in=torch.from_numpy(L).cuda())
+    torch.cuda.synchronize()
+    go = share.perm["group_offsets"].cpu().numpy()
+    assert np.diff(go).tolist() == sizes
+    X = np32(inp.X)
+    idx, gate = oracle.topk(L, 1)
+    pm = oracle.permute(X, idx, gate, E, inp.placement, 0)
+    for s in range(E):
+        if sizes[s]:
+            w13 = np32(share.weights.w13[s])
+            w2 = np32(share.weights.w2[s])
+            ref = oracle.expert_ffn(pm["x_perm"][go[s]:go[s + 1]], w13, w2)
+            close(np32(share.y_perm[go[s]:go[s + 1]]), ref, OUT_TOL["bf16"], "group %d" % s)
