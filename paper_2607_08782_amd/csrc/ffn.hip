@@ -257,21 +257,24 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 // Small groups (decode-sized, at most SMALL_ROWS rows): weight streaming with
 // split-K.  Here the weights dominate the traffic (each weight byte is used by
 // a handful of rows), so the aim is to read every weight byte once, from all
-// CUs at once.  Work item = (group, 64 weight rows, K chunk, 32 rows); one
-// wave per item, MFMA fragments loaded straight from global memory through
-// buffer descriptors (no LDS, no barriers), fp32 partial sums per K chunk.  A
-// second kernel adds the chunks in a fixed order (so results are
-// deterministic) and, for the gate/up product, applies SiLU(a) * b.
+// CUs at once.  Work item = (group, 256 weight rows, K chunk, 32 rows); one
+// workgroup per item, fp32 partial sums per K chunk.  A second kernel adds the
+// chunks in a fixed order (so results are deterministic) and, for the gate/up
+// product, applies SiLU(a) * b.
 // The split factor S is derived on the device from the group sizes; both
 // kernels derive the same plan from the same inputs.
 // ---------------------------------------------------------------------------
 constexpr int SMALL_ROWS = 64;
 constexpr int ST_M = 32;                 // rows per item
-constexpr int ST_N = 64;                 // weight rows per item
+constexpr int ST_N = 256;                // weight rows per item (64 per wave)
 constexpr int ST_THREADS = 256;
-constexpr int ST_WAVES_PER_CU = 8;
+constexpr int ST_WG_PER_CU = 3;
+constexpr int ST_RING = 1;               // K steps of loads in flight beyond the one in LDS
+constexpr int ST_A_PER = ST_M * 64 / 8 / ST_THREADS;   // 16-byte loads per thread per K step
+constexpr int ST_B_PER = ST_N * 64 / 8 / ST_THREADS;
 constexpr int SPLIT_MAX = 32;
 constexpr int PART_FACTOR = 8;           // partial capacity = PART_FACTOR x bound on small rows
+static_assert(ST_A_PER == 1 && ST_B_PER == 8, "streaming tile");
 
 struct StreamArgs {
     const bf16_t* w[MOE_MAX_GROUPS];     // per group [N][K]
@@ -330,39 +333,49 @@ __device__ void make_stream_plan(const StreamArgs& a, StreamPlan& P, int nthread
     __syncthreads();
 }
 
-__global__ __launch_bounds__(ST_THREADS) void stream_gemm_kernel(StreamArgs args) {
+// One workgroup per item (32 rows x 256 weight rows x one K chunk); each wave
+// takes 64 of the weight rows.  Loads are coalesced (8 lanes read one
+// 128-byte row segment) and run ST_RING K steps ahead in registers; one LDS
+// stage holds the step being multiplied.
+__global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(StreamArgs args) {
+    __shared__ __attribute__((aligned(16))) bf16_t As[ST_M * LDK];
+    __shared__ __attribute__((aligned(16))) bf16_t Bs[ST_N * LDK];
     __shared__ StreamPlan P;
+    __shared__ int s_item[4];
     make_stream_plan(args, P, ST_THREADS);
     if (P.total == 0) return;
-    const int lane = threadIdx.x & 63;
-    const int waves = gridDim.x * (ST_THREADS / 64);
-    // XCD-aware: the waves of one XCD walk one contiguous chunk of items
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wg_per_xcd = gridDim.x / NUM_XCD;
     const int xcd = blockIdx.x % NUM_XCD;
-    const int wave_in_xcd = (blockIdx.x / NUM_XCD) * (ST_THREADS / 64) + (threadIdx.x >> 6);
-    const int waves_per_xcd = wg_per_xcd * (ST_THREADS / 64);
+    const int widx = blockIdx.x / NUM_XCD;
     const int chunk = (P.total + NUM_XCD - 1) / NUM_XCD;
     const int i_begin = xcd * chunk, i_end = min(i_begin + chunk, P.total);
-    (void)waves;
-    const int K = args.K, KT = K / 64, S = P.S, nt = P.n_tiles;
-    const int kq = (lane >> 5) * 32;                 // lane half -> K offset inside a 64-wide step
-    const int r32 = lane & 31;
+    const int K = args.K, KT = K / 64, S = P.S;
+    const int kc = (tid & 7) * 8;
+    const int lrow = tid >> 3;                          // 0..31: row of this thread's loads
+    const int voff = (lrow * K + kc) * 2;
+    const int vstep = 32 * K * 2;
+    const int frag_col = (lane >> 5) * 32, frag_row = lane & 31;
 
-    for (int it = i_begin + wave_in_xcd; it < i_end; it += waves_per_xcd) {
-        int lo = 0, hi = args.n_groups - 1;          // group: last g with istart[g] <= it
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (P.istart[mid] <= it) lo = mid; else hi = mid - 1;
+    for (int it = i_begin + widx; it < i_end; it += wg_per_xcd) {
+        if (tid == 0) {
+            int lo = 0, hi = args.n_groups - 1;      // group: last g with istart[g] <= it
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (P.istart[mid] <= it) lo = mid; else hi = mid - 1;
+            }
+            s_item[0] = lo;
+            s_item[1] = it - P.istart[lo];
         }
-        const int g = lo;
+        __syncthreads();
+        const int g = s_item[0];
+        int local = s_item[1];
         const int rows = P.off[g + 1] - P.off[g];
         const int mt = (int)ceil_div(rows, ST_M);
-        int local = it - P.istart[g];
         const int m = local % mt;
         local /= mt;
         const int c = local % S;
-        const int n = local / S;
-        const int n0 = n * ST_N;
+        const int n0 = (local / S) * ST_N;
         const int row0 = P.off[g] + m * ST_M;
         const int rows_valid = min(ST_M, rows - m * ST_M);
         const int bvalid = min(ST_N, args.N - n0);
@@ -372,53 +385,58 @@ __global__ __launch_bounds__(ST_THREADS) void stream_gemm_kernel(StreamArgs args
             (void*)(args.a + (int64_t)row0 * K), (short)0, rows_valid * K * 2, RSRC_WORD3);
         const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
             (void*)(args.w[g] + (int64_t)n0 * K), (short)0, bvalid * K * 2, RSRC_WORD3);
-        const int va = (r32 * K + kq) * 2;
-        const int vb0 = (r32 * K + kq) * 2;
-        const int vb1 = ((32 + r32) * K + kq) * 2;
 
+        uint4 ring_a[ST_RING + 1], ring_b[ST_RING + 1][ST_B_PER];
+        auto load = [&](int kt, uint4& ra, uint4* rb) {
+            const int so = kt * 128;
+            ra = buffer_load16(ar, voff, so);
+#pragma unroll
+            for (int i = 0; i < ST_B_PER; ++i) rb[i] = buffer_load16(br, voff + i * vstep, so);
+        };
         f32x16 acc0, acc1;
 #pragma unroll
         for (int r = 0; r < 16; ++r) { acc0[r] = 0.f; acc1[r] = 0.f; }
-        uint4 a_cur[4], b0_cur[4], b1_cur[4], a_nxt[4], b0_nxt[4], b1_nxt[4];
-        auto load = [&](int kt, uint4* aa, uint4* bb0, uint4* bb1) {
-            const int so = kt * 128;
+        const int nsteps = kt1 - kt0;
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                aa[kk] = buffer_load16(ar, va + kk * 16, so);
-                bb0[kk] = buffer_load16(br, vb0 + kk * 16, so);
-                bb1[kk] = buffer_load16(br, vb1 + kk * 16, so);
-            }
-        };
-        auto step = [&](const uint4* aa, const uint4* bb0, const uint4* bb1) {
+        for (int u = 0; u <= ST_RING; ++u)
+            if (u < nsteps) load(kt0 + u, ring_a[u], ring_b[u]);
+        for (int t0 = 0; t0 < nsteps; t0 += ST_RING + 1) {
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                const bf16x8 af = __builtin_bit_cast(bf16x8, aa[kk]);
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, __builtin_bit_cast(bf16x8, bb0[kk]),
-                                                               acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, __builtin_bit_cast(bf16x8, bb1[kk]),
-                                                               acc1, 0, 0, 0);
+            for (int u = 0; u <= ST_RING; ++u) {
+                const int t = t0 + u;
+                if (t < nsteps) {
+                    __syncthreads();                 // previous step's fragment reads are done
+                    *(uint4*)&As[lrow * LDK + kc] = ring_a[u];
+#pragma unroll
+                    for (int i = 0; i < ST_B_PER; ++i)
+                        *(uint4*)&Bs[(lrow + 32 * i) * LDK + kc] = ring_b[u][i];
+                    __syncthreads();
+                    if (t + ST_RING + 1 < nsteps) load(kt0 + t + ST_RING + 1, ring_a[u], ring_b[u]);
+#pragma unroll
+                    for (int kk = 0; kk < 4; ++kk) {
+                        const bf16x8 af = *(const bf16x8*)&As[frag_row * LDK + frag_col + kk * 8];
+                        const bf16x8 b0 = *(const bf16x8*)&Bs[(wave * 64 + frag_row) * LDK + frag_col + kk * 8];
+                        const bf16x8 b1 = *(const bf16x8*)&Bs[(wave * 64 + 32 + frag_row) * LDK + frag_col + kk * 8];
+                        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, b0, acc0, 0, 0, 0);
+                        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, b1, acc1, 0, 0, 0);
+                    }
+                }
             }
-        };
-        load(kt0, a_cur, b0_cur, b1_cur);
-        int kt = kt0;
-        for (; kt + 2 <= kt1; kt += 2) {
-            load(kt + 1, a_nxt, b0_nxt, b1_nxt);
-            step(a_cur, b0_cur, b1_cur);
-            if (kt + 2 < kt1) load(kt + 2, a_cur, b0_cur, b1_cur);
-            step(a_nxt, b0_nxt, b1_nxt);
         }
-        if (kt < kt1) step(a_cur, b0_cur, b1_cur);
 
         // partial store: element r of a 32x32 tile is row 8*(r/4) + 4*(lane/32) + r%4, col lane%32
-        float* prow = args.part + ((int64_t)c * P.n_small + P.qbase[g] + m * ST_M) * args.N + n0;
+        float* prow = args.part + ((int64_t)c * P.n_small + P.qbase[g] + m * ST_M) * args.N + n0 +
+                      wave * 64;
+        const int cw = bvalid - wave * 64;           // valid columns of this wave
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int row = (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
             if (row >= rows_valid) continue;
             float* pr = prow + (int64_t)row * args.N;
-            if (r32 < bvalid) pr[r32] = acc0[r];
-            if (32 + r32 < bvalid) pr[32 + r32] = acc1[r];
+            if (frag_row < cw) pr[frag_row] = acc0[r];
+            if (32 + frag_row < cw) pr[32 + frag_row] = acc1[r];
         }
+        __syncthreads();                             // s_item and LDS reuse by the next item
     }
 }
 
@@ -584,7 +602,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     bf16_t* h = (bf16_t*)ws;
     float* part = (float*)((char*)ws + align256(cap_rows * (int64_t)f * 2));
     const int64_t rmax = small_rows_bound(cap_rows, n_groups);
-    const int sgrid = ((cus * ST_WAVES_PER_CU / (ST_THREADS / 64)) / NUM_XCD) * NUM_XCD;
+    const int sgrid = ((cus * ST_WG_PER_CU) / NUM_XCD) * NUM_XCD;
     const int64_t red_items = rmax * ((f > d ? f : d) / 8);
     int rgrid = (int)ceil_div(red_items, ST_THREADS);
     if (rgrid > 4096) rgrid = 4096;
@@ -615,7 +633,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s1.N = 2 * f;
     s1.ldo = f;
     s1.part_rows = (int)(PART_FACTOR * rmax);
-    s1.target_items = 2 * cus * ST_WAVES_PER_CU;
+    s1.target_items = 2 * cus * ST_WG_PER_CU;
     hipLaunchKernelGGL(stream_gemm_kernel, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
     hipLaunchKernelGGL(split_reduce_kernel<true>, dim3(rgrid), dim3(ST_THREADS), 0, s, s1);
 
