@@ -39,48 +39,83 @@ def make_share(cfg, T, seed=0, weights=None):
     return inp, share, (w13, w2, shared)
 
 
-def run_phases(share, ev):
-    """The five C-ABI calls of LayerShare.run, with an event after each."""
-    ev[0].record()
-    share.route()
-    ev[1].record()
-    moe.moe_expert_histogram(share.topk_idx, share.E, counts=share.counts, coact=share.coact)
-    ev[2].record()
-    moe.moe_permute(share.X, share.topk_idx, share.topk_gate, share.counts, share.placement,
-                    share.dev, E=share.E, cap_rows=share.cap_rows, out=share.perm, ws=share.ws_perm)
-    ev[3].record()
-    if share.weights is not None:
-        moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
-                            cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
-    ev[4].record()
-    if share.shared_weights is not None:
-        moe.moe_grouped_ffn(share.X, share.shared_offsets, share.shared_weights, cap_rows=share.T,
-                            y_perm=share.y_shared, ws=share.ws_shared)
-    ev[5].record()
-    moe.moe_combine(share.y_perm, share.perm["token_row"], share.topk_gate, share.y_shared,
-                    T=share.T, d=share.d, y=share.y)
-    ev[6].record()
+def phase_calls(share):
+    """The calls of LayerShare.run, one callable per phase."""
+    def route():
+        share.route()
+
+    def histogram():
+        moe.moe_expert_histogram(share.topk_idx, share.E, counts=share.counts, coact=share.coact)
+
+    def permute():
+        moe.moe_permute(share.X, share.topk_idx, share.topk_gate, share.counts, share.placement,
+                        share.dev, E=share.E, cap_rows=share.cap_rows, out=share.perm,
+                        ws=share.ws_perm)
+
+    def grouped_ffn():
+        if share.weights is not None:
+            moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
+                                cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
+
+    def shared_ffn():
+        if share.shared_weights is not None:
+            moe.moe_grouped_ffn(share.X, share.shared_offsets, share.shared_weights,
+                                cap_rows=share.T, y_perm=share.y_shared, ws=share.ws_shared)
+
+    def combine():
+        moe.moe_combine(share.y_perm, share.perm["token_row"], share.topk_gate, share.y_shared,
+                        T=share.T, d=share.d, y=share.y)
+
+    return dict(route_topk=route, histogram=histogram, permute=permute, grouped_ffn=grouped_ffn,
+                shared_ffn=shared_ffn, combine=combine)
+
+
+def capture(fn):
+    """One HIP graph of `fn`'s launches (captured on torch's capture stream)."""
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def time_replays(g, steps, warmup):
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
 
 
 def time_share(share, steps, warmup):
+    """Step time from HIP-graph replays of the whole share.  Per-phase GPU time
+    from an eager timed loop with an event after every call on the stream the
+    calls are enqueued on (torch's current stream); the eager step time is
+    reported beside the graph one."""
+    calls = phase_calls(share)
     for _ in range(warmup):
         share.run()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(PHASES) + 1)]
+           for _ in range(steps)]
     for i in range(steps):
-        run_phases(share, evs[i])
+        evs[i][0].record()
+        for j, name in enumerate(PHASES):
+            calls[name]()
+            evs[i][j + 1].record()
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    per_phase = np.zeros(len(PHASES))
-    total = 0.0
-    for ev in evs:
-        for j in range(len(PHASES)):
-            per_phase[j] += ev[j].elapsed_time(ev[j + 1])
-    total = evs[0][0].elapsed_time(evs[-1][6])
-    per_phase /= steps
-    return total / steps, dict(zip(PHASES, per_phase)), wall
+    phases = {name: sum(ev[j].elapsed_time(ev[j + 1]) for ev in evs) / steps
+              for j, name in enumerate(PHASES)}
+    eager_ms = evs[0][0].elapsed_time(evs[-1][-1]) / steps
+    ms = time_replays(capture(share.run), steps, warmup)
+    share.run()
+    torch.cuda.synchronize()
+    return ms, phases, eager_ms
 
 
 def ffn_work(share, cfg):
@@ -142,7 +177,7 @@ def main():
     T = cfg.T(regime)
 
     inp, share, weights = make_share(cfg, T)
-    ms, phases, wall = time_share(share, args.steps, args.warmup)
+    ms, phases, eager_ms = time_share(share, args.steps, args.warmup)
     N, active, flops, fbytes, sizes = ffn_work(share, cfg)
     t_ffn = phases["grouped_ffn"] * 1e-3
     achieved = flops / t_ffn
@@ -154,6 +189,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms,
+        "eager_ms_per_step": eager_ms,
+        "launch": "each step is one HIP graph replay of the five C-ABI calls",
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -178,11 +215,12 @@ def main():
     if args.decode and args.decode in dict(cfg.regimes) and args.decode != regime:
         Td = cfg.T(args.decode)
         dinp, dshare, _ = make_share(cfg, Td, weights=weights)
-        dms, dph, _ = time_share(dshare, max(args.steps * 5, 50), args.warmup * 2)
+        dms, dph, deager = time_share(dshare, max(args.steps * 5, 50), args.warmup * 2)
         dN, dact, dfl, dby, dsizes = ffn_work(dshare, cfg)
         dt = dph["grouped_ffn"] * 1e-3
         out["decode"] = {
-            "T": Td, "tokens_per_s": Td / (dms * 1e-3), "ms_per_step": dms, "rows_here": dN,
+            "T": Td, "tokens_per_s": Td / (dms * 1e-3), "ms_per_step": dms,
+            "eager_ms_per_step": deager, "rows_here": dN,
             "active_experts": dact,
             "roofline": {"kernel": "moe_grouped_ffn", "bound": "hbm",
                          "achieved": dby / dt / 1e9, "peak": PEAK_HBM_BYTES / 1e9, "unit": "GB/s",

@@ -80,12 +80,21 @@ const char* moe_status_string(int status);
  * logits    device [T][E] float: output, or input with MOE_LOGITS_IN; nullable
  *           otherwise (then the scores are not stored)
  * topk_idx  device [T][k] int32 output;  topk_gate  device [T][k] float output
+ * ws        device workspace of moe_route_topk_ws_bytes(dtype, T, d, E, flags)
+ *           bytes, 256-byte aligned; may be NULL when that size is 0.  (Short
+ *           batches split the gate GEMM over K across workgroups and keep the
+ *           per-chunk fp32 partial scores here; they are summed in chunk order.)
  * Requires 1 <= E <= MOE_MAX_E, 1 <= k <= min(E, MOE_MAX_K), T >= 0,
  * d >= 1 and, for MOE_BF16, d % 8 == 0.  Logits must be finite.
+ * Scores are deterministic: the same inputs give bitwise the same outputs.
  */
 int moe_route_topk(const void* x, int dtype, const void* w_router, const float* bias,
                    int64_t T, int d, int E, int k, int flags,
-                   float* logits, int32_t* topk_idx, float* topk_gate, void* stream);
+                   float* logits, int32_t* topk_idx, float* topk_gate,
+                   void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes moe_route_topk needs (0 = none). */
+size_t moe_route_topk_ws_bytes(int dtype, int64_t T, int d, int E, int flags);
 
 /*
  * moe_expert_histogram -- per-expert workload counts (Sec. VI-A: W_{j,i}

@@ -26,9 +26,14 @@ const char* moe_status_string(int status) {
     }
 }
 
+size_t moe_route_topk_ws_bytes(int dtype, int64_t T, int d, int E, int flags) {
+    if (T < 0 || d < 0 || E < 1) return 0;
+    return route_ws_bytes(dtype, T, d, E, flags);
+}
+
 int moe_route_topk(const void* x, int dtype, const void* w_router, const float* bias, int64_t T,
                    int d, int E, int k, int flags, float* logits, int32_t* topk_idx,
-                   float* topk_gate, void* stream) {
+                   float* topk_gate, void* ws, size_t ws_bytes, void* stream) {
     if (T < 0 || E < 1 || E > MOE_MAX_E || k < 1 || k > MOE_MAX_K || k > E) return MOE_ERR_ARG;
     if (flags & ~(MOE_RENORM | MOE_LOGITS_IN)) return MOE_ERR_ARG;
     if (T > (int64_t)0x7fffffff * 16) return MOE_ERR_ARG;
@@ -44,8 +49,10 @@ int moe_route_topk(const void* x, int dtype, const void* w_router, const float* 
             if (!aligned16(x) || !aligned16(w_router)) return MOE_ERR_ARG;
         }
     }
+    const size_t need = route_ws_bytes(dtype, T, d, E, flags);
+    if (need > 0 && (!ws || ws_bytes < need || ((uintptr_t)ws & 255u))) return MOE_ERR_SHAPE;
     return launch_route_topk(x, dtype, w_router, bias, T, d, E, k, flags, logits, topk_idx,
-                             topk_gate, (hipStream_t)stream);
+                             topk_gate, ws, (hipStream_t)stream);
 }
 
 int moe_expert_histogram(const int32_t* topk_idx, int64_t T, int k, int E, int32_t* counts,

@@ -48,8 +48,9 @@ inline int launch_status() {
 // Internal launchers (one translation unit each); arguments already validated.
 // ---------------------------------------------------------------------------
 int launch_route_topk(const void* x, int dtype, const void* w, const float* bias, int64_t T, int d,
-                      int E, int k, int flags, float* logits, int32_t* idx, float* gate,
+                      int E, int k, int flags, float* logits, int32_t* idx, float* gate, void* ws,
                       hipStream_t s);
+size_t route_ws_bytes(int dtype, int64_t T, int d, int E, int flags);
 
 int launch_histogram(const int32_t* idx, int64_t T, int k, int E, int32_t* counts, int32_t* coact,
                      hipStream_t s);

@@ -15,8 +15,13 @@ namespace {
 
 constexpr int ROUTE_TOKENS = 64;
 constexpr int ROUTE_THREADS = 256;
+constexpr int ROUTE_MAX_SPLIT = 16;    // K chunks of the split score kernel
 
-enum RouteMode { MODE_F32 = 1, MODE_LOGITS_IN = 2 };
+enum RouteMode { MODE_F32 = 1, MODE_LOGITS_IN = 2, MODE_PARTIALS = 3 };
+
+}  // namespace
+int route_split(int64_t T, int d, int E);
+namespace {
 
 // "a ranks before b": larger score, or equal score and lower expert index.
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
@@ -95,8 +100,8 @@ __device__ __forceinline__ void finish_tokens(float* S, int ldS, int nt, int64_t
 // bf16 gate scores on MFMA 16x16x32.  A workgroup of 16 waves owns 16*RT
 // tokens; wave w takes the K steps w, w+16, w+32, ... (32 elements each) for
 // all RT token tiles and up to NTM expert tiles, with operand fragments loaded
-// straight from global memory (the router matrix stays L2-resident); the
-// 16 waves per workgroup hide the load latency.  Partial scores are reduced in LDS in a fixed order
+// straight from global memory (the router matrix stays L2-resident), two K
+// steps of loads in flight per wave.  Partial scores are reduced in LDS in a fixed order
 // (four slices, each summed over its four waves in turn, then the slices in
 // turn), so the scores are deterministic.
 constexpr int RB_WAVES = 16;
@@ -106,7 +111,7 @@ template <int RT, int NTM, int KM>
 __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, const float* __restrict__ bias,
     int64_t T, int d, int E, int k, int renorm, float* __restrict__ logits,
-    int32_t* __restrict__ idx, float* __restrict__ gate) {
+    int32_t* __restrict__ idx, float* __restrict__ gate, int S, float* __restrict__ part) {
     extern __shared__ float smem[];
     constexpr int ROWS = 16 * RT;
     const int E_pad = (E + 15) & ~15;
@@ -126,36 +131,84 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
 #pragma unroll
         for (int j = 0; j < NTM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int nsteps = (d + 31) / 32;
-    for (int step = wave; step < nsteps; step += RB_WAVES) {
-        const int k0 = step * 32;
-        const bool kin = k0 + kq < d;
-        bf16x8 a[RT];
+    // K chunk of this workgroup (blockIdx.y of S): steps [sbeg, send), 32 elements each
+    const int nsteps_all = (d + 31) / 32;
+    const int chunk = blockIdx.y;
+    const int sbeg = (int)((int64_t)chunk * nsteps_all / S);
+    const int send = (int)((int64_t)(chunk + 1) * nsteps_all / S);
+    const int nsteps = send - sbeg;
+    if (NTM <= 4) {
+        // all tiles' fragments of one K step fit in registers: keep two steps of
+        // loads in flight (ring of two register sets, alternating by step parity)
+        uint4 av[2][RT], bv[2][NTM];
+        auto load = [&](int step, uint4* a_, uint4* b_) {
+            const int k0 = step * 32;
+            const bool kin = k0 + kq < d;
 #pragma unroll
-        for (int i = 0; i < RT; ++i) {
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (kin && i * 16 + row < nt) v = *(const uint4*)(xbase + (int64_t)i * 16 * d + k0);
-            a[i] = __builtin_bit_cast(bf16x8, v);
-        }
-#pragma unroll
-        for (int jc = 0; jc < NTM; jc += 4) {
-            if (jc >= NT) break;
-            bf16x8 b[4];
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                const int j = jc + jj;
-                uint4 v = make_uint4(0, 0, 0, 0);
-                if (kin && j < NT && j * 16 + row < E)
-                    v = *(const uint4*)(wbase + (int64_t)j * 16 * d + k0);
-                b[jj] = __builtin_bit_cast(bf16x8, v);
+            for (int i = 0; i < RT; ++i) {
+                a_[i] = make_uint4(0, 0, 0, 0);
+                if (kin && i * 16 + row < nt) a_[i] = *(const uint4*)(xbase + (int64_t)i * 16 * d + k0);
             }
+#pragma unroll
+            for (int j = 0; j < NTM; ++j) {
+                b_[j] = make_uint4(0, 0, 0, 0);
+                if (kin && j < NT && j * 16 + row < E)
+                    b_[j] = *(const uint4*)(wbase + (int64_t)j * 16 * d + k0);
+            }
+        };
+        auto mma = [&](const uint4* a_, const uint4* b_) {
 #pragma unroll
             for (int i = 0; i < RT; ++i)
 #pragma unroll
-                for (int jj = 0; jj < 4; ++jj)
-                    if (jc + jj < NT)
-                        acc[i][jc + jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            a[i], b[jj], acc[i][jc + jj], 0, 0, 0);
+                for (int j = 0; j < NTM; ++j)
+                    if (j < NT)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            __builtin_bit_cast(bf16x8, a_[i]), __builtin_bit_cast(bf16x8, b_[j]),
+                            acc[i][j], 0, 0, 0);
+        };
+        const int n_mine = wave < nsteps ? (nsteps - wave + RB_WAVES - 1) / RB_WAVES : 0;
+        const int s0 = sbeg + wave;
+        if (n_mine > 0) load(s0, av[0], bv[0]);
+        if (n_mine > 1) load(s0 + RB_WAVES, av[1], bv[1]);
+        for (int i = 0; i < n_mine; i += 2) {
+            mma(av[0], bv[0]);
+            if (i + 2 < n_mine) load(s0 + (i + 2) * RB_WAVES, av[0], bv[0]);
+            if (i + 1 < n_mine) {
+                mma(av[1], bv[1]);
+                if (i + 3 < n_mine) load(s0 + (i + 3) * RB_WAVES, av[1], bv[1]);
+            }
+        }
+    } else {
+        for (int step = sbeg + wave; step < send; step += RB_WAVES) {
+            const int k0 = step * 32;
+            const bool kin = k0 + kq < d;
+            bf16x8 a[RT];
+#pragma unroll
+            for (int i = 0; i < RT; ++i) {
+                uint4 v = make_uint4(0, 0, 0, 0);
+                if (kin && i * 16 + row < nt) v = *(const uint4*)(xbase + (int64_t)i * 16 * d + k0);
+                a[i] = __builtin_bit_cast(bf16x8, v);
+            }
+#pragma unroll
+            for (int jc = 0; jc < NTM; jc += 4) {
+                if (jc >= NT) break;
+                bf16x8 b[4];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const int j = jc + jj;
+                    uint4 v = make_uint4(0, 0, 0, 0);
+                    if (kin && j < NT && j * 16 + row < E)
+                        v = *(const uint4*)(wbase + (int64_t)j * 16 * d + k0);
+                    b[jj] = __builtin_bit_cast(bf16x8, v);
+                }
+#pragma unroll
+                for (int i = 0; i < RT; ++i)
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+                        if (jc + jj < NT)
+                            acc[i][jc + jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                a[i], b[jj], acc[i][jc + jj], 0, 0, 0);
+            }
         }
     }
 
@@ -184,7 +237,15 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
         smem[o] = ((smem[o] + smem[slice + o]) + smem[2 * slice + o]) + smem[3 * slice + o];
     }
     __syncthreads();
-    finish_tokens<KM>(smem, ldS, nt, t0, E, k, renorm, bias, true, logits, idx, gate);
+    if (S == 1) {
+        finish_tokens<KM>(smem, ldS, nt, t0, E, k, renorm, bias, true, logits, idx, gate);
+    } else {
+        // partial scores of this K chunk: part[chunk][t][e]
+        for (int c = tid; c < nt * E; c += RB_THREADS) {
+            const int r = c / E, e = c % E;
+            part[((int64_t)chunk * T + t0 + r) * E + e] = smem[r * ldS + e];
+        }
+    }
 }
 
 // fp32 scores (plain FMA loops) or scores handed in (MOE_LOGITS_IN): 64 tokens
@@ -193,10 +254,10 @@ template <int MODE, int KM>
 __global__ __launch_bounds__(ROUTE_THREADS) void route_simple_kernel(
     const float* __restrict__ X, const float* __restrict__ W, const float* __restrict__ bias,
     int64_t T, int d, int E, int k, int renorm, float* __restrict__ logits,
-    int32_t* __restrict__ idx, float* __restrict__ gate) {
+    int32_t* __restrict__ idx, float* __restrict__ gate, int S, const float* __restrict__ part) {
     extern __shared__ float smem[];
     const int ldS = ((E + 15) & ~15) + 1;
-    float* S = smem;
+    float* Sm = smem;
     const int tid = threadIdx.x;
     const int64_t t0 = (int64_t)blockIdx.x * ROUTE_TOKENS;
     const int nt = (int)((T - t0) < ROUTE_TOKENS ? (T - t0) : ROUTE_TOKENS);
@@ -209,27 +270,51 @@ __global__ __launch_bounds__(ROUTE_THREADS) void route_simple_kernel(
                 const float* wr = W + (int64_t)e * d;
                 for (int i = 0; i < d; ++i) a = fmaf(xr[i], wr[i], a);
             }
-            S[r * ldS + e] = a;
+            Sm[r * ldS + e] = a;
+        }
+    } else if (MODE == MODE_PARTIALS) {
+        // K chunks summed in chunk order
+        for (int c = tid; c < nt * E; c += ROUTE_THREADS) {
+            const int r = c / E, e = c % E;
+            const float* p = part + (t0 + r) * E + e;
+            const int64_t cs = T * E;                // chunk stride
+            float v[ROUTE_MAX_SPLIT];
+#pragma unroll
+            for (int ch = 0; ch < ROUTE_MAX_SPLIT; ++ch) v[ch] = ch < S ? p[ch * cs] : 0.f;
+            float sum = 0.f;
+#pragma unroll
+            for (int ch = 0; ch < ROUTE_MAX_SPLIT; ++ch) sum += v[ch];
+            Sm[r * ldS + e] = sum;
         }
     } else {
         for (int c = tid; c < nt * E; c += ROUTE_THREADS) {
             const int r = c / E, e = c % E;
-            S[r * ldS + e] = logits[(t0 + r) * E + e];
+            Sm[r * ldS + e] = logits[(t0 + r) * E + e];
         }
     }
     __syncthreads();
-    finish_tokens<KM>(S, ldS, nt, t0, E, k, renorm, bias, MODE == MODE_F32, logits, idx, gate);
+    finish_tokens<KM>(Sm, ldS, nt, t0, E, k, renorm, bias, MODE != MODE_LOGITS_IN, logits, idx,
+                      gate);
+}
+
+// Token rows per workgroup of the bf16 score kernel, by expert count.
+int route_rows(int E) {
+    const int E_pad = (E + 15) & ~15;
+    return 16 * (E_pad <= 16 ? 4 : (E_pad <= 128 ? 2 : 1));
 }
 
 template <int KM>
 int launch_km(const void* x, int dtype, const void* w, const float* bias, int64_t T, int d,
-              int E, int k, int flags, float* logits, int32_t* idx, float* gate, hipStream_t s) {
+              int E, int k, int flags, float* logits, int32_t* idx, float* gate, void* ws,
+              hipStream_t s) {
     const int renorm = (flags & MOE_RENORM) ? 1 : 0;
     const int E_pad = (E + 15) & ~15;
     if (!(flags & MOE_LOGITS_IN) && dtype == MOE_BF16) {
-        const int rt = E_pad <= 64 ? 4 : (E_pad <= 128 ? 2 : 1);
-        const size_t lds = (size_t)4 * 16 * rt * (E_pad + 1) * sizeof(float);
-        const dim3 grid((unsigned)ceil_div(T, 16 * rt)), block(RB_THREADS);
+        const int rows = route_rows(E);
+        const int S = route_split(T, d, E);
+        const size_t lds = (size_t)4 * rows * (E_pad + 1) * sizeof(float);
+        const dim3 grid((unsigned)ceil_div(T, rows), (unsigned)S), block(RB_THREADS);
+        float* part = (float*)ws;
 #define MOE_RB_LAUNCH(RT, NTM)                                                                  \
     do {                                                                                        \
         if (lds > 65536 &&                                                                      \
@@ -239,36 +324,62 @@ int launch_km(const void* x, int dtype, const void* w, const float* bias, int64_
             return MOE_ERR_DEVICE;                                                              \
         hipLaunchKernelGGL((route_bf16_kernel<RT, NTM, KM>), grid, block, lds, s,               \
                            (const bf16_t*)x, (const bf16_t*)w, bias, T, d, E, k, renorm,        \
-                           logits, idx, gate);                                                  \
+                           logits, idx, gate, S, part);                                         \
     } while (0)
-        if (rt == 4) MOE_RB_LAUNCH(4, 4);
-        else if (rt == 2) MOE_RB_LAUNCH(2, 8);
+        if (E_pad <= 16) MOE_RB_LAUNCH(4, 1);
+        else if (E_pad <= 64) MOE_RB_LAUNCH(2, 4);
+        else if (E_pad <= 128) MOE_RB_LAUNCH(2, 8);
         else MOE_RB_LAUNCH(1, 16);
 #undef MOE_RB_LAUNCH
+        if (S > 1) {
+            const size_t lds2 = (size_t)ROUTE_TOKENS * (E_pad + 1) * sizeof(float);
+            hipLaunchKernelGGL((route_simple_kernel<MODE_PARTIALS, KM>),
+                               dim3((unsigned)ceil_div(T, ROUTE_TOKENS)), dim3(ROUTE_THREADS),
+                               lds2, s, nullptr, nullptr, bias, T, d, E, k, renorm, logits, idx,
+                               gate, S, (const float*)part);
+        }
         return launch_status();
     }
     const size_t lds = (size_t)ROUTE_TOKENS * (E_pad + 1) * sizeof(float);
     const dim3 grid((unsigned)ceil_div(T, ROUTE_TOKENS)), block(ROUTE_THREADS);
     if (flags & MOE_LOGITS_IN)
         hipLaunchKernelGGL((route_simple_kernel<MODE_LOGITS_IN, KM>), grid, block, lds, s, nullptr,
-                           nullptr, nullptr, T, d, E, k, renorm, logits, idx, gate);
+                           nullptr, nullptr, T, d, E, k, renorm, logits, idx, gate, 1, nullptr);
     else
         hipLaunchKernelGGL((route_simple_kernel<MODE_F32, KM>), grid, block, lds, s,
                            (const float*)x, (const float*)w, bias, T, d, E, k, renorm, logits,
-                           idx, gate);
+                           idx, gate, 1, nullptr);
     return launch_status();
 }
 
 }  // namespace
 
+// K chunks of the bf16 score kernel: enough workgroups to spread the hidden
+// states over the chip when there are few token blocks (decode batches).
+int route_split(int64_t T, int d, int E) {
+    const int64_t blocks = ceil_div(T, route_rows(E));
+    if (blocks <= 0 || blocks >= 128) return 1;
+    const int nsteps = (d + 31) / 32;
+    int64_t S = ceil_div(256, blocks);
+    if (S > ROUTE_MAX_SPLIT) S = ROUTE_MAX_SPLIT;
+    if (S > nsteps / 4) S = nsteps / 4;
+    return S < 1 ? 1 : (int)S;
+}
+
+size_t route_ws_bytes(int dtype, int64_t T, int d, int E, int flags) {
+    if ((flags & MOE_LOGITS_IN) || dtype != MOE_BF16 || T <= 0) return 0;
+    const int S = route_split(T, d, E);
+    return S > 1 ? (size_t)S * (size_t)T * (size_t)E * sizeof(float) : 0;
+}
+
 int launch_route_topk(const void* x, int dtype, const void* w, const float* bias, int64_t T, int d,
-                      int E, int k, int flags, float* logits, int32_t* idx, float* gate,
+                      int E, int k, int flags, float* logits, int32_t* idx, float* gate, void* ws,
                       hipStream_t s) {
     if (T == 0) return MOE_OK;
-    if (k <= 2) return launch_km<2>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, s);
-    if (k <= 4) return launch_km<4>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, s);
-    if (k <= 8) return launch_km<8>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, s);
-    return launch_km<16>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, s);
+    if (k <= 2) return launch_km<2>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, ws, s);
+    if (k <= 4) return launch_km<4>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, ws, s);
+    if (k <= 8) return launch_km<8>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, ws, s);
+    return launch_km<16>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, ws, s);
 }
 
 }  // namespace moe

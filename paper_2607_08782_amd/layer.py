@@ -63,6 +63,9 @@ class LayerShare:
         self.logits = torch.empty((T, E), dtype=torch.float32, device=dv) if want_logits else None
         self.topk_idx = torch.empty((T, k), dtype=torch.int32, device=dv)
         self.topk_gate = torch.empty((T, k), dtype=torch.float32, device=dv)
+        dcode = moe.MOE_BF16 if dt == torch.bfloat16 else moe.MOE_F32
+        rb = moe.moe_route_topk_ws_bytes(dcode, T, d, E, moe.MOE_RENORM if renorm else 0)
+        self.ws_route = moe.workspace(rb, dv) if rb else None
         self.counts = torch.empty((E,), dtype=torch.int32, device=dv)
         self.coact = torch.empty((E, E), dtype=torch.int32, device=dv) if coact else None
         cap = max(self.cap_rows, 1)
@@ -117,7 +120,7 @@ class LayerShare:
         else:
             moe.moe_route_topk(self.X, self.Wr, self.bias, self.k, renorm=self.renorm,
                                logits=self.logits, want_logits=self.logits is not None,
-                               topk_idx=self.topk_idx, topk_gate=self.topk_gate)
+                               topk_idx=self.topk_idx, topk_gate=self.topk_gate, ws=self.ws_route)
 
     def run(self, logits_in: Optional[torch.Tensor] = None) -> torch.Tensor:
         """Enqueue the whole share on the current stream; returns y [T, d]."""

@@ -24,7 +24,8 @@ MOE_OK, MOE_ERR_ARG, MOE_ERR_PLACEMENT, MOE_ERR_SHAPE, MOE_ERR_DEVICE = 0, 1, 2,
 MOE_RENORM, MOE_LOGITS_IN = 1, 2
 MOE_MAX_E, MOE_MAX_K, MOE_MAX_G, MOE_MAX_GROUPS = 256, 16, 64, 128
 
-EXPORTS = ("moe_status_string", "moe_route_topk", "moe_expert_histogram", "moe_permute_ws_bytes",
+EXPORTS = ("moe_status_string", "moe_route_topk", "moe_route_topk_ws_bytes",
+           "moe_expert_histogram", "moe_permute_ws_bytes",
            "moe_permute", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_combine")
 
 _lib = None
@@ -47,8 +48,10 @@ def load_library(path: str = LIB_PATH):
     P, I, L, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
     lib.moe_status_string.argtypes = [I]
     lib.moe_status_string.restype = ctypes.c_char_p
-    lib.moe_route_topk.argtypes = [P, I, P, P, L, I, I, I, I, P, P, P, P]
+    lib.moe_route_topk.argtypes = [P, I, P, P, L, I, I, I, I, P, P, P, P, S, P]
     lib.moe_route_topk.restype = I
+    lib.moe_route_topk_ws_bytes.argtypes = [I, L, I, I, I]
+    lib.moe_route_topk_ws_bytes.restype = S
     lib.moe_expert_histogram.argtypes = [P, L, I, I, P, P, P]
     lib.moe_expert_histogram.restype = I
     lib.moe_permute_ws_bytes.argtypes = [L, I, I]
@@ -110,7 +113,8 @@ def moe_route_topk(x: Optional[torch.Tensor], w_router: Optional[torch.Tensor],
                    renorm: bool = True, logits: Optional[torch.Tensor] = None,
                    logits_in: bool = False, want_logits: bool = True,
                    topk_idx: Optional[torch.Tensor] = None,
-                   topk_gate: Optional[torch.Tensor] = None, stream=None):
+                   topk_gate: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                   stream=None):
     """Gate scores + top-k.  Returns (logits or None, topk_idx, topk_gate)."""
     lib = load_library()
     if logits_in:
@@ -136,13 +140,21 @@ def moe_route_topk(x: Optional[torch.Tensor], w_router: Optional[torch.Tensor],
     if topk_gate is None:
         topk_gate = _empty((T, k), torch.float32, device)
     flags = (MOE_RENORM if renorm else 0) | (MOE_LOGITS_IN if logits_in else 0)
+    need = moe_route_topk_ws_bytes(dtype, T, d, E_, flags)
+    if need and ws is None:
+        ws = workspace(need, device)
     st = lib.moe_route_topk(_dev(x, "x"), dtype, _dev(w_router, "w_router"),
                             _dev(bias, "bias", torch.float32), T, d, E_, k, flags,
                             _dev(logits, "logits", torch.float32),
                             _dev(topk_idx, "topk_idx", torch.int32),
-                            _dev(topk_gate, "topk_gate", torch.float32), _stream(stream))
+                            _dev(topk_gate, "topk_gate", torch.float32), _dev(ws, "ws"),
+                            0 if ws is None else ws.numel(), _stream(stream))
     _check("moe_route_topk", st)
     return logits, topk_idx, topk_gate
+
+
+def moe_route_topk_ws_bytes(dtype: int, T: int, d: int, E: int, flags: int) -> int:
+    return int(load_library().moe_route_topk_ws_bytes(dtype, T, d, E, flags))
 
 
 def moe_expert_histogram(topk_idx: torch.Tensor, E: int, *, counts: Optional[torch.Tensor] = None,

@@ -61,7 +61,7 @@ def test_route_topk_validation(lib):
     def call(**kw):
         a = dict(ok, **kw)
         return f(a["x"], a["dtype"], a["w"], a["b"], a["T"], a["d"], a["E"], a["k"], a["flags"],
-                 a["lg"], a["idx"], a["gate"], None)
+                 a["lg"], a["idx"], a["gate"], a.get("ws"), a.get("ws_bytes", 0), None)
     assert call(k=0) == moe.MOE_ERR_ARG
     assert call(k=9) == moe.MOE_ERR_ARG            # k > E
     assert call(E=300, k=2) == moe.MOE_ERR_ARG      # E > MOE_MAX_E
@@ -74,6 +74,14 @@ def test_route_topk_validation(lib):
     assert call(d=12) == moe.MOE_ERR_SHAPE          # bf16 rows must be 16-byte multiples
     assert call(x=ctypes.c_void_p(0x1002)) == moe.MOE_ERR_ARG   # misaligned bf16 rows
     assert call(flags=3, lg=None) == moe.MOE_ERR_ARG             # logits-in without logits
+    need = lib.moe_route_topk_ws_bytes(1, 4, 4096, 8, 1)
+    assert need > 0                                              # a 4-token batch splits K
+    assert call(d=4096) == moe.MOE_ERR_SHAPE                     # ... and needs its workspace
+    assert call(d=4096, ws=ctypes.c_void_p(0x100000), ws_bytes=need - 1) == moe.MOE_ERR_SHAPE
+    assert call(d=4096, ws=ctypes.c_void_p(0x100010), ws_bytes=need) == moe.MOE_ERR_SHAPE
+    assert lib.moe_route_topk_ws_bytes(1, 4, 64, 8, 1) == 0      # too short a K to split
+    assert lib.moe_route_topk_ws_bytes(1, 4, 64, 8, 3) == 0      # logits-in: none
+    assert lib.moe_route_topk_ws_bytes(0, 4, 64, 8, 1) == 0      # fp32 path: none
 
 
 def test_histogram_validation(lib):

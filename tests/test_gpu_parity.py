@@ -223,3 +223,36 @@ def test_group_sizes_around_the_streaming_threshold():
             w2 = np32(share.weights.w2[s])
             ref = oracle.expert_ffn(pm["x_perm"][go[s]:go[s + 1]], w13, w2)
             close(np32(share.y_perm[go[s]:go[s + 1]]), ref, OUT_TOL["bf16"], "group %d" % s)
+
+
+def test_graph_replays_match_eager_runs():
+    """The whole share captured once in a HIP graph: every replay (with new hidden
+    states copied in eagerly between replays) must equal an eager run bit for bit."""
+    cfg = synth.custom_config(d=256, E=16, k=4, f=256, shared_f=(128,), G=3, replicas=2,
+                              zipf=1.2)
+    inp, share = _share(cfg, 300)
+    share.coact = torch.empty((16, 16), dtype=torch.int32, device="cuda")
+    assert share.ws_route is not None                   # the split-K gate path is exercised
+
+    def snap():
+        N = int(share.perm["group_offsets"][-1])
+        return [share.y.clone(), share.topk_idx.clone(), share.counts.clone(), share.coact.clone(),
+                share.perm["token_row"].clone(), share.y_perm[:N].clone(), share.logits.clone()]
+
+    share.run()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        share.run()
+    torch.cuda.synchronize()
+    for i in range(4):
+        share.X.copy_(synth.normal(tuple(share.X.shape), 100 + i, "X", 0, 1.0, "cuda", torch.bfloat16))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = snap()
+        share.run()
+        torch.cuda.synchronize()
+        ref = snap()
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), "replay %d differs from the eager run" % i
