@@ -10,6 +10,7 @@ the decode batch (T=64) is reported beside it.  Prints ONE JSON line.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -118,6 +119,20 @@ def time_share(share, steps, warmup):
     return ms, phases, eager_ms
 
 
+def measured_traffic(workload):
+    """HBM bytes per moe_grouped_ffn call from the committed PMC record, or None
+    when the record is missing or the FFN kernels changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "ffn_traffic.json")
+    try:
+        rec = json.load(open(path))
+        src = open(os.path.join(ROOT, rec["kernel_source"]), "rb").read()
+    except (OSError, ValueError, KeyError):
+        return None
+    if hashlib.sha256(src).hexdigest() != rec.get("source_sha256") or workload not in rec:
+        return None
+    return rec[workload]["read"] + rec[workload]["write"]
+
+
 def ffn_work(share, cfg):
     go = share.perm["group_offsets"].cpu().numpy()
     sizes = np.diff(go)
@@ -162,6 +177,8 @@ def main():
     ap.add_argument("--workload", default="mixtral_8x7b:prefill")
     ap.add_argument("--decode", default="decode", help="regime reported beside the headline ('' = none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="first run a plain elementwise copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU's share of the layer; --gpus %d is not supported "
@@ -172,6 +189,14 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
     moe.load_library()
+    if args.calibrate_copy:
+        n = args.calibrate_copy * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)                 # reads and writes n*4 bytes each
+        torch.cuda.synchronize()
+        del src, dst
     name, regime = args.workload.split(":")
     cfg = synth.CONFIGS[name]
     T = cfg.T(regime)
@@ -207,7 +232,8 @@ def main():
         "roofline": {
             "kernel": "moe_grouped_ffn (grouped_gemm_kernel<swiglu> + grouped_gemm_kernel<plain>)",
             "bound": "mfma", "achieved": achieved / 1e12, "peak": PEAK_BF16_FLOPS / 1e12,
-            "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_FLOPS, "traffic": None,
+            "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_FLOPS,
+            "traffic": measured_traffic("%s:%s" % (name, regime)), "traffic_unit": "bytes per launch",
             "algorithmic_flops_per_launch": flops, "avg_launch_us": t_ffn * 1e6,
         },
         "phases_us": {k: v * 1e3 for k, v in phases.items()},
@@ -224,7 +250,9 @@ def main():
             "active_experts": dact,
             "roofline": {"kernel": "moe_grouped_ffn", "bound": "hbm",
                          "achieved": dby / dt / 1e9, "peak": PEAK_HBM_BYTES / 1e9, "unit": "GB/s",
-                         "frac": dby / dt / PEAK_HBM_BYTES, "traffic": None,
+                         "frac": dby / dt / PEAK_HBM_BYTES,
+                         "traffic": measured_traffic("%s:%s" % (name, args.decode)),
+                         "traffic_unit": "bytes per launch",
                          "algorithmic_bytes_per_launch": dby, "avg_launch_us": dt * 1e6},
             "phases_us": {k: v * 1e3 for k, v in dph.items()},
         }
