@@ -129,11 +129,13 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
             s_cur[2] = nt;
         }
         __syncthreads();
-        const int g = s_cur[0];
-        const int m0 = s_cur[1];
-        const int n0 = s_cur[2] * BN_OUT;
-        const int row0 = s_off[g] + m0;
-        const int rows_valid = min(BM, s_off[g + 1] - row0);
+        // tile coordinates are uniform across the workgroup: keep them (and the
+        // buffer descriptors built from them) in scalar registers
+        const int g = __builtin_amdgcn_readfirstlane(s_cur[0]);
+        const int m0 = __builtin_amdgcn_readfirstlane(s_cur[1]);
+        const int n0 = __builtin_amdgcn_readfirstlane(s_cur[2]) * BN_OUT;
+        const int row0 = __builtin_amdgcn_readfirstlane(s_off[g] + m0);
+        const int rows_valid = __builtin_amdgcn_readfirstlane(min(BM, s_off[g + 1] - row0));
         const bf16_t* __restrict__ W = args.w[g];
 
         const __amdgpu_buffer_rsrc_t arsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -368,15 +370,15 @@ __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(S
             s_item[1] = it - P.istart[lo];
         }
         __syncthreads();
-        const int g = s_item[0];
-        int local = s_item[1];
-        const int rows = P.off[g + 1] - P.off[g];
+        const int g = __builtin_amdgcn_readfirstlane(s_item[0]);
+        int local = __builtin_amdgcn_readfirstlane(s_item[1]);
+        const int rows = __builtin_amdgcn_readfirstlane(P.off[g + 1] - P.off[g]);
         const int mt = (int)ceil_div(rows, ST_M);
         const int m = local % mt;
         local /= mt;
         const int c = local % S;
         const int n0 = (local / S) * ST_N;
-        const int row0 = P.off[g] + m * ST_M;
+        const int row0 = __builtin_amdgcn_readfirstlane(P.off[g]) + m * ST_M;
         const int rows_valid = min(ST_M, rows - m * ST_M);
         const int bvalid = min(ST_N, args.N - n0);
         const int kt0 = (int)((int64_t)c * KT / S), kt1 = (int)((int64_t)(c + 1) * KT / S);
