@@ -13,6 +13,9 @@ with ctypes and marshals numpy arrays.  The steps follow the paper
 * packaging tokens for the GPUs that host their experts           -- Sec. II-B
 * workload matrix W, per-GPU load (Eq. 1), dispatch volume (Eq. 3),
   placement constraints (Eq. 6d, 6e)                              -- Sec. VI
+
+``oracle.placement`` is the plain reference of the placement model itself
+(Eq. 1-5, the LP relaxation's optimum, exhaustive search on tiny inputs).
 """
 from __future__ import annotations
 
