@@ -51,7 +51,32 @@ struct GemmArgs {
     int n_tiles;                       // output-column tiles per group
     int small_rows;                    // groups with at most this many rows are left to the
                                        // split-K streaming kernel (no tiles here)
+    float* part;                       // fp32 partial tiles for split K (nullptr: never split)
+    int* split_info;                   // the kernel records its split factor here for the reduce
+    int split_units;                   // workgroups split K aims to occupy (<= TILE_SPLIT_UNITS)
 };
+
+// With fewer tiles than half the workgroups (mid-sized groups: a few 256-row
+// tiles, long K), each tile's K range may be cut into S chunks of at least
+// TILE_SPLIT_MIN_STEPS stages; every (tile, chunk) unit writes an fp32 partial
+// tile and split_reduce_kernel sums the chunks in order and applies the epilogue.
+// S minimises (rounds of units) x (K stages per unit) plus the partial-tile
+// round trip, about 1/20 of a stage per unit (256 KB written and read back).
+constexpr int TILE_SPLIT_UNITS = 256;
+constexpr int TILE_SPLIT_MIN_STEPS = 8;
+
+__host__ __device__ __forceinline__ int tile_split(int total, int KT, int split_units) {
+    if (total <= 0 || 2 * total > split_units) return 1;
+    const int smax = min(split_units / total, KT / TILE_SPLIT_MIN_STEPS);
+    int best = 1;
+    int64_t best_cost = 20 * (int64_t)KT;
+    for (int S = 2; S <= smax; ++S) {
+        const int64_t rounds = ((int64_t)total * S + split_units - 1) / split_units;
+        const int64_t cost = 20 * rounds * ((KT + S - 1) / S) + (int64_t)S * total;
+        if (cost < best_cost) { best_cost = cost; best = S; }
+    }
+    return best;
+}
 
 // B-tile row of the jj-th 32-wide accumulator column block of wave column wn.
 // SwiGLU tiles hold 128 gate rows then the matching 128 up rows; a wave takes
@@ -101,22 +126,29 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
         }
     }
     __syncthreads();
-    const int total = s_tstart[n_groups];
+    const int KT = args.K / BK;
+    const int K = args.K;
+    const int total_tiles = s_tstart[n_groups];
+    const int S = args.part != nullptr ? tile_split(total_tiles, KT, args.split_units) : 1;
+    if (args.part != nullptr && blockIdx.x == 0 && tid == 0) *args.split_info = S;
+    const int total = total_tiles * S;             // work units: (tile, K chunk)
     const int nper = gridDim.x / NUM_XCD;
     const int xcd = blockIdx.x % NUM_XCD;
     const int widx = blockIdx.x / NUM_XCD;
     const int chunk = (total + NUM_XCD - 1) / NUM_XCD;
     const int t_begin = xcd * chunk;
     const int t_end = min(t_begin + chunk, total);
-    const int KT = args.K / BK;
-    const int K = args.K;
     const int kc = (tid & 7) * 8;
     const int voff = ((tid >> 3) * K + kc) * 2;
     const int vstep = ROWS_PER_PASS * K * 2;
     const int frag_col = (lane >> 5) * 32;
     const int frag_row = lane & 31;
 
-    for (int L = t_begin + widx; L < t_end; L += nper) {
+    for (int u = t_begin + widx; u < t_end; u += nper) {
+        const int L = u / S;                        // tile
+        const int kchunk = u - L * S;
+        const int kt0 = (int)((int64_t)kchunk * KT / S);
+        const int nsteps = (int)((int64_t)(kchunk + 1) * KT / S) - kt0;
         if (tid == 0) {
             int s = 0;
             while (s + 1 < n_groups && s_tstart[s + 1] <= L) ++s;
@@ -200,12 +232,12 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 
         // The K permutation inside a stage (lane half h, sub-step kk -> K offset
         // h*32 + kk*8) is the same for A and B, so the products sum over all K.
-        gload(0);
+        gload(kt0);
         sstore(0);
-        gload(KT > 1 ? 1 : 0);
+        gload(kt0 + (nsteps > 1 ? 1 : 0));
         __syncthreads();
         read(0, 0, fa0, fb0);
-        for (int t = 0; t < KT; ++t) {
+        for (int t = 0; t < nsteps; ++t) {
             const int buf = t & 1;
             __builtin_amdgcn_iglp_opt(1);
             read(buf, 1, fa1, fb1);
@@ -214,15 +246,36 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
             mfma(fa1, fb1);
             read(buf, 3, fa1, fb1);
             mfma(fa0, fb0);
-            if (t + 1 < KT) {
+            if (t + 1 < nsteps) {
                 sstore(buf ^ 1);
                 __syncthreads();
-                gload(t + 2 < KT ? t + 2 : KT - 1);
+                gload(kt0 + (t + 2 < nsteps ? t + 2 : nsteps - 1));
                 read(buf ^ 1, 0, fa0, fb0);
             }
             mfma(fa1, fb1);
         }
         __syncthreads();
+
+        if (S > 1) {
+            // fp32 partial tile of this K chunk, laid out [row][weight row of the
+            // tile]; rows past the group fall outside the descriptor and are dropped
+            const __amdgpu_buffer_rsrc_t prsrc = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(args.part + (int64_t)u * BM * BNW), (short)0, rows_valid * BNW * 4, RSRC_WORD3);
+            const int lbase = ((wm * (BM / WAVES_M) + (lane >> 5) * 4) * BNW +
+                               b_sub_row<SWIGLU>(wn, 0) + (lane & 31)) * 4;
+#pragma unroll
+            for (int mi = 0; mi < MS; ++mi)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+#pragma unroll
+                    for (int jj = 0; jj < NS; ++jj) {
+                        const int off = ((mi * 32 + (r >> 2) * 8 + (r & 3)) * BNW +
+                                         b_sub_row<SWIGLU>(0, jj)) * 4;
+                        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[mi][jj][r]), prsrc,
+                                                              lbase, off, 0);
+                    }
+            continue;
+        }
 
         // epilogue: accumulator element r of a 32x32 tile sits at
         // row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
@@ -442,12 +495,83 @@ __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(S
     }
 }
 
-// Fixed-order sum of the K chunks; SWIGLU: out[p][j] = SiLU(sum gate_j) * sum up_j
-// with gate in partial columns [0, N/2) and up in [N/2, N).
+// Sums, in chunk order, the K chunks of the tiled kernel's split tiles (fp32
+// partial tiles [row][weight row]; SWIGLU: gate in tile columns [0, 128), up
+// in [128, 256)) and applies the epilogue: out = SiLU(gate) * up, or the sum.
 template <bool SWIGLU>
-__global__ __launch_bounds__(ST_THREADS) void split_reduce_kernel(StreamArgs args) {
+__device__ void tile_split_reduce(const GemmArgs& t, int* s_off, int* s_tstart) {
+    const int n_groups = t.n_groups;
+    for (int g = threadIdx.x; g <= n_groups; g += ST_THREADS) s_off[g] = t.offsets[g];
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int acc = 0;
+        s_tstart[0] = 0;
+        for (int g = 0; g < n_groups; ++g) {
+            const int rows = s_off[g + 1] - s_off[g];
+            acc += rows > t.small_rows ? (int)ceil_div(rows, BM) * t.n_tiles : 0;
+            s_tstart[g + 1] = acc;
+        }
+    }
+    __syncthreads();
+    const int tiles = s_tstart[n_groups];
+    const int S = tile_split(tiles, t.K / BK, t.split_units);
+    if (S == 1) return;
+    constexpr int BN_OUT = SWIGLU ? BNW / 2 : BNW;
+    constexpr int C4 = BN_OUT / 4;
+    const int64_t items = (int64_t)tiles * BM * C4;
+    for (int64_t i = (int64_t)blockIdx.x * ST_THREADS + threadIdx.x; i < items;
+         i += (int64_t)gridDim.x * ST_THREADS) {
+        const int L = (int)(i / (BM * C4));
+        const int rem = (int)(i - (int64_t)L * BM * C4);
+        const int row = rem / C4, j = (rem - row * C4) * 4;
+        int g = 0;
+        while (g + 1 < n_groups && s_tstart[g + 1] <= L) ++g;
+        const int rows = s_off[g + 1] - s_off[g];
+        const int mt = (int)ceil_div(rows, BM);
+        const int local = L - s_tstart[g];
+        const int nt = local / mt;
+        const int m0 = (local - nt * mt) * BM;
+        if (m0 + row >= rows) continue;
+        const int n0 = nt * BN_OUT;
+        if (n0 + j >= t.N) continue;
+        float x[4] = {0.f, 0.f, 0.f, 0.f}, y[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < S; ++c) {
+            const float* pr = t.part + ((int64_t)(L * S + c) * BM + row) * BNW + j;
+            const float4 v = *(const float4*)pr;
+            x[0] += v.x; x[1] += v.y; x[2] += v.z; x[3] += v.w;
+            if (SWIGLU) {
+                const float4 w = *(const float4*)(pr + BNW / 2);
+                y[0] += w.x; y[1] += w.y; y[2] += w.z; y[3] += w.w;
+            }
+        }
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = SWIGLU ? silu(x[e]) * y[e] : x[e];
+        uint2 pk;
+        pk.x = pack_bf16x2(o[0], o[1]);
+        pk.y = pack_bf16x2(o[2], o[3]);
+        *(uint2*)(t.out + (int64_t)(s_off[g] + m0 + row) * t.ldo + n0 + j) = pk;
+    }
+}
+
+template <bool SWIGLU>
+__device__ __forceinline__ void stream_reduce(const StreamArgs& args, const StreamPlan& P);
+
+// Fixed-order sum of the K chunks; SWIGLU: out[p][j] = SiLU(sum gate_j) * sum up_j
+// with gate in partial columns [0, N/2) and up in [N/2, N).  The same launch
+// finishes the tiled kernel's split tiles (tile_split_reduce).
+template <bool SWIGLU>
+__global__ __launch_bounds__(ST_THREADS) void split_reduce_kernel(StreamArgs args, GemmArgs targs) {
     __shared__ StreamPlan P;
+    __shared__ int t_off[MOE_MAX_GROUPS + 1], t_tstart[MOE_MAX_GROUPS + 1];
+    const int tsplit = targs.part != nullptr ? *targs.split_info : 1;   // used at the end
     make_stream_plan(args, P, ST_THREADS);
+    stream_reduce<SWIGLU>(args, P);
+    if (tsplit > 1) tile_split_reduce<SWIGLU>(targs, t_off, t_tstart);
+}
+
+template <bool SWIGLU>
+__device__ __forceinline__ void stream_reduce(const StreamArgs& args, const StreamPlan& P) {
     const int n_small = P.n_small;
     if (n_small == 0) return;
     const int S = P.S;
@@ -571,12 +695,19 @@ static int64_t small_rows_bound(int64_t cap_rows, int n_groups) {
     return cap_rows < b ? cap_rows : b;
 }
 
+// fp32 partial tiles of the tiled kernel's split K (none when no group can be
+// big enough for the tiled kernel)
+static int64_t tile_part_bytes(int64_t cap_rows) {
+    return cap_rows > SMALL_ROWS ? 256 + (int64_t)TILE_SPLIT_UNITS * BM * BNW * 4 : 0;
+}
+
+// workspace: [H: cap_rows x f bf16][streaming partials][tiled partial tiles]
 size_t grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_groups) {
     if (dtype != MOE_BF16) return (size_t)cap_rows * (size_t)f * 4 + 256;
     const int64_t h = align256(cap_rows * (int64_t)f * 2);
     const int64_t ncols = 2 * (int64_t)f > d ? 2 * (int64_t)f : d;
-    const int64_t part = (int64_t)PART_FACTOR * small_rows_bound(cap_rows, n_groups) * ncols * 4;
-    return (size_t)(h + part + 256);
+    const int64_t part = align256((int64_t)PART_FACTOR * small_rows_bound(cap_rows, n_groups) * ncols * 4);
+    return (size_t)(h + part + tile_part_bytes(cap_rows) + 256);
 }
 
 int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, int n_groups,
@@ -604,9 +735,18 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     bf16_t* h = (bf16_t*)ws;
     float* part = (float*)((char*)ws + align256(cap_rows * (int64_t)f * 2));
     const int64_t rmax = small_rows_bound(cap_rows, n_groups);
+    const int64_t ncols = 2 * (int64_t)f > d ? 2 * (int64_t)f : d;
+    // tiled split K: two split factors (one per product) in a 256-byte header,
+    // then the partial tiles
+    char* tbase = tile_part_bytes(cap_rows) > 0
+                      ? (char*)part + align256((int64_t)PART_FACTOR * rmax * ncols * 4)
+                      : nullptr;
+    float* tpart = tbase ? (float*)(tbase + 256) : nullptr;
+    int* tinfo = tbase ? (int*)tbase : nullptr;
     const int sgrid = ((cus * ST_WG_PER_CU) / NUM_XCD) * NUM_XCD;
     const int64_t red_items = rmax * ((f > d ? f : d) / 8);
     int rgrid = (int)ceil_div(red_items, ST_THREADS);
+    if (tpart != nullptr && rgrid < 2 * cus) rgrid = 2 * cus;   // room for split tiles
     if (rgrid > 4096) rgrid = 4096;
     if (rgrid < 1) rgrid = 1;
 
@@ -623,6 +763,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a1.up_row = f;
     a1.n_tiles = (int)ceil_div(f, BNW / 2);
     a1.small_rows = SMALL_ROWS;
+    a1.part = tpart;
+    a1.split_info = tinfo;
+    a1.split_units = grid < TILE_SPLIT_UNITS ? grid : TILE_SPLIT_UNITS;
     hipLaunchKernelGGL(grouped_gemm_kernel<true>, dim3(grid), dim3(GEMM_THREADS), 0, s, a1);
     StreamArgs s1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) s1.w[i] = a1.w[i];
@@ -637,7 +780,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s1.part_rows = (int)(PART_FACTOR * rmax);
     s1.target_items = 2 * cus * ST_WG_PER_CU;
     hipLaunchKernelGGL(stream_gemm_kernel, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
-    hipLaunchKernelGGL(split_reduce_kernel<true>, dim3(rgrid), dim3(ST_THREADS), 0, s, s1);
+    hipLaunchKernelGGL(split_reduce_kernel<true>, dim3(rgrid), dim3(ST_THREADS), 0, s, s1, a1);
 
     // down product
     GemmArgs a2 = a1;
@@ -649,6 +792,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a2.ldo = d;
     a2.up_row = 0;
     a2.n_tiles = (int)ceil_div(d, BNW);
+    a2.split_info = tinfo ? tinfo + 1 : nullptr;
     hipLaunchKernelGGL(grouped_gemm_kernel<false>, dim3(grid), dim3(GEMM_THREADS), 0, s, a2);
     StreamArgs s2 = s1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) s2.w[i] = a2.w[i];
@@ -658,7 +802,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s2.N = d;
     s2.ldo = d;
     hipLaunchKernelGGL(stream_gemm_kernel, dim3(sgrid), dim3(ST_THREADS), 0, s, s2);
-    hipLaunchKernelGGL(split_reduce_kernel<false>, dim3(rgrid), dim3(ST_THREADS), 0, s, s2);
+    hipLaunchKernelGGL(split_reduce_kernel<false>, dim3(rgrid), dim3(ST_THREADS), 0, s, s2, a2);
     return launch_status();
 }
 
