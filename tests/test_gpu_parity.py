@@ -225,6 +225,40 @@ def test_group_sizes_around_the_streaming_threshold():
             close(np32(share.y_perm[go[s]:go[s + 1]]), ref, OUT_TOL["bf16"], "group %d" % s)
 
 
+def test_mid_sized_groups_split_k_in_the_tiled_kernel():
+    """Groups of 300 / 96 / 0 / 70 rows at d=1024, f=2048 give the tiled kernel 64
+    gate/up tiles (16 K stages) and 16 down tiles (32 K stages) for 256 CUs, so both
+    products split K (2 and 4 chunks) and finish in the reduce kernel.  Each group must
+    match the oracle, and two runs must agree bit for bit (chunks are summed in order)."""
+    sizes = [300, 96, 0, 70]
+    E = len(sizes)
+    cfg = synth.custom_config(d=1024, E=E, k=1, f=2048, G=1)
+    T = sum(sizes)
+    owner = np.repeat(np.arange(E), sizes)
+    np.random.default_rng(9).shuffle(owner)
+    L = np.zeros((T, E), np.float32)
+    L[np.arange(T), owner] = 1.0
+    inp, share = _share(cfg, T)
+    Lg = torch.from_numpy(L).cuda()
+    share.run(logits_in=Lg)
+    torch.cuda.synchronize()
+    first = share.y_perm[:T].clone()
+    share.run(logits_in=Lg)
+    torch.cuda.synchronize()
+    assert torch.equal(first, share.y_perm[:T])
+    go = share.perm["group_offsets"].cpu().numpy()
+    assert np.diff(go).tolist() == sizes
+    X = np32(inp.X)
+    idx, gate = oracle.topk(L, 1)
+    pm = oracle.permute(X, idx, gate, E, inp.placement, 0)
+    for s in range(E):
+        if sizes[s]:
+            w13 = np32(share.weights.w13[s])
+            w2 = np32(share.weights.w2[s])
+            ref = oracle.expert_ffn(pm["x_perm"][go[s]:go[s + 1]], w13, w2)
+            close(np32(share.y_perm[go[s]:go[s + 1]]), ref, OUT_TOL["bf16"], "group %d" % s)
+
+
 def test_graph_replays_match_eager_runs():
     """The whole share captured once in a HIP graph: every replay (with new hidden
     states copied in eagerly between replays) must equal an eager run bit for bit."""

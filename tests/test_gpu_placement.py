@@ -1,0 +1,59 @@
+"""The placement optimizer wired to the GPU layer (Sec. VI-A, Eq. 1 and Eq. 3).
+
+Each GPU's workload row W[j] is the expert histogram the library computes for
+that GPU's slice of the batch; the optimizer turns W into a placement; the same
+batch, packaged by ``moe_permute`` under that placement, must then send every
+GPU exactly the load Eq. 1 predicts (lambda_j), and the oracle's Eq. 3 volumes
+summed over senders must agree with it.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import placement as op
+from paper_2607_08782_amd import moe, placement as pl, synth
+from paper_2607_08782_amd.layer import LayerShare
+
+pytestmark = pytest.mark.gpu
+
+
+def _histograms(inp, cfg, G):
+    """W[j][i]: tokens of GPU j's slice routed to expert i (route + histogram on the GPU)."""
+    T = inp.X.shape[0]
+    rows = []
+    for j in range(G):
+        Xj = inp.X[j * T // G:(j + 1) * T // G].contiguous()
+        idx = torch.empty((Xj.shape[0], cfg.k), dtype=torch.int32, device="cuda")
+        gate = torch.empty((Xj.shape[0], cfg.k), dtype=torch.float32, device="cuda")
+        moe.moe_route_topk(Xj, inp.Wr, inp.bias, cfg.k, renorm=True, topk_idx=idx, topk_gate=gate,
+                           want_logits=False)
+        counts, _ = moe.moe_expert_histogram(idx, cfg.E)
+        rows.append(counts.cpu().numpy())
+    return np.stack(rows).astype(np.int64)
+
+
+def test_optimized_placement_sends_each_gpu_its_eq1_load():
+    cfg = synth.custom_config(d=256, E=16, k=4, f=128, G=4, zipf=1.2)
+    G, T, C_max = 4, 512, 5
+    inp = synth.make_layer(cfg, T, seed=3, device="cuda", experts="all")
+    W = _histograms(inp, cfg, G)
+    assert W.sum() == T * cfg.k
+    f_comp = [(0.0, 20.0), (0.05, 0.0)]
+    f_comm = [(1e6 / 153e9, 2.0)]
+    res = pl.place(W[None], G, C_max, cfg.d * 2.0, f_comp, f_comm, seed=0)
+    P = res.P[0]
+    x = res.x[0]
+    assert np.bincount(P, minlength=G).max() <= C_max
+    lam = op.loads(W.tolist(), P.tolist(), G)                     # Eq. 1
+    D = op.volumes(W.tolist(), P.tolist(), G, 1.0)               # Eq. 3 in tokens (d = 1)
+    for k in range(G):
+        assert lam[k] == sum(D[j][k] for j in range(G))
+    for dev in range(G):
+        local = [int(e) for e in np.nonzero(x[:, dev])[0]]
+        share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, x, dev,
+                           [inp.w13[e] for e in local], [inp.w2[e] for e in local])
+        share.run()
+        torch.cuda.synchronize()
+        send = share.perm["send_counts"].cpu().numpy().tolist()
+        assert send == [int(v) for v in lam]
+        assert int(share.perm["group_offsets"][-1]) == int(lam[dev])
