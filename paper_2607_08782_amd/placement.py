@@ -27,7 +27,8 @@ placement minimising T_comp + T_comm (Eq. 2, Eq. 4, problem of Eq. 5):
    fractional (or hosted more than once) are assigned, largest demand first,
    to the candidate GPU (x > 0, capacity left) that adds the least latency.
 5. Optional polish (not part of the paper's procedure): single-expert moves
-   and pairwise swaps while they strictly lower the exact latency.
+   and pairwise swaps while they strictly lower the exact latency; the
+   polished greedy placement is returned instead if it is better.
 
 Latency functions are convex piecewise-linear: pieces (slope, intercept),
 f(z) = max over pieces.  ``fit_convex_pwl`` builds one from profiled points.
@@ -438,12 +439,18 @@ def place(W, G: int, C_max: int, d: float, f_comp: Pieces, f_comm: Pieces, eps: 
     P = _complete(x_w.reshape(L, E, G), W, d, C_max, f_comp, f_comm)
     T_rounded = total_latency(W, P, d, f_comp, f_comm)
     moves = 0
+    source = "rounding"
     if polish:
         P, moves = _polish(P, W, d, C_max, f_comp, f_comm)
+        # safeguard: the polished greedy placement if it happens to be better
+        Pg, _ = _polish(P0, W, d, C_max, f_comp, f_comm)
+        if total_latency(W, Pg, d, f_comp, f_comm) < total_latency(W, P, d, f_comp, f_comm):
+            P, source = Pg, "greedy"
     xmap = np.zeros((L, E, G), dtype=np.uint8)
     xmap[np.arange(L)[:, None], np.arange(E)[None, :], P] = 1
     T = total_latency(W, P, d, f_comp, f_comm)
     info = {"lp_solves": solves, "beta_greedy": float(total_latency(W, P0, d, f_comp, f_comm)),
             "beta_rounding": beta_r, "latency_rounded": T_rounded, "polish_moves": moves,
+            "source": source,
             "search_s": t_search, "total_s": time.perf_counter() - t0, "walk": stats}
     return PlacementResult(P=P, x=xmap, beta_star=beta_star, latency=T, info=info)

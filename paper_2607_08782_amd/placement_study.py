@@ -1,0 +1,158 @@
+"""Proactive vs. reactive vs. static placement on a drifting workload (Sec. III,
+Finding 3; Sec. VI), measured on this GPU.
+
+For each batch of a drifting sequence (Qwen1.5-MoE-shaped layer: 60 experts, 8
+GPUs, top-4; the expert popularity is re-drawn every 4 batches) the GPU routes
+every GPU's slice of the batch and counts tokens per expert
+(``moe_route_topk`` + ``moe_expert_histogram``), giving the workload matrix W_b
+(Sec. VI-A).  Three placements are compared on each batch:
+
+* static: the placement computed once from the first batch, kept;
+* reactive: the optimizer's placement for the previous batch (the best a
+  system that reacts to observed load can do);
+* proactive: the optimizer's placement for the batch itself (Director with a
+  perfect predictor).
+
+Each is priced with the model of Eq. 1-4, using f_comp profiled on this GPU
+(``profiles/fcomp_qwen15_moe_a27b.json``) and f_comm = 5 us + bytes / 153 GB/s
+per peer (one xGMI link; a model, not a measurement), and its computation side
+is also measured: the straggler GPU's expert step is run for real (its share of
+the batch packaged by ``moe_permute`` and pushed through ``moe_grouped_ffn``) and
+timed.
+
+    python -m paper_2607_08782_amd.placement_study --out profiles/placement_qwen15_drift.md
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+import torch
+
+if __package__ in (None, ""):
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    __package__ = "paper_2607_08782_amd"
+
+from . import moe, placement as pl, synth  # noqa: E402
+from .layer import LayerShare  # noqa: E402
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+LINK_BYTES_PER_US = 153e9 / 1e6
+LINK_LATENCY_US = 5.0
+
+
+def workload(inp, cfg, G):
+    T = inp.X.shape[0]
+    W = np.zeros((G, cfg.E), np.int64)
+    for j in range(G):
+        Xj = inp.X[j * T // G:(j + 1) * T // G].contiguous()
+        _, idx, _ = moe.moe_route_topk(Xj, inp.Wr, inp.bias, cfg.k, renorm=True, want_logits=False)
+        counts, _ = moe.moe_expert_histogram(idx, cfg.E)
+        W[j] = counts.cpu().numpy()
+    return W
+
+
+def straggler_ffn_us(inp, cfg, x_map, weights, reps=5):
+    """Measured time of the routed-expert FFN step of the busiest GPU."""
+    G = x_map.shape[1]
+    worst = 0.0
+    for dev in range(G):
+        local = [int(e) for e in np.nonzero(x_map[:, dev])[0]]
+        if not local:
+            continue
+        share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, x_map, dev,
+                           [weights[e][0] for e in local], [weights[e][1] for e in local])
+        share.run()
+        times = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
+                                cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
+            b.record()
+            b.synchronize()
+            times.append(a.elapsed_time(b) * 1e3)
+        worst = max(worst, statistics.median(times))
+    return worst
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--batches", type=int, default=16)
+    ap.add_argument("--cmax", type=int, default=8)
+    ap.add_argument("--out", default=None)
+    args = ap.parse_args(argv)
+    if not torch.cuda.is_available():
+        raise SystemExit("the study routes and times on the GPU; no GPU is visible")
+    cfg = synth.CONFIGS["qwen15_moe_a27b"]
+    G, T = cfg.G, cfg.T("batch")
+    prof = json.load(open(os.path.join(ROOT, "profiles", "fcomp_qwen15_moe_a27b.json")))
+    f_comp = [tuple(p) for p in prof["pieces"]]
+    f_comm = [(1.0 / LINK_BYTES_PER_US, LINK_LATENCY_US)]
+    d_bytes = cfg.d * 2.0
+    weights = [synth.expert_weights(cfg, e, 0, "cuda") for e in range(cfg.E)]
+    rows, P_prev, P_static = [], None, None
+    opt_s = []
+    for b in range(args.batches):
+        inp = synth.make_layer(cfg, T, seed=0, device="cuda", batch=b, experts="none")
+        W = workload(inp, cfg, G)
+        t0 = time.perf_counter()
+        res = pl.place(W[None], G, args.cmax, d_bytes, f_comp, f_comm, seed=b)
+        opt_s.append(time.perf_counter() - t0)
+        if P_static is None:
+            P_static = res.P
+        plans = {"static": P_static, "reactive": P_prev if P_prev is not None else P_static,
+                 "proactive": res.P}
+        row = {"batch": b, "beta_star": res.beta_star}
+        for name, P in plans.items():
+            comp, comm = pl.layer_latencies(W[None].astype(np.float64), P, d_bytes, f_comp, f_comm)
+            x_map = np.zeros((cfg.E, G), np.uint8)
+            x_map[np.arange(cfg.E), P[0]] = 1
+            row[name] = {"model_us": float(comp[0] + comm[0]), "comp_us": float(comp[0]),
+                         "comm_us": float(comm[0]),
+                         "measured_ffn_us": straggler_ffn_us(inp, cfg, x_map, weights)}
+        rows.append(row)
+        P_prev = res.P
+        print("batch %2d: beta* %.1f | static %.1f | reactive %.1f | proactive %.1f (model us)" % (
+            b, res.beta_star, row["static"]["model_us"], row["reactive"]["model_us"],
+            row["proactive"]["model_us"]), flush=True)
+    mean = lambda k, f: statistics.mean(r[k][f] for r in rows)
+    lines = ["# Proactive vs. reactive vs. static placement on a drifting workload", "",
+             "Qwen1.5-MoE-A2.7B-shaped layer (d=2048, 60 experts, top-4, f=1408), 8 GPUs, C_max = %d,"
+             % args.cmax,
+             "%d batches of %d tokens (a GPU slice each of %d), popularity re-drawn every %d batches;"
+             % (args.batches, T, T // G, cfg.drift_every),
+             "synthetic seeded inputs.  Model: Eq. 1-4 with f_comp profiled on this GPU and f_comm =",
+             "%.0f us + bytes / 153 GB/s per peer (modelled link).  Measured: the busiest GPU's"
+             % LINK_LATENCY_US,
+             "`moe_grouped_ffn` step under each placement, median of 5 timed calls.", "",
+             "Command: `python -m paper_2607_08782_amd.placement_study --batches %d --cmax %d --out %s`"
+             % (args.batches, args.cmax, args.out), "",
+             "| batch | beta* (LP) | static model | reactive model | proactive model | static FFN | reactive FFN | proactive FFN |",
+             "|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append("| %d | %.1f | %.1f | %.1f | %.1f | %.1f | %.1f | %.1f |" % (
+            r["batch"], r["beta_star"], r["static"]["model_us"], r["reactive"]["model_us"],
+            r["proactive"]["model_us"], r["static"]["measured_ffn_us"],
+            r["reactive"]["measured_ffn_us"], r["proactive"]["measured_ffn_us"]))
+    lines.append("| mean | %.1f | %.1f | %.1f | %.1f | %.1f | %.1f | %.1f |" % (
+        statistics.mean(r["beta_star"] for r in rows), mean("static", "model_us"),
+        mean("reactive", "model_us"), mean("proactive", "model_us"),
+        mean("static", "measured_ffn_us"), mean("reactive", "measured_ffn_us"),
+        mean("proactive", "measured_ffn_us")))
+    lines += ["", "All times in microseconds.  Optimizer wall time per batch (host CPU): "
+              "median %.2f s, max %.2f s." % (statistics.median(opt_s), max(opt_s)), ""]
+    text = "\n".join(lines)
+    if args.out:
+        with open(args.out, "w") as fh:
+            fh.write(text)
+    print(text)
+
+
+if __name__ == "__main__":
+    main()
