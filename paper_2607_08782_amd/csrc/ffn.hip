@@ -78,6 +78,28 @@ __host__ __device__ __forceinline__ int tile_split(int total, int KT, int split_
     return best;
 }
 
+// Which tiles split: with few tiles all of them; otherwise only the tiles of a
+// last round that would fill at most half the workgroups (the round every
+// other workgroup waits for).  Tiles [0, head) run whole; tiles
+// [head, head + tail) run as S chunks each.
+struct SplitPlan {
+    int head, tail, S;
+};
+
+__host__ __device__ __forceinline__ SplitPlan split_plan(int total, int KT, int split_units) {
+    SplitPlan p = {total, 0, 1};
+    if (total <= 0) return p;
+    const int rounds = total / split_units;
+    const int rest = total - rounds * split_units;
+    const int S = tile_split(rest, KT, split_units);
+    if (S > 1) {
+        p.head = total - rest;
+        p.tail = rest;
+        p.S = S;
+    }
+    return p;
+}
+
 // B-tile row of the jj-th 32-wide accumulator column block of wave column wn.
 // SwiGLU tiles hold 128 gate rows then the matching 128 up rows; a wave takes
 // the same columns from both halves, so gate and up meet in its registers.
@@ -129,24 +151,33 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
     const int KT = args.K / BK;
     const int K = args.K;
     const int total_tiles = s_tstart[n_groups];
-    const int S = args.part != nullptr ? tile_split(total_tiles, KT, args.split_units) : 1;
-    if (args.part != nullptr && blockIdx.x == 0 && tid == 0) *args.split_info = S;
-    const int total = total_tiles * S;             // work units: (tile, K chunk)
+    SplitPlan plan = {total_tiles, 0, 1};
+    if (args.part != nullptr) plan = split_plan(total_tiles, KT, args.split_units);
+    if (args.part != nullptr && blockIdx.x == 0 && tid == 0) *args.split_info = plan.S;
+    // each XCD takes a contiguous chunk of the whole tiles and a contiguous
+    // chunk of the split units, so every XCD carries the same share of both
     const int nper = gridDim.x / NUM_XCD;
     const int xcd = blockIdx.x % NUM_XCD;
     const int widx = blockIdx.x / NUM_XCD;
-    const int chunk = (total + NUM_XCD - 1) / NUM_XCD;
-    const int t_begin = xcd * chunk;
-    const int t_end = min(t_begin + chunk, total);
+    const int hchunk = (plan.head + NUM_XCD - 1) / NUM_XCD;
+    const int h_begin = min(xcd * hchunk, plan.head), h_end = min(h_begin + hchunk, plan.head);
+    const int n_units = plan.tail * plan.S;
+    const int uchunk = (n_units + NUM_XCD - 1) / NUM_XCD;
+    const int s_begin = min(xcd * uchunk, n_units), s_end = min(s_begin + uchunk, n_units);
+    const int n_head = h_end - h_begin, n_mine = n_head + (s_end - s_begin);
     const int kc = (tid & 7) * 8;
     const int voff = ((tid >> 3) * K + kc) * 2;
     const int vstep = ROWS_PER_PASS * K * 2;
     const int frag_col = (lane >> 5) * 32;
     const int frag_row = lane & 31;
 
-    for (int u = t_begin + widx; u < t_end; u += nper) {
-        const int L = u / S;                        // tile
-        const int kchunk = u - L * S;
+    for (int i = widx; i < n_mine; i += nper) {
+        // whole tile, or unit u = (split tile, K chunk)
+        const bool split = i >= n_head;
+        const int u = split ? s_begin + (i - n_head) : 0;
+        const int L = split ? plan.head + u / plan.S : h_begin + i;
+        const int S = split ? plan.S : 1;
+        const int kchunk = split ? u - (u / plan.S) * plan.S : 0;
         const int kt0 = (int)((int64_t)kchunk * KT / S);
         const int nsteps = (int)((int64_t)(kchunk + 1) * KT / S) - kt0;
         if (tid == 0) {
@@ -256,7 +287,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
         }
         __syncthreads();
 
-        if (S > 1) {
+        if (split) {
             // fp32 partial tile of this K chunk, laid out [row][weight row of the
             // tile]; rows past the group fall outside the descriptor and are dropped
             const __amdgpu_buffer_rsrc_t prsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -513,16 +544,17 @@ __device__ void tile_split_reduce(const GemmArgs& t, int* s_off, int* s_tstart) 
         }
     }
     __syncthreads();
-    const int tiles = s_tstart[n_groups];
-    const int S = tile_split(tiles, t.K / BK, t.split_units);
+    const SplitPlan plan = split_plan(s_tstart[n_groups], t.K / BK, t.split_units);
+    const int S = plan.S;
     if (S == 1) return;
     constexpr int BN_OUT = SWIGLU ? BNW / 2 : BNW;
     constexpr int C4 = BN_OUT / 4;
-    const int64_t items = (int64_t)tiles * BM * C4;
+    const int64_t items = (int64_t)plan.tail * BM * C4;
     for (int64_t i = (int64_t)blockIdx.x * ST_THREADS + threadIdx.x; i < items;
          i += (int64_t)gridDim.x * ST_THREADS) {
-        const int L = (int)(i / (BM * C4));
-        const int rem = (int)(i - (int64_t)L * BM * C4);
+        const int q = (int)(i / (BM * C4));          // split tile, counted from plan.head
+        const int L = plan.head + q;
+        const int rem = (int)(i - (int64_t)q * BM * C4);
         const int row = rem / C4, j = (rem - row * C4) * 4;
         int g = 0;
         while (g + 1 < n_groups && s_tstart[g + 1] <= L) ++g;
@@ -536,7 +568,7 @@ __device__ void tile_split_reduce(const GemmArgs& t, int* s_off, int* s_tstart) 
         if (n0 + j >= t.N) continue;
         float x[4] = {0.f, 0.f, 0.f, 0.f}, y[4] = {0.f, 0.f, 0.f, 0.f};
         for (int c = 0; c < S; ++c) {
-            const float* pr = t.part + ((int64_t)(L * S + c) * BM + row) * BNW + j;
+            const float* pr = t.part + ((int64_t)(q * S + c) * BM + row) * BNW + j;
             const float4 v = *(const float4*)pr;
             x[0] += v.x; x[1] += v.y; x[2] += v.z; x[3] += v.w;
             if (SWIGLU) {
