@@ -373,7 +373,7 @@ struct StreamArgs {
     int N;                               // weight rows (2f for gate/up, d for down)
     int ldo;
     int part_rows;                       // capacity of `part` in rows (S * n_small <= part_rows)
-    int target_items;
+    int grid;                            // workgroups of the streaming launch
 };
 
 struct StreamPlan {
@@ -399,7 +399,11 @@ __device__ void make_stream_plan(const StreamArgs& a, StreamPlan& P, int nthread
             }
         }
         P.qbase[a.n_groups] = rows_small;
-        int S = base > 0 ? (int)ceil_div(a.target_items, base) : 1;
+        // split factor: as many K chunks as fit the grid in one round (every
+        // workgroup streams one item; a partly filled extra round would leave
+        // most of HBM idle); each workgroup computes this plan before its
+        // first load, so it is kept to a few integer operations
+        int S = base > 0 ? a.grid / base : 1;
         S = min(S, SPLIT_MAX);
         S = min(S, KT);
         if (rows_small > 0) S = min(S, a.part_rows / rows_small);
@@ -810,7 +814,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s1.N = 2 * f;
     s1.ldo = f;
     s1.part_rows = (int)(PART_FACTOR * rmax);
-    s1.target_items = 2 * cus * ST_WG_PER_CU;
+    s1.grid = sgrid;
     hipLaunchKernelGGL(stream_gemm_kernel, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
     hipLaunchKernelGGL(split_reduce_kernel<true>, dim3(rgrid), dim3(ST_THREADS), 0, s, s1, a1);
 
