@@ -12,6 +12,7 @@ namespace {
 
 constexpr int HIST_THREADS = 256;
 constexpr int LDS_COACT_MAX_E = 128;     // E*E int32 bins fit in 64 KiB of LDS
+constexpr int DIRECT_MAX_TOKENS = 512;   // up to this many tokens one workgroup does it all
 
 __global__ void zero_i32_kernel(int32_t* __restrict__ p, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
@@ -19,7 +20,9 @@ __global__ void zero_i32_kernel(int32_t* __restrict__ p, int64_t n) {
         p[i] = 0;
 }
 
-template <bool COACT, bool LDS_COACT>
+// DIRECT: a single workgroup covers all tokens and stores its bins (zeros
+// included), so the outputs need no clearing launch beforehand.
+template <bool COACT, bool LDS_COACT, bool DIRECT = false>
 __global__ __launch_bounds__(HIST_THREADS) void histogram_kernel(
     const int32_t* __restrict__ idx, int64_t T, int k, int E, int32_t* __restrict__ counts,
     int32_t* __restrict__ coact) {
@@ -57,6 +60,12 @@ __global__ __launch_bounds__(HIST_THREADS) void histogram_kernel(
         }
     }
     __syncthreads();
+    if (DIRECT) {
+        for (int i = threadIdx.x; i < E; i += HIST_THREADS) counts[i] = c_lds[i];
+        if (LDS_COACT)
+            for (int i = threadIdx.x; i < E * E; i += HIST_THREADS) coact[i] = co_lds[i];
+        return;
+    }
     for (int i = threadIdx.x; i < E; i += HIST_THREADS)
         if (c_lds[i]) atomicAdd(&counts[i], c_lds[i]);
     if (LDS_COACT)
@@ -68,6 +77,16 @@ __global__ __launch_bounds__(HIST_THREADS) void histogram_kernel(
 
 int launch_histogram(const int32_t* idx, int64_t T, int k, int E, int32_t* counts, int32_t* coact,
                      hipStream_t s) {
+    // short batches (decode): one workgroup, bins stored directly, one launch
+    if (T <= DIRECT_MAX_TOKENS && (!coact || E <= LDS_COACT_MAX_E)) {
+        if (coact)
+            hipLaunchKernelGGL((histogram_kernel<true, true, true>), dim3(1), dim3(HIST_THREADS),
+                               (size_t)E * E * sizeof(int32_t), s, idx, T, k, E, counts, coact);
+        else
+            hipLaunchKernelGGL((histogram_kernel<false, false, true>), dim3(1), dim3(HIST_THREADS),
+                               0, s, idx, T, k, E, counts, coact);
+        return launch_status();
+    }
     const int64_t nbins = (int64_t)E + (coact ? (int64_t)E * E : 0);
     hipLaunchKernelGGL(zero_i32_kernel, dim3((unsigned)ceil_div(E, 256)), dim3(256), 0, s, counts,
                        (int64_t)E);

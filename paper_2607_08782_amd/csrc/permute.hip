@@ -151,6 +151,98 @@ __global__ __launch_bounds__(PERM_TOKENS) void perm_scatter_kernel(
     }
 }
 
+// Short batches (at most SMALL_T tokens): count, scan and scatter in one
+// workgroup, one wave per 64-token block, the same arithmetic as the three
+// kernels above (so the same unique result), one launch instead of three.
+constexpr int SMALL_T = 1024;
+constexpr int SMALL_BLK = SMALL_T / PERM_TOKENS;
+
+__global__ __launch_bounds__(SMALL_T) void perm_small_kernel(
+    const int32_t* __restrict__ idx, const float* __restrict__ gate,
+    const int32_t* __restrict__ counts, int64_t T, int k, int E, SlotTable st, HostTable ht,
+    int n_local, int G, int dev, int32_t* __restrict__ group_offsets,
+    int32_t* __restrict__ row_token, float* __restrict__ row_gate, int32_t* __restrict__ token_row,
+    int32_t* __restrict__ send_counts) {
+    __shared__ unsigned long long bits[SMALL_BLK][MOE_MAX_GROUPS];
+    __shared__ int32_t base[SMALL_BLK][MOE_MAX_GROUPS];
+    __shared__ int16_t slot_lds[MOE_MAX_E];
+    __shared__ int32_t lo_s[MOE_MAX_GROUPS], size_s[MOE_MAX_GROUPS], off_s[MOE_MAX_GROUPS + 1];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int nblk = (int)ceil_div(T, PERM_TOKENS);
+    for (int e = tid; e < E; e += SMALL_T) slot_lds[e] = st.slot_of[e];
+    for (int i = tid; i < SMALL_BLK * MOE_MAX_GROUPS; i += SMALL_T)
+        bits[i / MOE_MAX_GROUPS][i % MOE_MAX_GROUPS] = 0ull;
+    __syncthreads();
+    const int64_t t = (int64_t)wave * PERM_TOKENS + lane;
+    if (t < T) {
+        for (int r = 0; r < k; ++r) {
+            const int e = idx[t * k + r];
+            if ((unsigned)e >= (unsigned)E) continue;
+            const int sl = slot_lds[e];
+            if (sl >= 0) atomicOr(&bits[wave][sl], 1ull << lane);
+        }
+    }
+    __syncthreads();
+    const uint64_t below = dev == 0 ? 0ull : (~0ull >> (64 - dev));
+    if (tid < n_local) {
+        int32_t run = 0;
+        for (int b = 0; b < nblk; ++b) {
+            base[b][tid] = run;
+            run += __popcll(bits[b][tid]);
+        }
+        const int e = ht.expert_of_slot[tid];
+        const int64_t c = counts[e];
+        const uint64_t h = ht.hosts[e];
+        const int n = __popcll(h);
+        const int q = __popcll(h & below);
+        const int64_t lo = (int64_t)q * c / n;
+        lo_s[tid] = (int32_t)lo;
+        size_s[tid] = (int32_t)((int64_t)(q + 1) * c / n - lo);
+    }
+    if (send_counts && tid >= SMALL_T - 64 && tid - (SMALL_T - 64) < G) {
+        const int j = tid - (SMALL_T - 64);
+        const uint64_t below_j = j == 0 ? 0ull : (~0ull >> (64 - j));
+        int64_t sum = 0;
+        for (int e = 0; e < E; ++e) {
+            const uint64_t h = ht.hosts[e];
+            if (!((h >> j) & 1ull)) continue;
+            const int64_t c = counts[e];
+            const int n = __popcll(h);
+            const int q = __popcll(h & below_j);
+            sum += (int64_t)(q + 1) * c / n - (int64_t)q * c / n;
+        }
+        send_counts[j] = (int32_t)sum;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int32_t run = 0;
+        off_s[0] = 0;
+        for (int sl = 0; sl < n_local; ++sl) {
+            run += size_s[sl];
+            off_s[sl + 1] = run;
+        }
+    }
+    __syncthreads();
+    for (int sl = tid; sl <= n_local; sl += SMALL_T) group_offsets[sl] = off_s[sl];
+    if (t >= T) return;
+    const unsigned long long lower = (1ull << lane) - 1ull;
+    for (int r = 0; r < k; ++r) {
+        const int e = idx[t * k + r];
+        int32_t p = -1;
+        const int sl = (unsigned)e < (unsigned)E ? (int)slot_lds[e] : -1;
+        if (sl >= 0) {
+            const int32_t rank = base[wave][sl] + __popcll(bits[wave][sl] & lower);
+            const int32_t lo = lo_s[sl];
+            if (rank >= lo && rank < lo + size_s[sl]) {
+                p = off_s[sl] + (rank - lo);
+                row_token[p] = (int32_t)t;
+                row_gate[p] = gate[t * k + r];
+            }
+        }
+        token_row[t * k + r] = p;
+    }
+}
+
 template <typename U>
 __global__ __launch_bounds__(256) void gather_rows_kernel(
     const U* __restrict__ x, const int32_t* __restrict__ row_token,
@@ -190,15 +282,21 @@ int launch_permute(const void* x, int dtype, const int32_t* idx, const float* ga
     }
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) ht.expert_of_slot[i] = tabs.expert_of_slot[i];
 
-    if (nblk > 0 && n_local > 0)
-        hipLaunchKernelGGL(perm_count_kernel, dim3((unsigned)nblk), dim3(PERM_TOKENS), 0, s, idx,
-                           T, k, E, st, n_local, blk);
-    hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(256), 0, s, counts, ht, E, n_local, G, dev,
-                       n_local > 0 ? nblk : (int64_t)0, blk, group_offsets, lo_ws, send_counts);
-    if (nblk > 0)
-        hipLaunchKernelGGL(perm_scatter_kernel, dim3((unsigned)nblk), dim3(PERM_TOKENS), 0, s, idx,
-                           gate, T, k, E, st, n_local, blk, lo_ws, group_offsets, row_token,
+    if (T <= SMALL_T) {
+        hipLaunchKernelGGL(perm_small_kernel, dim3(1), dim3(SMALL_T), 0, s, idx, gate, counts, T, k,
+                           E, st, ht, n_local, G, dev, group_offsets, row_token, row_gate,
+                           token_row, send_counts);
+    } else {
+        if (n_local > 0)
+            hipLaunchKernelGGL(perm_count_kernel, dim3((unsigned)nblk), dim3(PERM_TOKENS), 0, s,
+                               idx, T, k, E, st, n_local, blk);
+        hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(256), 0, s, counts, ht, E, n_local, G,
+                           dev, n_local > 0 ? nblk : (int64_t)0, blk, group_offsets, lo_ws,
+                           send_counts);
+        hipLaunchKernelGGL(perm_scatter_kernel, dim3((unsigned)nblk), dim3(PERM_TOKENS), 0, s,
+                           idx, gate, T, k, E, st, n_local, blk, lo_ws, group_offsets, row_token,
                            row_gate, token_row);
+    }
     if (nblk > 0 && n_local > 0 && d > 0) {
         const size_t row_bytes = (size_t)d * (dtype == MOE_BF16 ? 2 : 4);
         int64_t max_rows = cap_rows;
