@@ -53,7 +53,7 @@ def pwl_eval(pieces: Pieces, z):
 
 
 def fit_convex_pwl(z, t) -> List[Tuple[float, float]]:
-    """Convex piecewise-linear model through the lower convex hull of (z, t)."""
+    """Convex, non-decreasing piecewise-linear model through the lower convex hull of (z, t)."""
     pts = sorted(zip(np.asarray(z, float).tolist(), np.asarray(t, float).tolist()))
     hull: List[Tuple[float, float]] = []
     for p in pts:
@@ -74,6 +74,11 @@ def fit_convex_pwl(z, t) -> List[Tuple[float, float]]:
     for (x1, y1), (x2, y2) in zip(hull[:-1], hull[1:]):
         a = (y2 - y1) / (x2 - x1)
         pieces.append((a, y1 - a * x1))
+    # a latency does not fall as the load grows: a falling start of the hull
+    # (measurement noise at small loads) becomes a flat piece at its minimum
+    if pieces[0][0] < 0:
+        floor = min(y for _, y in hull)
+        pieces = [(0.0, floor)] + [p for p in pieces if p[0] >= 0]
     return pieces
 
 
@@ -164,15 +169,20 @@ def _build_lp(W: np.ndarray, d: float, C_max: int, f_comp: Pieces, f_comm: Piece
 
 
 def _feasible(lp: _LP, beta: float, c: Optional[np.ndarray] = None):
+    """A point of the LP at budget beta, or (None, None) when there is none.  If the
+    solver cannot decide (numerical trouble), the interior-point method is tried;
+    a budget still undecided is treated as infeasible, which only keeps the binary
+    search's upper end at a budget known to be feasible."""
     b = lp.b.copy()
     b[0] = beta
-    res = linprog(np.zeros(lp.nv) if c is None else c, A_ub=lp.A, b_ub=b, bounds=lp.bounds,
-                  method="highs")
-    if res.status == 0:
-        return np.clip(res.x[:lp.nx], 0.0, 1.0), res.x
-    if res.status == 2:
-        return None, None
-    raise RuntimeError("LP solver: %s" % res.message)
+    obj = np.zeros(lp.nv) if c is None else c
+    for method in ("highs", "highs-ipm"):
+        res = linprog(obj, A_ub=lp.A, b_ub=b, bounds=lp.bounds, method=method)
+        if res.status == 0:
+            return np.clip(res.x[:lp.nx], 0.0, 1.0), res.x
+        if res.status == 2:
+            return None, None
+    return None, None
 
 
 # ----------------------------------------------------------------------------- rounding

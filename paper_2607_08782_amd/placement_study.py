@@ -81,6 +81,46 @@ def straggler_ffn_us(inp, cfg, x_map, weights, reps=5):
     return worst
 
 
+def migration_rows(cfg, G, T, weights, plans, f_comp, dev=0, reps=3):
+    """For each change of the proactive placement on `dev`: bytes brought in, the
+    copies scheduled into the FFN windows of the following steps, the steps needed,
+    the FFN time with and without copies in flight, and the wait at window close."""
+    from .migration import ExpertStore, Migrator, measure_h2d_rate, run_step
+
+    store = ExpertStore([w[0] for w in weights], [w[1] for w in weights])
+    rate = measure_h2d_rate()                                   # bytes per us
+    out = []
+    for b in range(1, len(plans)):
+        P_old, P_new = plans[b - 1], plans[b]
+        x_old = np.zeros((cfg.E, G), np.uint8); x_old[np.arange(cfg.E), P_old[0]] = 1
+        x_new = np.zeros((cfg.E, G), np.uint8); x_new[np.arange(cfg.E), P_new[0]] = 1
+        inc = set(np.nonzero(x_new[:, dev])[0]) - set(np.nonzero(x_old[:, dev])[0])
+        if not inc or x_new[:, dev].sum() != x_old[:, dev].sum():
+            continue
+        inp = synth.make_layer(cfg, T, seed=0, device="cuda", batch=b, experts="none")
+        mig = Migrator(store, x_old, dev, spare=len(inc))
+        w13, w2 = mig.weights()
+        share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, x_old, dev, w13, w2)
+        base = {}
+        for _ in range(reps):
+            run_step(share, None, 0, base)
+        lam = int(share.perm["group_offsets"][-1])
+        window_us = float(pl.pwl_eval(f_comp, lam))
+        moved = mig.plan(x_new)
+        during, stalls, steps = {}, [], 0
+        while not mig.finished:
+            st = run_step(share, mig, int(window_us * rate), during)
+            stalls.append(0.0 if st is None else st * 1e3)
+            steps += 1
+        torch.cuda.synchronize()
+        out.append({"batch": b, "experts_in": len(inc), "mbytes": moved / 1e6, "rate_gbs": rate / 1e3,
+                    "window_us": window_us, "steps": steps,
+                    "ffn_us": statistics.median(base["ffn"]) * 1e3,
+                    "ffn_copy_us": statistics.median(during["ffn"]) * 1e3,
+                    "max_stall_us": max(stalls)})
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--batches", type=int, default=16)
@@ -97,7 +137,7 @@ def main(argv=None):
     d_bytes = cfg.d * 2.0
     weights = [synth.expert_weights(cfg, e, 0, "cuda") for e in range(cfg.E)]
     rows, P_prev, P_static = [], None, None
-    opt_s = []
+    opt_s, proactive = [], []
     for b in range(args.batches):
         inp = synth.make_layer(cfg, T, seed=0, device="cuda", batch=b, experts="none")
         W = workload(inp, cfg, G)
@@ -118,6 +158,7 @@ def main(argv=None):
                          "measured_ffn_us": straggler_ffn_us(inp, cfg, x_map, weights)}
         rows.append(row)
         P_prev = res.P
+        proactive.append(res.P)
         print("batch %2d: beta* %.1f | static %.1f | reactive %.1f | proactive %.1f (model us)" % (
             b, res.beta_star, row["static"]["model_us"], row["reactive"]["model_us"],
             row["proactive"]["model_us"]), flush=True)
@@ -147,6 +188,21 @@ def main(argv=None):
         mean("proactive", "measured_ffn_us")))
     lines += ["", "All times in microseconds.  Optimizer wall time per batch (host CPU): "
               "median %.2f s, max %.2f s." % (statistics.median(opt_s), max(opt_s)), ""]
+    mrows = migration_rows(cfg, G, T, weights, proactive, f_comp)
+    lines += ["## Migrating to each new proactive placement (GPU 0, Sec. V-B)", "",
+              "Incoming experts are copied from pinned host memory (standing in for the peer",
+              "GPUs; a host-to-device copy on the DMA engines) into spare buffers, chunk by chunk,",
+              "inside the FFN window of the following steps: each window gets the bytes that",
+              "f_comp(lambda of GPU 0) at the measured copy rate predicts it can hide, and the",
+              "step waits for them where the window closes (where the combine's all-to-all",
+              "would start).  The batch keeps being served on the old placement meanwhile.", "",
+              "| batch | experts in | MB | copy GB/s | window us | steps | FFN us alone | FFN us with copies | max wait at close us |",
+              "|---|---|---|---|---|---|---|---|---|"]
+    for m in mrows:
+        lines.append("| %d | %d | %.1f | %.1f | %.1f | %d | %.1f | %.1f | %.1f |" % (
+            m["batch"], m["experts_in"], m["mbytes"], m["rate_gbs"], m["window_us"], m["steps"],
+            m["ffn_us"], m["ffn_copy_us"], m["max_stall_us"]))
+    lines.append("")
     text = "\n".join(lines)
     if args.out:
         with open(args.out, "w") as fh:

@@ -57,3 +57,49 @@ def test_optimized_placement_sends_each_gpu_its_eq1_load():
         send = share.perm["send_counts"].cpu().numpy().tolist()
         assert send == [int(v) for v in lam]
         assert int(share.perm["group_offsets"][-1]) == int(lam[dev])
+
+
+def test_migration_in_ffn_windows_keeps_serving_then_switches_exactly():
+    """Experts moving in are copied, chunk by chunk, into spare buffers inside the FFN
+    windows of successive steps (Sec. V-B); every step during the migration gives the
+    old placement's output bit for bit, and after the switch the layer gives bit for bit
+    what a share built directly on the new placement gives."""
+    from paper_2607_08782_amd.migration import ExpertStore, Migrator, run_step
+
+    cfg = synth.custom_config(d=256, E=16, k=4, f=256, G=4, zipf=1.2)
+    T = 256
+    inp = synth.make_layer(cfg, T, seed=2, device="cuda", experts="all")
+    P0 = np.ascontiguousarray(inp.placement, dtype=np.uint8)
+    only = lambda j: [e for e in range(cfg.E) if P0[e].sum() == 1 and P0[e, j]]
+    P1 = P0.copy()
+    for a, b in zip(only(0)[:2], only(1)[:2]):          # two experts trade places 0 <-> 1
+        P1[a, 0], P1[a, 1], P1[b, 0], P1[b, 1] = 0, 1, 1, 0
+    assert P1[:, 0].sum() == P0[:, 0].sum() and not np.array_equal(P0, P1)
+    store = ExpertStore(inp.w13, inp.w2)
+    mig = Migrator(store, P0, 0, spare=2, chunk_bytes=32 << 10)
+    w13, w2 = mig.weights()
+    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, P0, 0, w13, w2)
+    share.run()
+    torch.cuda.synchronize()
+    y0 = share.y.clone()
+    moved = mig.plan(P1)
+    assert moved == 2 * store.nbytes(only(1)[0])
+    steps = 0
+    while not mig.finished:
+        run_step(share, mig, budget_bytes=64 << 10)
+        torch.cuda.synchronize()
+        assert torch.equal(share.y, y0)
+        steps += 1
+    assert steps > 1 and mig.stats.bytes == moved
+    w13n, w2n = mig.switch()
+    share.set_placement(P1, w13n, w2n)
+    share.run()
+    torch.cuda.synchronize()
+    local1 = [int(e) for e in np.nonzero(P1[:, 0])[0]]
+    fresh = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, P1, 0, [inp.w13[e] for e in local1],
+                       [inp.w2[e] for e in local1])
+    fresh.run()
+    torch.cuda.synchronize()
+    assert torch.equal(share.y, fresh.y)
+    for e, t13, t2 in zip(local1, w13n, w2n):
+        assert torch.equal(t13, inp.w13[e]) and torch.equal(t2, inp.w2[e])
