@@ -201,6 +201,50 @@ int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets,
 int moe_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* topk_gate,
                 const void* y_shared, int64_t T, int d, int k, void* y, void* stream);
 
+/*
+ * moe_quantize_e4m3 -- per-row FP8 quantization for the quantized routing
+ * predictor (Sec. V-A: a low-bit replica with weights and activations both
+ * quantized; gfx950 multiplies OCP FP8 E4M3 natively).  For every row r:
+ *
+ *   scales[r] = max_i |x[r][i]| / 448          (fp32 division; 1 if the row is 0)
+ *   q[r][i]   = E4M3(x[r][i] / scales[r])      (fp32 division, round to nearest,
+ *                                               ties to even; |.| > 448 saturates)
+ *
+ * E4M3: 1 sign, 4 exponent bits (bias 7), 3 mantissa bits, subnormals, max 448,
+ * no infinities; a value that rounds to zero is stored as +0 (code 0x00).
+ * x       device [rows][cols] of `dtype` (MOE_F32 or MOE_BF16), finite
+ * q       device [rows][cols] uint8 output;  scales device [rows] float output
+ * Requires rows >= 0, cols >= 1.  Results are exact (bitwise reproducible).
+ */
+int moe_quantize_e4m3(const void* x, int dtype, int64_t rows, int cols, uint8_t* q,
+                      float* scales, void* stream);
+
+/*
+ * moe_route_topk_e4m3 -- gate scores of the quantized predictor (Sec. V-A)
+ * and their top-k, whose agreement with moe_route_topk's choice is the
+ * predictor's accuracy (top-k match rate, Sec. VIII):
+ *
+ *   logits[t][e] = x_scale[t] * w_scale[e] * sum_i E4M3(xq[t][i]) * E4M3(wq[e][i])
+ *                  + bias[e]
+ *
+ * then top-k and gates exactly as moe_route_topk does for given scores.
+ * xq       device [T][d] uint8 E4M3 codes, x_scale device [T] float (from
+ *          moe_quantize_e4m3 of the activations)
+ * wq       device [E][d] uint8 E4M3 codes, w_scale device [E] float (of the
+ *          router weights [E][d])
+ * bias     device [E] float, nullable
+ * logits   device [T][E] float output (required: the top-k reads it back)
+ * topk_idx device [T][k] int32 output;  topk_gate device [T][k] float output
+ * flags    MOE_RENORM or 0
+ * Requires d % 64 == 0, xq and wq 16-byte aligned, 1 <= E <= MOE_MAX_E,
+ * 1 <= k <= min(E, MOE_MAX_K), T >= 0.  The code products are exact in fp32;
+ * their sum is accumulated in fp32 in a fixed order (deterministic).
+ */
+int moe_route_topk_e4m3(const uint8_t* xq, const float* x_scale, const uint8_t* wq,
+                        const float* w_scale, const float* bias, int64_t T, int d, int E, int k,
+                        int flags, float* logits, int32_t* topk_idx, float* topk_gate,
+                        void* stream);
+
 #ifdef __cplusplus
 }
 #endif

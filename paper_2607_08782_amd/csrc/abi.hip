@@ -152,4 +152,27 @@ int moe_combine(const void* y_perm, int dtype, const int32_t* token_row, const f
                           (hipStream_t)stream);
 }
 
+int moe_quantize_e4m3(const void* x, int dtype, int64_t rows, int cols, uint8_t* q,
+                      float* scales, void* stream) {
+    if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
+    if (rows < 0 || cols < 1) return MOE_ERR_ARG;
+    if (rows > 0 && (!x || !q || !scales)) return MOE_ERR_ARG;
+    return launch_quantize_e4m3(x, dtype, rows, cols, q, scales, (hipStream_t)stream);
+}
+
+int moe_route_topk_e4m3(const uint8_t* xq, const float* x_scale, const uint8_t* wq,
+                        const float* w_scale, const float* bias, int64_t T, int d, int E, int k,
+                        int flags, float* logits, int32_t* topk_idx, float* topk_gate,
+                        void* stream) {
+    if (T < 0 || E < 1 || E > MOE_MAX_E || k < 1 || k > MOE_MAX_K || k > E) return MOE_ERR_ARG;
+    if (flags & ~MOE_RENORM) return MOE_ERR_ARG;
+    if (T > (int64_t)0x7fffffff * 16) return MOE_ERR_ARG;
+    if (d < 64 || d % 64) return MOE_ERR_SHAPE;
+    if (!wq || !w_scale) return MOE_ERR_ARG;
+    if (T > 0 && (!xq || !x_scale || !logits || !topk_idx || !topk_gate)) return MOE_ERR_ARG;
+    if (!aligned16(wq) || (xq && !aligned16(xq))) return MOE_ERR_ARG;
+    return launch_route_topk_e4m3(xq, x_scale, wq, w_scale, bias, T, d, E, k, flags, logits,
+                                  topk_idx, topk_gate, (hipStream_t)stream);
+}
+
 }  // extern "C"

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "moe.h"
 
 namespace moe {
@@ -44,6 +46,25 @@ inline int launch_status() {
     return e == hipSuccess ? MOE_OK : MOE_ERR_DEVICE;
 }
 
+// Raise kernel F's dynamic-LDS limit to `bytes` on the current device.  The
+// setting persists, so each device is configured once per size increase and
+// later launches skip the runtime call.
+template <auto F>
+inline int allow_dynamic_lds(size_t bytes) {
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> granted[kMaxDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return MOE_ERR_DEVICE;
+    int cur = granted[dev].load(std::memory_order_acquire);
+    if (cur >= (int)bytes) return MOE_OK;
+    if (hipFuncSetAttribute((const void*)F, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)bytes) != hipSuccess)
+        return MOE_ERR_DEVICE;
+    while (cur < (int)bytes && !granted[dev].compare_exchange_weak(cur, (int)bytes)) {
+    }
+    return MOE_OK;
+}
+
 // ---------------------------------------------------------------------------
 // Internal launchers (one translation unit each); arguments already validated.
 // ---------------------------------------------------------------------------
@@ -51,6 +72,12 @@ int launch_route_topk(const void* x, int dtype, const void* w, const float* bias
                       int E, int k, int flags, float* logits, int32_t* idx, float* gate, void* ws,
                       hipStream_t s);
 size_t route_ws_bytes(int dtype, int64_t T, int d, int E, int flags);
+
+int launch_quantize_e4m3(const void* x, int dtype, int64_t rows, int cols, uint8_t* q, float* scales,
+                         hipStream_t s);
+int launch_route_topk_e4m3(const uint8_t* xq, const float* sx, const uint8_t* wq, const float* sw,
+                           const float* bias, int64_t T, int d, int E, int k, int flags,
+                           float* logits, int32_t* idx, float* gate, hipStream_t s);
 
 int launch_histogram(const int32_t* idx, int64_t T, int k, int E, int32_t* counts, int32_t* coact,
                      hipStream_t s);

@@ -5,15 +5,14 @@
 // Each workgroup owns a block of tokens:
 //   phase 1  scores for its tokens x all E experts into LDS
 //            bf16: MFMA 16x16x32, K split over 16 waves, fixed-order reduction;
-//            f32:  plain FMA loops;  logits-in: copied from global memory
+//            f32:  plain FMA loops;  logits-in: read in place from global memory
 //   phase 2  bias added, scores written back coalesced (if requested)
-//   phase 3  one thread per token: insertion top-k over the LDS row, gates.
+//   phase 3  a group of lanes per token: k rounds of a group-wide maximum, gates.
 #include "common.h"
 
 namespace moe {
 namespace {
 
-constexpr int ROUTE_TOKENS = 64;
 constexpr int ROUTE_THREADS = 256;
 constexpr int ROUTE_MAX_SPLIT = 16;    // K chunks of the split score kernel
 
@@ -23,36 +22,112 @@ enum RouteMode { MODE_F32 = 1, MODE_LOGITS_IN = 2, MODE_PARTIALS = 3 };
 int route_split(int64_t T, int d, int E);
 namespace {
 
-// "a ranks before b": larger score, or equal score and lower expert index.
-__device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
-    return va > vb || (va == vb && ia < ib);
+// Top-k of one token by a group of L adjacent lanes (L in {4, ..., 64}, E <= 4L):
+// lane g of the group holds the scores of experts g, g + L, g + 2L, g + 3L as
+// 64-bit keys (order-preserving image of the fp32 score in the high half, the
+// complement of the expert index in the low half), so "larger key" means larger
+// score, ties to the lower index.  Each of the k rounds takes the group-wide
+// maximum key by xor shuffles and retires it.
+__host__ __device__ inline int topk_lanes(int E) {
+    int L = 4;
+    while (L * 4 < E) L *= 2;
+    return L;
 }
 
+__device__ __forceinline__ uint32_t ord_f32(float x) {
+    uint32_t u = __float_as_uint(x);
+    if (u == 0x80000000u) u = 0u;                        // -0 ranks as +0
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ float unord_f32(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o, 64);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), o, 64);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Cross-lane moves inside a row of 16 lanes (DPP): quad_perm [1,0,3,2] and
+// [2,3,0,1], half-row mirror (lane i <- 7 - i) and row mirror (i <- 15 - i).
+// Applied in that order, each pairs every lane with one that holds the
+// result of a disjoint lane set, so the four steps combine 4, 8, 16 lanes.
+constexpr int DPP_QUAD_XOR1 = 0xB1, DPP_QUAD_XOR2 = 0x4E, DPP_HALF_MIRROR = 0x141,
+              DPP_MIRROR = 0x140;
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, 0xf, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, 0xf, 0xf, false);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+// Maximum over each aligned group of L lanes (L in {4, ..., 64}); every lane of
+// the wave must be active.
+__device__ __forceinline__ uint64_t group_max(uint64_t b, int L) {
+    b = umax64(b, dpp_u64<DPP_QUAD_XOR1>(b));
+    b = umax64(b, dpp_u64<DPP_QUAD_XOR2>(b));
+    if (L >= 8) b = umax64(b, dpp_u64<DPP_HALF_MIRROR>(b));
+    if (L >= 16) b = umax64(b, dpp_u64<DPP_MIRROR>(b));
+    if (L >= 32) b = umax64(b, shfl_xor_u64(b, 16));
+    if (L >= 64) b = umax64(b, shfl_xor_u64(b, 32));
+    return b;
+}
+
+// Sum over each aligned group of L lanes, the same value on every lane.
+__device__ __forceinline__ float group_sum(float v, int L) {
+    v += dpp_f32<DPP_QUAD_XOR1>(v);
+    v += dpp_f32<DPP_QUAD_XOR2>(v);
+    if (L >= 8) v += dpp_f32<DPP_HALF_MIRROR>(v);
+    if (L >= 16) v += dpp_f32<DPP_MIRROR>(v);
+    if (L >= 32) v += __shfl_xor(v, 16, 64);
+    if (L >= 64) v += __shfl_xor(v, 32, 64);
+    return v;
+}
+
+// `s` points at the token's E scores (LDS or global memory); every lane of the
+// group must call (valid = false only masks the loads and stores).
 template <int KM>
-__device__ void topk_row(const float* s, int E, int k, bool renorm, int32_t* idx_out,
-                         float* gate_out) {
+__device__ __forceinline__ void topk_group(const float* s, int E, int k, bool renorm, int L, int g,
+                                           bool valid, int32_t* __restrict__ idx_out,
+                                           float* __restrict__ gate_out) {
+    uint64_t key[4];
+    float sv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int e = g + i * L;
+        key[i] = 0;
+        sv[i] = 0.f;
+        if (valid && e < E) {
+            sv[i] = s[e];
+            key[i] = ((uint64_t)ord_f32(sv[i]) << 32) | (uint64_t)(0xffffffffu - (uint32_t)e);
+        }
+    }
     float v[KM];
     int id[KM];
 #pragma unroll
-    for (int j = 0; j < KM; ++j) { v[j] = -__builtin_inff(); id[j] = 0x7fffffff; }
-    float kth_v = -__builtin_inff();
-    int kth_i = 0x7fffffff;
-    for (int e = 0; e < E; ++e) {
-        float x = s[e];
-        if (!better(x, e, kth_v, kth_i)) continue;
+    for (int r = 0; r < KM; ++r) {
+        v[r] = 0.f;
+        id[r] = 0;
+        if (r < k) {
+            uint64_t b = key[0] > key[1] ? key[0] : key[1];
+            const uint64_t c = key[2] > key[3] ? key[2] : key[3];
+            b = group_max(b > c ? b : c, L);
 #pragma unroll
-        for (int j = 0; j < KM; ++j)
-            if (j == k - 1) { v[j] = x; id[j] = e; }
-#pragma unroll
-        for (int j = KM - 1; j > 0; --j) {
-            if (j < k && better(v[j], id[j], v[j - 1], id[j - 1])) {
-                float tv = v[j]; v[j] = v[j - 1]; v[j - 1] = tv;
-                int ti = id[j]; id[j] = id[j - 1]; id[j - 1] = ti;
-            }
+            for (int i = 0; i < 4; ++i)
+                if (key[i] == b) key[i] = 0;
+            v[r] = unord_f32((uint32_t)(b >> 32));
+            id[r] = (int)(0xffffffffu - (uint32_t)b);
         }
-#pragma unroll
-        for (int j = 0; j < KM; ++j)
-            if (j == k - 1) { kth_v = v[j]; kth_i = id[j]; }
     }
     const float m = v[0];
     float denom = 0.f;
@@ -61,40 +136,58 @@ __device__ void topk_row(const float* s, int E, int k, bool renorm, int32_t* idx
         for (int j = 0; j < KM; ++j)
             if (j < k) denom += expf(v[j] - m);
     } else {
-        for (int e = 0; e < E; ++e) denom += expf(s[e] - m);
-    }
-    const float inv = 1.0f / denom;
 #pragma unroll
-    for (int j = 0; j < KM; ++j) {
-        if (j < k) {
-            idx_out[j] = id[j];
-            gate_out[j] = expf(v[j] - m) * inv;
+        for (int i = 0; i < 4; ++i)
+            if (valid && g + i * L < E) denom += expf(sv[i] - m);
+        denom = group_sum(denom, L);
+    }
+    if (valid && g == 0) {
+        const float inv = 1.0f / denom;
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+            if (j < k) {
+                idx_out[j] = id[j];
+                gate_out[j] = expf(v[j] - m) * inv;
+            }
         }
     }
 }
 
+// Top-k of `nt` tokens whose scores sit at S[r * ldS + e] (LDS or global
+// memory), by every lane of the workgroup in groups of topk_lanes(E).
+template <int KM>
+__device__ __forceinline__ void topk_tokens(const float* S, int ldS, int nt, int64_t t0, int E,
+                                            int k, int renorm, int32_t* __restrict__ idx,
+                                            float* __restrict__ gate) {
+    const int L = topk_lanes(E);
+    const int tid = threadIdx.x, groups = blockDim.x / L;
+    const int grp = tid / L, g = tid % L;
+    for (int base = 0; base < nt; base += groups) {
+        const int r = base + grp;
+        const bool valid = r < nt;
+        const int64_t t = t0 + (valid ? r : 0);
+        topk_group<KM>(S + (valid ? r : 0) * ldS, E, k, renorm != 0, L, g, valid, idx + t * k,
+                       gate + t * k);
+    }
+}
+
 // Bias, optional score store and top-k for the `nt` tokens whose scores sit in
-// S[r * ldS + e] (LDS), one thread per token.
+// S[r * ldS + e] (LDS).
 template <int KM>
 __device__ __forceinline__ void finish_tokens(float* S, int ldS, int nt, int64_t t0, int E, int k,
                                               int renorm, const float* __restrict__ bias,
-                                              bool add_bias, float* __restrict__ logits,
+                                              float* __restrict__ logits,
                                               int32_t* __restrict__ idx, float* __restrict__ gate) {
     const int tid = threadIdx.x, nthr = blockDim.x;
-    if (add_bias) {
-        for (int c = tid; c < nt * E; c += nthr) {
-            const int r = c / E, e = c % E;
-            float v = S[r * ldS + e];
-            if (bias) v += bias[e];
-            S[r * ldS + e] = v;
-            if (logits) logits[(t0 + r) * E + e] = v;
-        }
-        __syncthreads();
+    for (int c = tid; c < nt * E; c += nthr) {
+        const int r = c / E, e = c % E;
+        float v = S[r * ldS + e];
+        if (bias) v += bias[e];
+        S[r * ldS + e] = v;
+        if (logits) logits[(t0 + r) * E + e] = v;
     }
-    if (tid < nt) {
-        const int64_t t = t0 + tid;
-        topk_row<KM>(S + tid * ldS, E, k, renorm != 0, idx + t * k, gate + t * k);
-    }
+    __syncthreads();
+    topk_tokens<KM>(S, ldS, nt, t0, E, k, renorm, idx, gate);
 }
 
 // bf16 gate scores on MFMA 16x16x32.  A workgroup of 16 waves owns 16*RT
@@ -112,11 +205,10 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, const float* __restrict__ bias,
     int64_t T, int d, int E, int k, int renorm, float* __restrict__ logits,
     int32_t* __restrict__ idx, float* __restrict__ gate, int S, float* __restrict__ part) {
-    extern __shared__ float smem[];
+    extern __shared__ __attribute__((aligned(16))) float smem[];
     constexpr int ROWS = 16 * RT;
     const int E_pad = (E + 15) & ~15;
     const int ldS = E_pad + 1;
-    const int slice = ROWS * ldS;                     // floats per partial-score slice
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t t0 = (int64_t)blockIdx.x * ROWS;
     const int nt = (int)((T - t0) < ROWS ? (T - t0) : ROWS);
@@ -212,9 +304,13 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
         }
     }
 
-    // fixed-order reduction: slice g = wave & 3 receives waves g, g+4, g+8, g+12 in turn
+    // fixed-order reduction in the MFMA output layout (one 16-byte LDS access per
+    // tile and lane): slice g = wave & 3 receives waves g, g+4, g+8, g+12 in turn,
+    // the four slices are added in order into slice 0, and the sums are laid out
+    // row-major (over slices 1..3) for the epilogue.
     const int g = wave & 3, q = wave >> 2;
-    float* Sg = smem + g * slice;
+    const int nslice = ROWS * E_pad;                  // floats per slice
+    f32x4* Sg = (f32x4*)smem + g * (nslice / 4);
     for (int pass = 0; pass < 4; ++pass) {
         if (q == pass) {
 #pragma unroll
@@ -222,48 +318,57 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
 #pragma unroll
                 for (int j = 0; j < NTM; ++j) {
                     if (j >= NT) continue;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        float* dst = Sg + (i * 16 + (lane >> 4) * 4 + r) * ldS + j * 16 + (lane & 15);
-                        *dst = pass == 0 ? acc[i][j][r] : *dst + acc[i][j][r];
-                    }
+                    f32x4* p = Sg + (i * NT + j) * 64 + lane;
+                    *p = pass == 0 ? acc[i][j] : *p + acc[i][j];
                 }
         }
         __syncthreads();
     }
+    {
+        f32x4* s4 = (f32x4*)smem;
+        const int n4 = nslice / 4;
+        for (int c = tid; c < n4; c += RB_THREADS)
+            s4[c] = ((s4[c] + s4[n4 + c]) + s4[2 * n4 + c]) + s4[3 * n4 + c];
+    }
+    __syncthreads();
+    float* Sm = smem + nslice;
     for (int c = tid; c < ROWS * E_pad; c += RB_THREADS) {
         const int r = c / E_pad, e = c % E_pad;
-        const int o = r * ldS + e;
-        smem[o] = ((smem[o] + smem[slice + o]) + smem[2 * slice + o]) + smem[3 * slice + o];
+        const int rr = r & 15;
+        const int o = (((r >> 4) * NT + (e >> 4)) * 64 + (rr >> 2) * 16 + (e & 15)) * 4 + (rr & 3);
+        Sm[r * ldS + e] = smem[o];
     }
     __syncthreads();
     if (S == 1) {
-        finish_tokens<KM>(smem, ldS, nt, t0, E, k, renorm, bias, true, logits, idx, gate);
+        finish_tokens<KM>(Sm, ldS, nt, t0, E, k, renorm, bias, logits, idx, gate);
     } else {
         // partial scores of this K chunk: part[chunk][t][e]
         for (int c = tid; c < nt * E; c += RB_THREADS) {
             const int r = c / E, e = c % E;
-            part[((int64_t)chunk * T + t0 + r) * E + e] = smem[r * ldS + e];
+            part[((int64_t)chunk * T + t0 + r) * E + e] = Sm[r * ldS + e];
         }
     }
 }
 
-// fp32 scores (plain FMA loops) or scores handed in (MOE_LOGITS_IN): 64 tokens
-// per workgroup of 256 threads.
+// fp32 scores (plain FMA loops), scores handed in (MOE_LOGITS_IN) or K-chunk
+// partial scores to be summed: `tpb` tokens per workgroup of 256 threads, one
+// token per top-k lane group (route_tokens_per_block), so short batches still
+// spread over many workgroups.
 template <int MODE, int KM>
 __global__ __launch_bounds__(ROUTE_THREADS) void route_simple_kernel(
     const float* __restrict__ X, const float* __restrict__ W, const float* __restrict__ bias,
     int64_t T, int d, int E, int k, int renorm, float* __restrict__ logits,
-    int32_t* __restrict__ idx, float* __restrict__ gate, int S, const float* __restrict__ part) {
-    extern __shared__ float smem[];
+    int32_t* __restrict__ idx, float* __restrict__ gate, int S, const float* __restrict__ part,
+    int tpb) {
+    extern __shared__ __attribute__((aligned(16))) float smem[];
     const int ldS = ((E + 15) & ~15) + 1;
     float* Sm = smem;
     const int tid = threadIdx.x;
-    const int64_t t0 = (int64_t)blockIdx.x * ROUTE_TOKENS;
-    const int nt = (int)((T - t0) < ROUTE_TOKENS ? (T - t0) : ROUTE_TOKENS);
+    const int64_t t0 = (int64_t)blockIdx.x * tpb;
+    const int nt = (int)((T - t0) < tpb ? (T - t0) : tpb);
     if (MODE == MODE_F32) {
-        for (int c = tid; c < ROUTE_TOKENS * E; c += ROUTE_THREADS) {
-            const int r = c % ROUTE_TOKENS, e = c / ROUTE_TOKENS;
+        for (int c = tid; c < tpb * E; c += ROUTE_THREADS) {
+            const int r = c % tpb, e = c / tpb;
             float a = 0.f;
             if (r < nt) {
                 const float* xr = X + (t0 + r) * d;
@@ -287,15 +392,16 @@ __global__ __launch_bounds__(ROUTE_THREADS) void route_simple_kernel(
             Sm[r * ldS + e] = sum;
         }
     } else {
-        for (int c = tid; c < nt * E; c += ROUTE_THREADS) {
-            const int r = c / E, e = c % E;
-            Sm[r * ldS + e] = logits[(t0 + r) * E + e];
-        }
+        // scores handed in: top-k straight from global memory
+        topk_tokens<KM>(logits + t0 * E, E, nt, t0, E, k, renorm, idx, gate);
+        return;
     }
     __syncthreads();
-    finish_tokens<KM>(Sm, ldS, nt, t0, E, k, renorm, bias, MODE != MODE_LOGITS_IN, logits, idx,
-                      gate);
+    finish_tokens<KM>(Sm, ldS, nt, t0, E, k, renorm, bias, logits, idx, gate);
 }
+
+// Tokens per workgroup of route_simple_kernel: one per top-k lane group.
+int route_tokens_per_block(int E) { return ROUTE_THREADS / topk_lanes(E); }
 
 // Token rows per workgroup of the bf16 score kernel, by expert count.
 int route_rows(int E) {
@@ -317,10 +423,7 @@ int launch_km(const void* x, int dtype, const void* w, const float* bias, int64_
         float* part = (float*)ws;
 #define MOE_RB_LAUNCH(RT, NTM)                                                                  \
     do {                                                                                        \
-        if (lds > 65536 &&                                                                      \
-            hipFuncSetAttribute((const void*)route_bf16_kernel<RT, NTM, KM>,                    \
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=        \
-                hipSuccess)                                                                     \
+        if (lds > 65536 && allow_dynamic_lds<route_bf16_kernel<RT, NTM, KM>>(lds) != MOE_OK)  \
             return MOE_ERR_DEVICE;                                                              \
         hipLaunchKernelGGL((route_bf16_kernel<RT, NTM, KM>), grid, block, lds, s,               \
                            (const bf16_t*)x, (const bf16_t*)w, bias, T, d, E, k, renorm,        \
@@ -332,23 +435,26 @@ int launch_km(const void* x, int dtype, const void* w, const float* bias, int64_
         else MOE_RB_LAUNCH(1, 16);
 #undef MOE_RB_LAUNCH
         if (S > 1) {
-            const size_t lds2 = (size_t)ROUTE_TOKENS * (E_pad + 1) * sizeof(float);
+            const int tpb = route_tokens_per_block(E);
+            const size_t lds2 = (size_t)tpb * (E_pad + 1) * sizeof(float);
             hipLaunchKernelGGL((route_simple_kernel<MODE_PARTIALS, KM>),
-                               dim3((unsigned)ceil_div(T, ROUTE_TOKENS)), dim3(ROUTE_THREADS),
-                               lds2, s, nullptr, nullptr, bias, T, d, E, k, renorm, logits, idx,
-                               gate, S, (const float*)part);
+                               dim3((unsigned)ceil_div(T, tpb)), dim3(ROUTE_THREADS), lds2, s,
+                               nullptr, nullptr, bias, T, d, E, k, renorm, logits, idx, gate, S,
+                               (const float*)part, tpb);
         }
         return launch_status();
     }
-    const size_t lds = (size_t)ROUTE_TOKENS * (E_pad + 1) * sizeof(float);
-    const dim3 grid((unsigned)ceil_div(T, ROUTE_TOKENS)), block(ROUTE_THREADS);
+    const int tpb = route_tokens_per_block(E);
+    const size_t lds = (size_t)tpb * (E_pad + 1) * sizeof(float);
+    const dim3 grid((unsigned)ceil_div(T, tpb)), block(ROUTE_THREADS);
     if (flags & MOE_LOGITS_IN)
-        hipLaunchKernelGGL((route_simple_kernel<MODE_LOGITS_IN, KM>), grid, block, lds, s, nullptr,
-                           nullptr, nullptr, T, d, E, k, renorm, logits, idx, gate, 1, nullptr);
+        hipLaunchKernelGGL((route_simple_kernel<MODE_LOGITS_IN, KM>), grid, block, 0, s, nullptr,
+                           nullptr, nullptr, T, d, E, k, renorm, logits, idx, gate, 1, nullptr,
+                           tpb);
     else
         hipLaunchKernelGGL((route_simple_kernel<MODE_F32, KM>), grid, block, lds, s,
                            (const float*)x, (const float*)w, bias, T, d, E, k, renorm, logits,
-                           idx, gate, 1, nullptr);
+                           idx, gate, 1, nullptr, tpb);
     return launch_status();
 }
 

@@ -26,7 +26,8 @@ MOE_MAX_E, MOE_MAX_K, MOE_MAX_G, MOE_MAX_GROUPS = 256, 16, 64, 128
 
 EXPORTS = ("moe_status_string", "moe_route_topk", "moe_route_topk_ws_bytes",
            "moe_expert_histogram", "moe_permute_ws_bytes",
-           "moe_permute", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_combine")
+           "moe_permute", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_combine",
+           "moe_quantize_e4m3", "moe_route_topk_e4m3")
 
 _lib = None
 
@@ -64,6 +65,10 @@ def load_library(path: str = LIB_PATH):
     lib.moe_grouped_ffn.restype = I
     lib.moe_combine.argtypes = [P, I, P, P, P, L, I, I, P, P]
     lib.moe_combine.restype = I
+    lib.moe_quantize_e4m3.argtypes = [P, I, L, I, P, P, P]
+    lib.moe_quantize_e4m3.restype = I
+    lib.moe_route_topk_e4m3.argtypes = [P, P, P, P, P, L, I, I, I, I, P, P, P, P]
+    lib.moe_route_topk_e4m3.restype = I
     _lib = lib
     return lib
 
@@ -150,6 +155,49 @@ def moe_route_topk(x: Optional[torch.Tensor], w_router: Optional[torch.Tensor],
                             _dev(topk_gate, "topk_gate", torch.float32), _dev(ws, "ws"),
                             0 if ws is None else ws.numel(), _stream(stream))
     _check("moe_route_topk", st)
+    return logits, topk_idx, topk_gate
+
+
+def moe_quantize_e4m3(x: torch.Tensor, *, q: Optional[torch.Tensor] = None,
+                      scales: Optional[torch.Tensor] = None, stream=None):
+    """Per-row E4M3 codes (uint8 [rows, cols]) and fp32 scales ([rows]) of x."""
+    lib = load_library()
+    rows, cols = x.shape
+    if q is None:
+        q = _empty((rows, cols), torch.uint8, x.device)
+    if scales is None:
+        scales = _empty((rows,), torch.float32, x.device)
+    st = lib.moe_quantize_e4m3(_dev(x, "x"), _dtype_code(x), rows, cols, _dev(q, "q", torch.uint8),
+                               _dev(scales, "scales", torch.float32), _stream(stream))
+    _check("moe_quantize_e4m3", st)
+    return q, scales
+
+
+def moe_route_topk_e4m3(xq: torch.Tensor, x_scale: torch.Tensor, wq: torch.Tensor,
+                        w_scale: torch.Tensor, bias: Optional[torch.Tensor], k: int, *,
+                        renorm: bool = True, logits: Optional[torch.Tensor] = None,
+                        topk_idx: Optional[torch.Tensor] = None,
+                        topk_gate: Optional[torch.Tensor] = None, stream=None):
+    """Quantized-predictor scores + top-k.  Returns (logits, topk_idx, topk_gate)."""
+    lib = load_library()
+    T, d = xq.shape
+    E = wq.shape[0]
+    if wq.shape[1] != d:
+        raise ValueError("wq must be [E, d]")
+    if logits is None:
+        logits = _empty((T, E), torch.float32, xq.device)
+    if topk_idx is None:
+        topk_idx = _empty((T, k), torch.int32, xq.device)
+    if topk_gate is None:
+        topk_gate = _empty((T, k), torch.float32, xq.device)
+    st = lib.moe_route_topk_e4m3(_dev(xq, "xq", torch.uint8), _dev(x_scale, "x_scale", torch.float32),
+                                 _dev(wq, "wq", torch.uint8), _dev(w_scale, "w_scale", torch.float32),
+                                 _dev(bias, "bias", torch.float32), T, d, E, k,
+                                 MOE_RENORM if renorm else 0,
+                                 _dev(logits, "logits", torch.float32),
+                                 _dev(topk_idx, "topk_idx", torch.int32),
+                                 _dev(topk_gate, "topk_gate", torch.float32), _stream(stream))
+    _check("moe_route_topk_e4m3", st)
     return logits, topk_idx, topk_gate
 
 

@@ -1,0 +1,136 @@
+"""Accuracy and cost of the FP8 quantized routing predictor (Sec. V-A), measured
+on this GPU.
+
+For each model-shaped layer the router weights are quantized once (per
+expert row, E4M3) and every batch's hidden states per token; the predictor's
+top-k is compared with the bf16 gate's (``moe_route_topk``) by the top-k match
+rate of Sec. VIII, over several batches of the drifting synthetic workload.
+Cost: device time of the bf16 gate vs. the predictor (activation quantization
+plus FP8 scores and top-k), median of timed repetitions.
+
+    python -m paper_2607_08782_amd.predictor_study --out profiles/predictor_e4m3.md
+"""
+from __future__ import annotations
+
+import argparse
+import os
+import statistics
+import sys
+
+import numpy as np
+import torch
+
+if __package__ in (None, ""):
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    __package__ = "paper_2607_08782_amd"
+
+from . import moe, synth  # noqa: E402
+
+CASES = [("mixtral_8x7b", "prefill"), ("mixtral_8x7b", "decode"),
+         ("deepseek_v2_lite", "prefill"), ("deepseek_v2_lite", "decode"),
+         ("qwen15_moe_a27b", "batch"),
+         ("qwen3_30b_a3b", "prefill"), ("qwen3_30b_a3b", "decode")]
+
+
+def match_rate(pred: torch.Tensor, true: torch.Tensor) -> float:
+    """Mean over tokens of |predicted top-k & true top-k| / k (on the GPU)."""
+    k = true.shape[1]
+    hit = (pred[:, :, None] == true[:, None, :]).any(dim=2).sum()
+    return float(hit) / max(1, true.numel()) if true.numel() else 1.0
+
+
+def _time_us(fn, reps: int) -> float:
+    """Device time per call: `reps` calls captured in one graph, the replay timed
+    with events (host launch overhead excluded)."""
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(reps):
+            fn()
+    g.replay()
+    torch.cuda.synchronize()
+    out = []
+    for _ in range(5):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        g.replay()
+        b.record()
+        b.synchronize()
+        out.append(a.elapsed_time(b) * 1e3 / reps)
+    return statistics.median(out)
+
+
+def run_case(name: str, regime: str, batches: int, reps: int) -> dict:
+    cfg = synth.CONFIGS[name]
+    T = cfg.T(regime)
+    rates, top1 = [], []
+    for b in range(batches):
+        inp = synth.make_layer(cfg, T, seed=0, device="cuda", batch=b, experts="none")
+        wq, sw = moe.moe_quantize_e4m3(inp.Wr)
+        _, ref_idx, _ = moe.moe_route_topk(inp.X, inp.Wr, inp.bias, cfg.k, want_logits=False)
+        xq, sx = moe.moe_quantize_e4m3(inp.X)
+        _, idx, _ = moe.moe_route_topk_e4m3(xq, sx, wq, sw, inp.bias, cfg.k)
+        rates.append(match_rate(idx, ref_idx))
+        top1.append(float((idx[:, 0] == ref_idx[:, 0]).float().mean()))
+    # cost, on the last batch's inputs with outputs and workspace preallocated
+    logits = torch.empty(T, cfg.E, device="cuda")
+    i0 = torch.empty(T, cfg.k, dtype=torch.int32, device="cuda")
+    g0 = torch.empty(T, cfg.k, device="cuda")
+    need = moe.moe_route_topk_ws_bytes(moe.MOE_BF16, T, cfg.d, cfg.E, moe.MOE_RENORM)
+    ws = moe.workspace(need, "cuda") if need else None
+    xq = torch.empty(T, cfg.d, dtype=torch.uint8, device="cuda")
+    sx = torch.empty(T, device="cuda")
+    bf16 = _time_us(lambda: moe.moe_route_topk(inp.X, inp.Wr, inp.bias, cfg.k, logits=logits,
+                                               topk_idx=i0, topk_gate=g0, ws=ws), reps)
+    quant = _time_us(lambda: moe.moe_quantize_e4m3(inp.X, q=xq, scales=sx), reps)
+    qroute = _time_us(lambda: moe.moe_route_topk_e4m3(xq, sx, wq, sw, inp.bias, cfg.k, logits=logits,
+                                                      topk_idx=i0, topk_gate=g0), reps)
+    w_bytes = cfg.E * cfg.d * 2
+    return {"name": name, "regime": regime, "T": T, "d": cfg.d, "E": cfg.E, "k": cfg.k,
+            "match": statistics.mean(rates), "match_min": min(rates), "top1": statistics.mean(top1),
+            "bf16_us": bf16, "quant_us": quant, "qroute_us": qroute,
+            "w_bytes": w_bytes, "wq_bytes": cfg.E * cfg.d + cfg.E * 4}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--batches", type=int, default=4)
+    ap.add_argument("--reps", type=int, default=20)
+    ap.add_argument("--out", default=None)
+    args = ap.parse_args(argv)
+    if not torch.cuda.is_available():
+        raise SystemExit("the study runs on the GPU; no GPU is visible")
+    rows = []
+    for name, regime in CASES:
+        r = run_case(name, regime, args.batches, args.reps)
+        print("%s/%s: match %.4f (min %.4f) top1 %.4f | bf16 %.1f us, quant %.1f + fp8 %.1f us" % (
+            name, regime, r["match"], r["match_min"], r["top1"], r["bf16_us"], r["quant_us"],
+            r["qroute_us"]), flush=True)
+        rows.append(r)
+    lines = ["# FP8 (E4M3) quantized routing predictor: accuracy and cost", "",
+             "Router weights quantized once per expert row, hidden states per token (scale =",
+             "row max / 448, round to nearest even); scores by the FP8 matrix cores with fp32",
+             "accumulation; top-k as for the bf16 gate.  Accuracy: top-k match rate against the",
+             "bf16 gate's choice (Sec. VIII), mean over %d batches of the drifting synthetic" % args.batches,
+             "workload (seeded normal hidden states, N(0, 0.02) router, Zipf popularity bias);",
+             "top-1: fraction of tokens whose first choice agrees.  Cost: device time per call,",
+             "%d calls captured in one graph, replay timed with events (median of 5)." % args.reps, "",
+             "Command: `python -m paper_2607_08782_amd.predictor_study --batches %d --reps %d --out %s`"
+             % (args.batches, args.reps, args.out), "",
+             "| layer | T | d | E | k | match rate | min over batches | top-1 agree | bf16 gate us | quantize x us | FP8 scores+top-k us | router bytes bf16 -> fp8 |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append("| %s/%s | %d | %d | %d | %d | %.4f | %.4f | %.4f | %.1f | %.1f | %.1f | %d -> %d |" % (
+            r["name"], r["regime"], r["T"], r["d"], r["E"], r["k"], r["match"], r["match_min"],
+            r["top1"], r["bf16_us"], r["quant_us"], r["qroute_us"], r["w_bytes"], r["wq_bytes"]))
+    lines.append("")
+    text = "\n".join(lines)
+    if args.out:
+        with open(args.out, "w") as fh:
+            fh.write(text)
+    print(text)
+
+
+if __name__ == "__main__":
+    main()

@@ -152,3 +152,29 @@ def test_workspace_sizes(lib):
     assert 0 < a < b
     assert lib.moe_grouped_ffn_ws_bytes(1, 100, 256, 128, 4) >= 100 * 128 * 2
     assert lib.moe_grouped_ffn_ws_bytes(0, 100, 256, 128, 4) >= 100 * 128 * 4
+
+
+def test_quantize_e4m3_validation(lib):
+    f = lib.moe_quantize_e4m3
+    assert f(FAKE, 2, 4, 64, FAKE, FAKE, None) == moe.MOE_ERR_ARG      # dtype
+    assert f(FAKE, 1, -1, 64, FAKE, FAKE, None) == moe.MOE_ERR_ARG     # rows < 0
+    assert f(FAKE, 1, 4, 0, FAKE, FAKE, None) == moe.MOE_ERR_ARG       # cols < 1
+    assert f(FAKE, 1, 4, 64, None, FAKE, None) == moe.MOE_ERR_ARG      # q
+    assert f(FAKE, 1, 4, 64, FAKE, None, None) == moe.MOE_ERR_ARG      # scales
+
+
+def test_route_topk_e4m3_validation(lib):
+    f = lib.moe_route_topk_e4m3
+
+    def call(xq=FAKE, wq=FAKE, T=4, d=128, E=8, k=2, flags=1, lg=FAKE):
+        return f(xq, FAKE, wq, FAKE, None, T, d, E, k, flags, lg, FAKE, FAKE, None)
+    assert call(d=96) == moe.MOE_ERR_SHAPE                  # d % 64
+    assert call(d=0) == moe.MOE_ERR_SHAPE
+    assert call(E=0) == moe.MOE_ERR_ARG
+    assert call(E=257) == moe.MOE_ERR_ARG
+    assert call(k=9) == moe.MOE_ERR_ARG                     # k > E
+    assert call(k=17, E=64) == moe.MOE_ERR_ARG              # k > MOE_MAX_K
+    assert call(flags=2) == moe.MOE_ERR_ARG                 # scores are computed here
+    assert call(lg=None) == moe.MOE_ERR_ARG                 # logits are required
+    assert call(wq=ctypes.c_void_p(0x1008)) == moe.MOE_ERR_ARG   # 16-byte alignment
+    assert call(xq=None) == moe.MOE_ERR_ARG

@@ -134,6 +134,28 @@ def test_ties_all_equal_and_signed_zero_logits():
     close(np32(share.topk_gate), og, 1e-5, "gates")
 
 
+@pytest.mark.parametrize("E", [1, 3, 8, 16, 17, 60, 64, 65, 128, 129, 200, 256])
+@pytest.mark.parametrize("renorm", [True, False])
+def test_topk_of_given_scores_with_ties_every_width(E, renorm):
+    """Top-k over handed-in scores: few distinct levels (many ties), signed zeros,
+    a ragged token count; indices bit-exact, gates within 1e-5."""
+    T = 100
+    rng = np.random.default_rng(E * 2 + renorm)
+    L = (rng.integers(-3, 4, size=(T, E)) * 0.5).astype(np.float32)
+    z = L == 0
+    L[z] = np.where(rng.random(int(z.sum())) < 0.5, np.float32(-0.0), np.float32(0.0))
+    L[: T // 2] += rng.standard_normal((T // 2, E)).astype(np.float32)
+    Lg = torch.from_numpy(L).cuda()
+    for k in sorted({1, min(2, E), min(E, 6), min(E, 16)}):
+        say("[topk]", E, k, renorm)
+        _, idx, gate = moe.moe_route_topk(None, None, None, k, logits=Lg, logits_in=True,
+                                          renorm=renorm)
+        torch.cuda.synchronize()
+        oidx, og = oracle.topk(L, k, renorm=renorm)
+        np.testing.assert_array_equal(idx.cpu().numpy(), oidx)
+        close(np32(gate), og, 1e-5, "gates")
+
+
 def test_every_token_to_one_expert_and_a_gpu_with_no_rows():
     cfg = synth.custom_config(d=128, E=8, k=2, f=128, G=2)
     T = 150
