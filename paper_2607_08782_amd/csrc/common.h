@@ -79,6 +79,17 @@ int launch_route_topk_e4m3(const uint8_t* xq, const float* sx, const uint8_t* wq
                            const float* bias, int64_t T, int d, int E, int k, int flags,
                            float* logits, int32_t* idx, float* gate, hipStream_t s);
 
+// Tiled score kernel (score.hip): K chunks for a batch, 0 if the shape does not
+// suit it; launch with S chunks (S == 1 writes scores + bias to out[T][E],
+// S > 1 partial scores to out[S][T][E], to be summed in chunk order).
+int score_tiles_split(int64_t T, int rowbytes, int E, bool allow_split);
+int launch_score_tiles(bool fp8, const void* x, const void* w, const float* sx, const float* sw,
+                       const float* bias, int64_t T, int rowbytes, int E, int S, float* out,
+                       hipStream_t s);
+// Top-k and gates of given scores (route.hip): scores[T][E] read in place.
+int launch_topk_given(const float* scores, int64_t T, int E, int k, int flags, int32_t* idx,
+                      float* gate, hipStream_t s);
+
 int launch_histogram(const int32_t* idx, int64_t T, int k, int E, int32_t* counts, int32_t* coact,
                      hipStream_t s);
 

@@ -125,12 +125,13 @@ __global__ __launch_bounds__(QTHREADS) void quantize_rows_vec_kernel(const T* __
 #pragma unroll
         for (int i = 0; i < CH; ++i) {
             const int c = tid + i * QTHREADS;
-            if (c < nchunk) {
-                load8(xr + c * 8, v[i]);
+            load8(xr + (c < nchunk ? c : 0) * 8, v[i]);     // in-bounds, masked below
+        }
+#pragma unroll
+        for (int i = 0; i < CH; ++i)
+            if (tid + i * QTHREADS < nchunk)
 #pragma unroll
                 for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(v[i][j]));
-            }
-        }
         for (int c = tid + CH * QTHREADS; c < nchunk; c += QTHREADS) {
             float t[8];
             load8(xr + c * 8, t);
@@ -158,26 +159,25 @@ __global__ __launch_bounds__(QTHREADS) void quantize_rows_vec_kernel(const T* __
 // 64-byte K step; A and B use the same K order, so the sum runs over all K.
 // Wave w takes the K steps w, w + QR_WAVES, ... with the next step's operands
 // loaded while the current step's products run.
+constexpr uint32_t QR_RSRC_WORD3 = 0x00020000;     // raw buffer, 32-bit data format
+constexpr int QR_OOB = 0x7fffffc0;                 // an offset past every descriptor's range
+
+__device__ __forceinline__ i32x8 qr_load32(__amdgpu_buffer_rsrc_t r, int voff) {
+    const uint4 lo = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+    const uint4 hi = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 16, 0));
+    return (i32x8){(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+}
+
+// Operands of one 64-byte K step at byte kb: rows past the block's tokens or
+// past E fall outside the descriptors and read as zero, so every load is
+// issued unconditionally (the compiler keeps them in flight).
 template <int ET>
-__device__ __forceinline__ void qroute_load(const uint8_t* __restrict__ xrow, bool tvalid,
-                                            const uint8_t* __restrict__ wq, int d, int E, int row,
-                                            int kb, i32x8& a, i32x8 (&b)[ET]) {
-    a = (i32x8){0, 0, 0, 0, 0, 0, 0, 0};
-    if (tvalid) {
-        const uint4* pa = (const uint4*)(xrow + kb);
-        const uint4 a0 = pa[0], a1 = pa[1];
-        a = (i32x8){(int)a0.x, (int)a0.y, (int)a0.z, (int)a0.w, (int)a1.x, (int)a1.y, (int)a1.z, (int)a1.w};
-    }
+__device__ __forceinline__ void qroute_load(__amdgpu_buffer_rsrc_t xr, __amdgpu_buffer_rsrc_t wr,
+                                            int d, int row, int kb, bool valid, i32x8& a,
+                                            i32x8 (&b)[ET]) {
+    a = qr_load32(xr, valid ? row * d + kb : QR_OOB);
 #pragma unroll
-    for (int j = 0; j < ET; ++j) {
-        const int e = j * 32 + row;
-        b[j] = (i32x8){0, 0, 0, 0, 0, 0, 0, 0};
-        if (e < E) {
-            const uint4* pb = (const uint4*)(wq + (int64_t)e * d + kb);
-            const uint4 b0 = pb[0], b1 = pb[1];
-            b[j] = (i32x8){(int)b0.x, (int)b0.y, (int)b0.z, (int)b0.w, (int)b1.x, (int)b1.y, (int)b1.z, (int)b1.w};
-        }
-    }
+    for (int j = 0; j < ET; ++j) b[j] = qr_load32(wr, valid ? (j * 32 + row) * d + kb : QR_OOB);
 }
 
 template <int ET>
@@ -189,36 +189,47 @@ __global__ __launch_bounds__(QR_WAVES * 64) void qroute_kernel(
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t t0 = (int64_t)blockIdx.x * QR_TOKENS;
     const int row = lane & 31, half = lane >> 5;
-    const int64_t trow = t0 + row;
-    const bool tvalid = trow < T;
-    const uint8_t* xrow = xq + (tvalid ? trow : 0) * d;
+    const int nt = (int)((T - t0) < QR_TOKENS ? (T - t0) : QR_TOKENS);
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(xq + t0 * d), (short)0, nt * d, QR_RSRC_WORD3);
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)wq, (short)0, E * d, QR_RSRC_WORD3);
     f32x16 acc[ET];
 #pragma unroll
     for (int j = 0; j < ET; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+    // wave w takes K steps w, w + QR_WAVES, ...; the loads of a step past its
+    // last get out-of-range offsets (zeros, no memory traffic), so the loops
+    // have no branches around loads and the compiler's waits stay exact
     const int ksteps = d / 64;
-    i32x8 a, b[ET];
-    if (wave < ksteps) qroute_load<ET>(xrow, tvalid, wq, d, E, row, wave * 64 + half * 32, a, b);
-    constexpr bool PREFETCH = ET <= 4;         // registers for a second operand set
-    for (int ks = wave; ks < ksteps; ks += QR_WAVES) {
-        const int kn = ks + QR_WAVES;
-        if (PREFETCH) {
-            i32x8 an, bn[ET];
-            if (kn < ksteps) qroute_load<ET>(xrow, tvalid, wq, d, E, row, kn * 64 + half * 32, an, bn);
+    const int n_mine = wave < ksteps ? (ksteps - wave + QR_WAVES - 1) / QR_WAVES : 0;
+    const int koff = half * 32;
+    auto mma = [&](const i32x8& a_, const i32x8 (&b_)[ET]) {
 #pragma unroll
-            for (int j = 0; j < ET; ++j)
-                acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b[j], acc[j], 0, 0, 0, 127, 0, 127);
-            if (kn < ksteps) {
-                a = an;
-#pragma unroll
-                for (int j = 0; j < ET; ++j) b[j] = bn[j];
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < ET; ++j)
-                acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b[j], acc[j], 0, 0, 0, 127, 0, 127);
-            if (kn < ksteps) qroute_load<ET>(xrow, tvalid, wq, d, E, row, kn * 64 + half * 32, a, b);
+        for (int j = 0; j < ET; ++j)
+            acc[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a_, b_[j], acc[j], 0, 0, 0, 127,
+                                                                     0, 127);
+    };
+    auto kb_of = [&](int i) { return (wave + i * QR_WAVES) * 64 + koff; };
+    if constexpr (ET <= 4) {
+        // two steps of loads in flight (ring of two operand sets, by step parity)
+        i32x8 a0, b0[ET], a1, b1[ET];
+        qroute_load<ET>(xr, wr, d, row, kb_of(0), 0 < n_mine, a0, b0);
+        qroute_load<ET>(xr, wr, d, row, kb_of(1), 1 < n_mine, a1, b1);
+        for (int i = 0; i < n_mine; i += 2) {
+            mma(a0, b0);
+            qroute_load<ET>(xr, wr, d, row, kb_of(i + 2), i + 2 < n_mine, a0, b0);
+            mma(a1, b1);                          // zeros when i + 1 == n_mine
+            qroute_load<ET>(xr, wr, d, row, kb_of(i + 3), i + 3 < n_mine, a1, b1);
+        }
+    } else {
+        // eight expert tiles: registers for one operand set
+        i32x8 a, b[ET];
+        qroute_load<ET>(xr, wr, d, row, kb_of(0), 0 < n_mine, a, b);
+        for (int i = 0; i < n_mine; ++i) {
+            mma(a, b);
+            qroute_load<ET>(xr, wr, d, row, kb_of(i + 1), i + 1 < n_mine, a, b);
         }
     }
     // fixed-order reduction in the MFMA output layout: slice g = wave & 1
@@ -295,6 +306,11 @@ int launch_route_topk_e4m3(const uint8_t* xq, const float* sx, const uint8_t* wq
                            const float* bias, int64_t T, int d, int E, int k, int flags,
                            float* logits, int32_t* idx, float* gate, hipStream_t s) {
     if (T == 0) return MOE_OK;
+    if (score_tiles_split(T, d, E, false) == 1) {  // long batch over many experts
+        const int st = launch_score_tiles(true, xq, wq, sx, sw, bias, T, d, E, 1, logits, s);
+        if (st != MOE_OK) return st;
+        return launch_topk_given(logits, T, E, k, flags, idx, gate, s);
+    }
     const unsigned grid = (unsigned)ceil_div(T, QR_TOKENS);
     const int et = (int)ceil_div(E, 32);
 #define QR(N)                                                                                   \
@@ -306,8 +322,7 @@ int launch_route_topk_e4m3(const uint8_t* xq, const float* sx, const uint8_t* wq
 #undef QR
     const int st = launch_status();
     if (st != MOE_OK) return st;
-    return launch_route_topk(nullptr, MOE_F32, nullptr, nullptr, T, 0, E, k,
-                             (flags & MOE_RENORM) | MOE_LOGITS_IN, logits, idx, gate, nullptr, s);
+    return launch_topk_given(logits, T, E, k, flags, idx, gate, s);
 }
 
 }  // namespace moe

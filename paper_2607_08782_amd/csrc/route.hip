@@ -4,16 +4,19 @@
 //
 // Each workgroup owns a block of tokens:
 //   phase 1  scores for its tokens x all E experts into LDS
-//            bf16: MFMA 16x16x32, K split over 16 waves, fixed-order reduction;
+//            bf16: MFMA 16x16x32, K split over 16 waves, fixed-order reduction
+//            (long batches over more than 32 experts use the tiled kernel of
+//            score.hip instead);
 //            f32:  plain FMA loops;  logits-in: read in place from global memory
 //   phase 2  bias added, scores written back coalesced (if requested)
 //   phase 3  a group of lanes per token: k rounds of a group-wide maximum, gates.
 #include "common.h"
+#include "topk.h"
 
 namespace moe {
 namespace {
 
-constexpr int ROUTE_THREADS = 256;
+constexpr int ROUTE_THREADS = TOPK_THREADS;
 constexpr int ROUTE_MAX_SPLIT = 16;    // K chunks of the split score kernel
 
 enum RouteMode { MODE_F32 = 1, MODE_LOGITS_IN = 2, MODE_PARTIALS = 3 };
@@ -21,174 +24,6 @@ enum RouteMode { MODE_F32 = 1, MODE_LOGITS_IN = 2, MODE_PARTIALS = 3 };
 }  // namespace
 int route_split(int64_t T, int d, int E);
 namespace {
-
-// Top-k of one token by a group of L adjacent lanes (L in {4, ..., 64}, E <= 4L):
-// lane g of the group holds the scores of experts g, g + L, g + 2L, g + 3L as
-// 64-bit keys (order-preserving image of the fp32 score in the high half, the
-// complement of the expert index in the low half), so "larger key" means larger
-// score, ties to the lower index.  Each of the k rounds takes the group-wide
-// maximum key by xor shuffles and retires it.
-__host__ __device__ inline int topk_lanes(int E) {
-    int L = 4;
-    while (L * 4 < E) L *= 2;
-    return L;
-}
-
-__device__ __forceinline__ uint32_t ord_f32(float x) {
-    uint32_t u = __float_as_uint(x);
-    if (u == 0x80000000u) u = 0u;                        // -0 ranks as +0
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-__device__ __forceinline__ float unord_f32(uint32_t k) {
-    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
-}
-
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
-    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, o, 64);
-    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), o, 64);
-    return ((uint64_t)hi << 32) | lo;
-}
-
-// Cross-lane moves inside a row of 16 lanes (DPP): quad_perm [1,0,3,2] and
-// [2,3,0,1], half-row mirror (lane i <- 7 - i) and row mirror (i <- 15 - i).
-// Applied in that order, each pairs every lane with one that holds the
-// result of a disjoint lane set, so the four steps combine 4, 8, 16 lanes.
-constexpr int DPP_QUAD_XOR1 = 0xB1, DPP_QUAD_XOR2 = 0x4E, DPP_HALF_MIRROR = 0x141,
-              DPP_MIRROR = 0x140;
-
-template <int CTRL>
-__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
-    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, 0xf, 0xf, false);
-    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, 0xf, 0xf, false);
-    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
-}
-
-template <int CTRL>
-__device__ __forceinline__ float dpp_f32(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
-}
-
-__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
-
-// Maximum over each aligned group of L lanes (L in {4, ..., 64}); every lane of
-// the wave must be active.
-__device__ __forceinline__ uint64_t group_max(uint64_t b, int L) {
-    b = umax64(b, dpp_u64<DPP_QUAD_XOR1>(b));
-    b = umax64(b, dpp_u64<DPP_QUAD_XOR2>(b));
-    if (L >= 8) b = umax64(b, dpp_u64<DPP_HALF_MIRROR>(b));
-    if (L >= 16) b = umax64(b, dpp_u64<DPP_MIRROR>(b));
-    if (L >= 32) b = umax64(b, shfl_xor_u64(b, 16));
-    if (L >= 64) b = umax64(b, shfl_xor_u64(b, 32));
-    return b;
-}
-
-// Sum over each aligned group of L lanes, the same value on every lane.
-__device__ __forceinline__ float group_sum(float v, int L) {
-    v += dpp_f32<DPP_QUAD_XOR1>(v);
-    v += dpp_f32<DPP_QUAD_XOR2>(v);
-    if (L >= 8) v += dpp_f32<DPP_HALF_MIRROR>(v);
-    if (L >= 16) v += dpp_f32<DPP_MIRROR>(v);
-    if (L >= 32) v += __shfl_xor(v, 16, 64);
-    if (L >= 64) v += __shfl_xor(v, 32, 64);
-    return v;
-}
-
-// `s` points at the token's E scores (LDS or global memory); every lane of the
-// group must call (valid = false only masks the loads and stores).
-template <int KM>
-__device__ __forceinline__ void topk_group(const float* s, int E, int k, bool renorm, int L, int g,
-                                           bool valid, int32_t* __restrict__ idx_out,
-                                           float* __restrict__ gate_out) {
-    uint64_t key[4];
-    float sv[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int e = g + i * L;
-        key[i] = 0;
-        sv[i] = 0.f;
-        if (valid && e < E) {
-            sv[i] = s[e];
-            key[i] = ((uint64_t)ord_f32(sv[i]) << 32) | (uint64_t)(0xffffffffu - (uint32_t)e);
-        }
-    }
-    float v[KM];
-    int id[KM];
-#pragma unroll
-    for (int r = 0; r < KM; ++r) {
-        v[r] = 0.f;
-        id[r] = 0;
-        if (r < k) {
-            uint64_t b = key[0] > key[1] ? key[0] : key[1];
-            const uint64_t c = key[2] > key[3] ? key[2] : key[3];
-            b = group_max(b > c ? b : c, L);
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (key[i] == b) key[i] = 0;
-            v[r] = unord_f32((uint32_t)(b >> 32));
-            id[r] = (int)(0xffffffffu - (uint32_t)b);
-        }
-    }
-    const float m = v[0];
-    float denom = 0.f;
-    if (renorm) {
-#pragma unroll
-        for (int j = 0; j < KM; ++j)
-            if (j < k) denom += expf(v[j] - m);
-    } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            if (valid && g + i * L < E) denom += expf(sv[i] - m);
-        denom = group_sum(denom, L);
-    }
-    if (valid && g == 0) {
-        const float inv = 1.0f / denom;
-#pragma unroll
-        for (int j = 0; j < KM; ++j) {
-            if (j < k) {
-                idx_out[j] = id[j];
-                gate_out[j] = expf(v[j] - m) * inv;
-            }
-        }
-    }
-}
-
-// Top-k of `nt` tokens whose scores sit at S[r * ldS + e] (LDS or global
-// memory), by every lane of the workgroup in groups of topk_lanes(E).
-template <int KM>
-__device__ __forceinline__ void topk_tokens(const float* S, int ldS, int nt, int64_t t0, int E,
-                                            int k, int renorm, int32_t* __restrict__ idx,
-                                            float* __restrict__ gate) {
-    const int L = topk_lanes(E);
-    const int tid = threadIdx.x, groups = blockDim.x / L;
-    const int grp = tid / L, g = tid % L;
-    for (int base = 0; base < nt; base += groups) {
-        const int r = base + grp;
-        const bool valid = r < nt;
-        const int64_t t = t0 + (valid ? r : 0);
-        topk_group<KM>(S + (valid ? r : 0) * ldS, E, k, renorm != 0, L, g, valid, idx + t * k,
-                       gate + t * k);
-    }
-}
-
-// Bias, optional score store and top-k for the `nt` tokens whose scores sit in
-// S[r * ldS + e] (LDS).
-template <int KM>
-__device__ __forceinline__ void finish_tokens(float* S, int ldS, int nt, int64_t t0, int E, int k,
-                                              int renorm, const float* __restrict__ bias,
-                                              float* __restrict__ logits,
-                                              int32_t* __restrict__ idx, float* __restrict__ gate) {
-    const int tid = threadIdx.x, nthr = blockDim.x;
-    for (int c = tid; c < nt * E; c += nthr) {
-        const int r = c / E, e = c % E;
-        float v = S[r * ldS + e];
-        if (bias) v += bias[e];
-        S[r * ldS + e] = v;
-        if (logits) logits[(t0 + r) * E + e] = v;
-    }
-    __syncthreads();
-    topk_tokens<KM>(S, ldS, nt, t0, E, k, renorm, idx, gate);
-}
 
 // bf16 gate scores on MFMA 16x16x32.  A workgroup of 16 waves owns 16*RT
 // tokens; wave w takes the K steps w, w+16, w+32, ... (32 elements each) for
@@ -199,8 +34,14 @@ __device__ __forceinline__ void finish_tokens(float* S, int ldS, int nt, int64_t
 // turn), so the scores are deterministic.
 constexpr int RB_WAVES = 16;
 constexpr int RB_THREADS = RB_WAVES * 64;
+constexpr uint32_t RB_RSRC_WORD3 = 0x00020000;     // raw buffer, 32-bit data format
+constexpr int RB_OOB = 0x7ffffff0;                 // an offset past every descriptor's range
 
-template <int RT, int NTM, int KM>
+__device__ __forceinline__ uint4 rb_load16(__amdgpu_buffer_rsrc_t r, int voff) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+}
+
+template <int RT, int NTM, int KM, int C>
 __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, const float* __restrict__ bias,
     int64_t T, int d, int E, int k, int renorm, float* __restrict__ logits,
@@ -215,8 +56,19 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
     const int NT = E_pad / 16;
     const int row = lane & 15, kq = (lane >> 4) * 8;
 
-    const bf16_t* xbase = X + (t0 + row) * d + kq;       // token row `row` of tile 0
-    const bf16_t* wbase = W + (int64_t)row * d + kq;     // expert row `row` of tile 0
+    // operands through buffer descriptors: rows past the block's tokens or past E
+    // fall outside them and read as zero, and a masked lane (K past d, a tile past
+    // the experts) gets an offset outside them too, so every load is issued
+    // unconditionally and the compiler can keep several in flight
+    const __amdgpu_buffer_rsrc_t xrsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(X + t0 * d), (short)0, nt * d * 2, RB_RSRC_WORD3);
+    const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)W, (short)0, E * d * 2, RB_RSRC_WORD3);
+    int xoff[RT], woff[NTM];
+#pragma unroll
+    for (int i = 0; i < RT; ++i) xoff[i] = ((i * 16 + row) * d + kq) * 2;
+#pragma unroll
+    for (int j = 0; j < NTM; ++j) woff[j] = ((j * 16 + row) * d + kq) * 2;   // j >= NT: rows >= E
     f32x4 acc[RT][NTM];
 #pragma unroll
     for (int i = 0; i < RT; ++i)
@@ -231,44 +83,38 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
     const int nsteps = send - sbeg;
     if (NTM <= 4) {
         // all tiles' fragments of one K step fit in registers: keep two steps of
-        // loads in flight (ring of two register sets, alternating by step parity)
+        // loads in flight (ring of two register sets, alternating by step parity).
+        // Loads past this wave's last step get out-of-range offsets (zeros, no
+        // memory traffic), so the loop has no branches and the waits are exact.
         uint4 av[2][RT], bv[2][NTM];
-        auto load = [&](int step, uint4* a_, uint4* b_) {
-            const int k0 = step * 32;
-            const bool kin = k0 + kq < d;
+        const int n_mine = wave < nsteps ? (nsteps - wave + RB_WAVES - 1) / RB_WAVES : 0;
+        const int s0 = sbeg + wave;
+        auto load = [&](int i, uint4* a_, uint4* b_) {
+            const int k0 = (s0 + i * RB_WAVES) * 32;
+            const bool kin = i < n_mine && k0 + kq < d;
 #pragma unroll
-            for (int i = 0; i < RT; ++i) {
-                a_[i] = make_uint4(0, 0, 0, 0);
-                if (kin && i * 16 + row < nt) a_[i] = *(const uint4*)(xbase + (int64_t)i * 16 * d + k0);
-            }
+            for (int r = 0; r < RT; ++r) a_[r] = rb_load16(xrsrc, kin ? xoff[r] + k0 * 2 : RB_OOB);
 #pragma unroll
-            for (int j = 0; j < NTM; ++j) {
-                b_[j] = make_uint4(0, 0, 0, 0);
-                if (kin && j < NT && j * 16 + row < E)
-                    b_[j] = *(const uint4*)(wbase + (int64_t)j * 16 * d + k0);
-            }
+            for (int j = 0; j < NTM; ++j) b_[j] = rb_load16(wrsrc, kin ? woff[j] + k0 * 2 : RB_OOB);
         };
+        // every tile, also those past the experts (their operands read as zero):
+        // a branch here would make the compiler wait for every load in flight
         auto mma = [&](const uint4* a_, const uint4* b_) {
 #pragma unroll
             for (int i = 0; i < RT; ++i)
 #pragma unroll
                 for (int j = 0; j < NTM; ++j)
-                    if (j < NT)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            __builtin_bit_cast(bf16x8, a_[i]), __builtin_bit_cast(bf16x8, b_[j]),
-                            acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8, a_[i]), __builtin_bit_cast(bf16x8, b_[j]),
+                        acc[i][j], 0, 0, 0);
         };
-        const int n_mine = wave < nsteps ? (nsteps - wave + RB_WAVES - 1) / RB_WAVES : 0;
-        const int s0 = sbeg + wave;
-        if (n_mine > 0) load(s0, av[0], bv[0]);
-        if (n_mine > 1) load(s0 + RB_WAVES, av[1], bv[1]);
+        load(0, av[0], bv[0]);
+        load(1, av[1], bv[1]);
         for (int i = 0; i < n_mine; i += 2) {
             mma(av[0], bv[0]);
-            if (i + 2 < n_mine) load(s0 + (i + 2) * RB_WAVES, av[0], bv[0]);
-            if (i + 1 < n_mine) {
-                mma(av[1], bv[1]);
-                if (i + 3 < n_mine) load(s0 + (i + 3) * RB_WAVES, av[1], bv[1]);
-            }
+            load(i + 2, av[0], bv[0]);
+            mma(av[1], bv[1]);                    // zeros when i + 1 == n_mine
+            load(i + 3, av[1], bv[1]);
         }
     } else {
         for (int step = sbeg + wave; step < send; step += RB_WAVES) {
@@ -276,23 +122,16 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
             const bool kin = k0 + kq < d;
             bf16x8 a[RT];
 #pragma unroll
-            for (int i = 0; i < RT; ++i) {
-                uint4 v = make_uint4(0, 0, 0, 0);
-                if (kin && i * 16 + row < nt) v = *(const uint4*)(xbase + (int64_t)i * 16 * d + k0);
-                a[i] = __builtin_bit_cast(bf16x8, v);
-            }
+            for (int i = 0; i < RT; ++i)
+                a[i] = __builtin_bit_cast(bf16x8, rb_load16(xrsrc, kin ? xoff[i] + k0 * 2 : RB_OOB));
 #pragma unroll
             for (int jc = 0; jc < NTM; jc += 4) {
                 if (jc >= NT) break;
                 bf16x8 b[4];
 #pragma unroll
-                for (int jj = 0; jj < 4; ++jj) {
-                    const int j = jc + jj;
-                    uint4 v = make_uint4(0, 0, 0, 0);
-                    if (kin && j < NT && j * 16 + row < E)
-                        v = *(const uint4*)(wbase + (int64_t)j * 16 * d + k0);
-                    b[jj] = __builtin_bit_cast(bf16x8, v);
-                }
+                for (int jj = 0; jj < 4; ++jj)
+                    b[jj] = __builtin_bit_cast(bf16x8,
+                                               rb_load16(wrsrc, kin ? woff[jc + jj] + k0 * 2 : RB_OOB));
 #pragma unroll
                 for (int i = 0; i < RT; ++i)
 #pragma unroll
@@ -340,7 +179,8 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
     }
     __syncthreads();
     if (S == 1) {
-        finish_tokens<KM>(Sm, ldS, nt, t0, E, k, renorm, bias, logits, idx, gate);
+        // 1024 threads hold at least one lane group per token: one token per group
+        finish_tokens<KM, C, 1>(Sm, ldS, nt, t0, E, k, renorm, bias, logits, idx, gate);
     } else {
         // partial scores of this K chunk: part[chunk][t][e]
         for (int c = tid; c < nt * E; c += RB_THREADS) {
@@ -352,9 +192,9 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
 
 // fp32 scores (plain FMA loops), scores handed in (MOE_LOGITS_IN) or K-chunk
 // partial scores to be summed: `tpb` tokens per workgroup of 256 threads, one
-// token per top-k lane group (route_tokens_per_block), so short batches still
+// token per top-k lane group (topk_tokens_per_block), so short batches still
 // spread over many workgroups.
-template <int MODE, int KM>
+template <int MODE, int KM, int C>
 __global__ __launch_bounds__(ROUTE_THREADS) void route_simple_kernel(
     const float* __restrict__ X, const float* __restrict__ W, const float* __restrict__ bias,
     int64_t T, int d, int E, int k, int renorm, float* __restrict__ logits,
@@ -378,30 +218,30 @@ __global__ __launch_bounds__(ROUTE_THREADS) void route_simple_kernel(
             Sm[r * ldS + e] = a;
         }
     } else if (MODE == MODE_PARTIALS) {
-        // K chunks summed in chunk order
+        // K chunks summed in chunk order.  Chunks are split only for short
+        // batches, where a thread has few elements: per element, all
+        // ROUTE_MAX_SPLIT chunk loads go out together (unconditionally, clamped to
+        // chunk S - 1 and masked by a 0/1 factor), one round trip per element
+        const float* pb = part + t0 * E;
+        const int64_t cs = T * E;                     // chunk stride
         for (int c = tid; c < nt * E; c += ROUTE_THREADS) {
-            const int r = c / E, e = c % E;
-            const float* p = part + (t0 + r) * E + e;
-            const int64_t cs = T * E;                // chunk stride
-            float v[ROUTE_MAX_SPLIT];
+            float x[ROUTE_MAX_SPLIT];
 #pragma unroll
-            for (int ch = 0; ch < ROUTE_MAX_SPLIT; ++ch) v[ch] = ch < S ? p[ch * cs] : 0.f;
+            for (int ch = 0; ch < ROUTE_MAX_SPLIT; ++ch) x[ch] = pb[(ch < S ? ch : S - 1) * cs + c];
             float sum = 0.f;
 #pragma unroll
-            for (int ch = 0; ch < ROUTE_MAX_SPLIT; ++ch) sum += v[ch];
+            for (int ch = 0; ch < ROUTE_MAX_SPLIT; ++ch) sum = fmaf(x[ch], ch < S ? 1.0f : 0.0f, sum);
+            const int r = c / E, e = c - r * E;
             Sm[r * ldS + e] = sum;
         }
     } else {
         // scores handed in: top-k straight from global memory
-        topk_tokens<KM>(logits + t0 * E, E, nt, t0, E, k, renorm, idx, gate);
+        topk_tokens<KM, C>(logits + t0 * E, E, nt, t0, E, k, renorm, idx, gate);
         return;
     }
     __syncthreads();
-    finish_tokens<KM>(Sm, ldS, nt, t0, E, k, renorm, bias, logits, idx, gate);
+    finish_tokens<KM, C>(Sm, ldS, nt, t0, E, k, renorm, bias, logits, idx, gate);
 }
-
-// Tokens per workgroup of route_simple_kernel: one per top-k lane group.
-int route_tokens_per_block(int E) { return ROUTE_THREADS / topk_lanes(E); }
 
 // Token rows per workgroup of the bf16 score kernel, by expert count.
 int route_rows(int E) {
@@ -409,50 +249,77 @@ int route_rows(int E) {
     return 16 * (E_pad <= 16 ? 4 : (E_pad <= 128 ? 2 : 1));
 }
 
-template <int KM>
-int launch_km(const void* x, int dtype, const void* w, const float* bias, int64_t T, int d,
+// Tokens per workgroup of route_simple_kernel: at most one pass of the top-k
+// lane groups, and few enough that a short batch still spreads over >= 128
+// workgroups (the chunk sums and the top-k are latency-bound per workgroup).
+int simple_tokens_per_block(int64_t T, int E) {
+    const int cap = topk_tokens_per_block(E);
+    const int64_t want = ceil_div(T, 128);
+    return want >= cap ? cap : (want < 1 ? 1 : (int)want);
+}
+
+template <int KM, int C>
+int launch_kmv(const void* x, int dtype, const void* w, const float* bias, int64_t T, int d,
               int E, int k, int flags, float* logits, int32_t* idx, float* gate, void* ws,
               hipStream_t s) {
     const int renorm = (flags & MOE_RENORM) ? 1 : 0;
     const int E_pad = (E + 15) & ~15;
     if (!(flags & MOE_LOGITS_IN) && dtype == MOE_BF16) {
         const int rows = route_rows(E);
-        const int S = route_split(T, d, E);
+        const int St = score_tiles_split(T, 2 * d, E, true);
+        const int S = St > 0 ? St : route_split(T, d, E);
         const size_t lds = (size_t)4 * rows * (E_pad + 1) * sizeof(float);
         const dim3 grid((unsigned)ceil_div(T, rows), (unsigned)S), block(RB_THREADS);
         float* part = (float*)ws;
+        if (St > 0) {
+            // long batch over many experts: the tiled score kernel; with one K
+            // chunk its scores (bias added) go to `logits`, or to the workspace
+            float* out = (St == 1 && logits) ? logits : part;
+            const int st = launch_score_tiles(false, x, w, nullptr, nullptr, bias, T, 2 * d, E,
+                                              St, out, s);
+            if (st != MOE_OK) return st;
+            if (St == 1) {
+                const int tpb = simple_tokens_per_block(T, E);
+                hipLaunchKernelGGL((route_simple_kernel<MODE_LOGITS_IN, KM, C>),
+                                   dim3((unsigned)ceil_div(T, tpb)), dim3(ROUTE_THREADS), 0, s,
+                                   nullptr, nullptr, nullptr, T, d, E, k, renorm, out, idx, gate, 1,
+                                   nullptr, tpb);
+                return launch_status();
+            }
+        } else {
 #define MOE_RB_LAUNCH(RT, NTM)                                                                  \
     do {                                                                                        \
-        if (lds > 65536 && allow_dynamic_lds<route_bf16_kernel<RT, NTM, KM>>(lds) != MOE_OK)  \
+        if (lds > 65536 && allow_dynamic_lds<route_bf16_kernel<RT, NTM, KM, C>>(lds) != MOE_OK)  \
             return MOE_ERR_DEVICE;                                                              \
-        hipLaunchKernelGGL((route_bf16_kernel<RT, NTM, KM>), grid, block, lds, s,               \
+        hipLaunchKernelGGL((route_bf16_kernel<RT, NTM, KM, C>), grid, block, lds, s,               \
                            (const bf16_t*)x, (const bf16_t*)w, bias, T, d, E, k, renorm,        \
                            logits, idx, gate, S, part);                                         \
     } while (0)
-        if (E_pad <= 16) MOE_RB_LAUNCH(4, 1);
-        else if (E_pad <= 64) MOE_RB_LAUNCH(2, 4);
-        else if (E_pad <= 128) MOE_RB_LAUNCH(2, 8);
+        if constexpr (C == 0) MOE_RB_LAUNCH(4, 1);          // E <= 16
+        else if constexpr (C <= 2) MOE_RB_LAUNCH(2, 4);     // E <= 64
+        else if constexpr (C == 3) MOE_RB_LAUNCH(2, 8);     // E <= 128
         else MOE_RB_LAUNCH(1, 16);
 #undef MOE_RB_LAUNCH
+        }
         if (S > 1) {
-            const int tpb = route_tokens_per_block(E);
+            const int tpb = simple_tokens_per_block(T, E);
             const size_t lds2 = (size_t)tpb * (E_pad + 1) * sizeof(float);
-            hipLaunchKernelGGL((route_simple_kernel<MODE_PARTIALS, KM>),
+            hipLaunchKernelGGL((route_simple_kernel<MODE_PARTIALS, KM, C>),
                                dim3((unsigned)ceil_div(T, tpb)), dim3(ROUTE_THREADS), lds2, s,
                                nullptr, nullptr, bias, T, d, E, k, renorm, logits, idx, gate, S,
                                (const float*)part, tpb);
         }
         return launch_status();
     }
-    const int tpb = route_tokens_per_block(E);
+    const int tpb = simple_tokens_per_block(T, E);
     const size_t lds = (size_t)tpb * (E_pad + 1) * sizeof(float);
     const dim3 grid((unsigned)ceil_div(T, tpb)), block(ROUTE_THREADS);
     if (flags & MOE_LOGITS_IN)
-        hipLaunchKernelGGL((route_simple_kernel<MODE_LOGITS_IN, KM>), grid, block, 0, s, nullptr,
+        hipLaunchKernelGGL((route_simple_kernel<MODE_LOGITS_IN, KM, C>), grid, block, 0, s, nullptr,
                            nullptr, nullptr, T, d, E, k, renorm, logits, idx, gate, 1, nullptr,
                            tpb);
     else
-        hipLaunchKernelGGL((route_simple_kernel<MODE_F32, KM>), grid, block, lds, s,
+        hipLaunchKernelGGL((route_simple_kernel<MODE_F32, KM, C>), grid, block, lds, s,
                            (const float*)x, (const float*)w, bias, T, d, E, k, renorm, logits,
                            idx, gate, 1, nullptr, tpb);
     return launch_status();
@@ -474,18 +341,38 @@ int route_split(int64_t T, int d, int E) {
 
 size_t route_ws_bytes(int dtype, int64_t T, int d, int E, int flags) {
     if ((flags & MOE_LOGITS_IN) || dtype != MOE_BF16 || T <= 0) return 0;
-    const int S = route_split(T, d, E);
-    return S > 1 ? (size_t)S * (size_t)T * (size_t)E * sizeof(float) : 0;
+    const int St = score_tiles_split(T, 2 * d, E, true);
+    const int S = St > 0 ? St : route_split(T, d, E);
+    // the tiled kernel with one chunk keeps its scores here when none are requested
+    return (S > 1 || St == 1) ? (size_t)S * (size_t)T * (size_t)E * sizeof(float) : 0;
+}
+
+int launch_topk_given(const float* scores, int64_t T, int E, int k, int flags, int32_t* idx,
+                      float* gate, hipStream_t s) {
+    return launch_route_topk(nullptr, MOE_F32, nullptr, nullptr, T, 0, E, k,
+                             (flags & MOE_RENORM) | MOE_LOGITS_IN, (float*)scores, idx, gate,
+                             nullptr, s);
 }
 
 int launch_route_topk(const void* x, int dtype, const void* w, const float* bias, int64_t T, int d,
                       int E, int k, int flags, float* logits, int32_t* idx, float* gate, void* ws,
                       hipStream_t s) {
     if (T == 0) return MOE_OK;
-    if (k <= 2) return launch_km<2>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, ws, s);
-    if (k <= 4) return launch_km<4>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, ws, s);
-    if (k <= 8) return launch_km<8>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, ws, s);
-    return launch_km<16>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, ws, s);
+#define MOE_KC(KM, C) launch_kmv<KM, C>(x, dtype, w, bias, T, d, E, k, flags, logits, idx, gate, ws, s)
+#define MOE_KMV(KM)                                                                              \
+    switch (topk_class(E)) {                                                                     \
+        case 0: return MOE_KC(KM, 0);                                                            \
+        case 1: return MOE_KC(KM, 1);                                                            \
+        case 2: return MOE_KC(KM, 2);                                                            \
+        case 3: return MOE_KC(KM, 3);                                                            \
+        default: return MOE_KC(KM, 4);                                                           \
+    }
+    if (k <= 2) MOE_KMV(2);
+    if (k <= 4) MOE_KMV(4);
+    if (k <= 8) MOE_KMV(8);
+    MOE_KMV(16);
+#undef MOE_KMV
+#undef MOE_KC
 }
 
 }  // namespace moe

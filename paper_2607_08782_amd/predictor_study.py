@@ -98,11 +98,14 @@ def main(argv=None):
     ap.add_argument("--batches", type=int, default=4)
     ap.add_argument("--reps", type=int, default=20)
     ap.add_argument("--out", default=None)
+    ap.add_argument("--cases", default=None,
+                    help="comma-separated name/regime pairs (default: all seven layer shapes)")
     args = ap.parse_args(argv)
     if not torch.cuda.is_available():
         raise SystemExit("the study runs on the GPU; no GPU is visible")
+    cases = CASES if not args.cases else [tuple(c.split("/")) for c in args.cases.split(",")]
     rows = []
-    for name, regime in CASES:
+    for name, regime in cases:
         r = run_case(name, regime, args.batches, args.reps)
         print("%s/%s: match %.4f (min %.4f) top1 %.4f | bf16 %.1f us, quant %.1f + fp8 %.1f us" % (
             name, regime, r["match"], r["match_min"], r["top1"], r["bf16_us"], r["quant_us"],

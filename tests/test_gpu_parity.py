@@ -13,7 +13,7 @@ from paper_2607_08782_amd import moe, synth
 from paper_2607_08782_amd.layer import LayerShare
 
 from parity import (Case, check_end_to_end_routing, check_ffn_and_combine, check_logits,
-                    check_routing, close, np32, say, OUT_TOL)
+                    check_routing, close, np32, say, GATE_TOL, OUT_TOL)
 
 pytestmark = pytest.mark.gpu
 
@@ -72,6 +72,25 @@ def test_model_shaped_layer_share(name, regime):
     worst = check_ffn_and_combine(case, idx, gate, pm, sample=6)
     differ = check_end_to_end_routing(case, ref_logits)
     say("  worst rel err %.2e, top-k sets differing from the oracle: %.4f" % (worst, differ))
+
+
+TILED = [  # (T, d, E, k): batches of >= 192 64-token tiles over > 32 experts take the tiled kernel
+    (12225, 128, 33, 2),      # the smallest batch and width that take it; one K stage
+    (12290, 256, 96, 8),      # two 32-expert tiles per wave
+    (12300, 256, 130, 5),     # four (E > 128)
+]
+
+
+@pytest.mark.parametrize("T,d,E,k", TILED)
+def test_tiled_gate_scores_and_topk_every_element(T, d, E, k):
+    cfg = synth.custom_config(d=d, E=E, k=k, f=64, G=1)
+    say("[tiled]", T, d, E, k)
+    case = Case(cfg, T)
+    check_logits(case)
+    gl = np32(case.share.logits)
+    oidx, og = oracle.topk(gl, k)
+    np.testing.assert_array_equal(case.share.topk_idx.cpu().numpy(), oidx)
+    close(np32(case.share.topk_gate), og, GATE_TOL, "gates")
 
 
 def test_drift_sequence_swaps_placement_without_reallocating():

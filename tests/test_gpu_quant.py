@@ -99,6 +99,9 @@ SMALL = [  # (T, d, E, k, bias)
     (130, 192, 33, 3, True),
     (65, 4096, 8, 2, True),
     (0, 128, 16, 2, True),
+    (12300, 256, 130, 5, True),      # >= 192 64-token tiles over > 32 experts: the tiled kernel
+    (12290, 128, 40, 3, False),
+    (12225, 256, 96, 8, True),
 ]
 
 
