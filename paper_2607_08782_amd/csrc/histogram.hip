@@ -73,10 +73,52 @@ __global__ __launch_bounds__(HIST_THREADS) void histogram_kernel(
             if (co_lds[i]) atomicAdd(&coact[i], co_lds[i]);
 }
 
+// Counts only, up to HF_MAX entries (T*k) in one workgroup: entry e = tid + j*1024
+// (coalesced, all sixteen loads of a thread issued together from clamped
+// indices), per-wave bins in LDS (atomics contend only within a wave), then the
+// waves' bins summed and stored directly: one launch, no clearing pass.
+constexpr int HF_THREADS = 1024;
+constexpr int HF_PER = 16;
+constexpr int HF_MAX = HF_THREADS * HF_PER;
+
+__global__ __launch_bounds__(HF_THREADS) void histogram_flat_kernel(const int32_t* __restrict__ idx,
+                                                                   int n, int E,
+                                                                   int32_t* __restrict__ counts) {
+    __shared__ int32_t bins[HF_THREADS / 64][MOE_MAX_E];
+    const int tid = threadIdx.x, wave = tid >> 6;
+    for (int i = tid; i < (HF_THREADS / 64) * MOE_MAX_E; i += HF_THREADS) (&bins[0][0])[i] = 0;
+    int v[HF_PER];
+#pragma unroll
+    for (int j = 0; j < HF_PER; ++j) {
+        const int e = tid + j * HF_THREADS;
+        v[j] = idx[e < n ? e : 0];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < HF_PER; ++j) {
+        const int e = tid + j * HF_THREADS;
+        // out-of-range expert ids are ignored rather than counted out of bounds
+        if (e < n && (unsigned)v[j] < (unsigned)E) atomicAdd(&bins[wave][v[j]], 1);
+    }
+    __syncthreads();
+    for (int i = tid; i < E; i += HF_THREADS) {
+        int c = 0;
+#pragma unroll
+        for (int w = 0; w < HF_THREADS / 64; ++w) c += bins[w][i];
+        counts[i] = c;
+    }
+}
+
 }  // namespace
 
 int launch_histogram(const int32_t* idx, int64_t T, int k, int E, int32_t* counts, int32_t* coact,
                      hipStream_t s) {
+    // counts of up to HF_MAX assignments: one workgroup, one launch
+    if (!coact && T > 0 && T * k <= HF_MAX) {
+        hipLaunchKernelGGL(histogram_flat_kernel, dim3(1), dim3(HF_THREADS), 0, s, idx,
+                           (int)(T * k), E, counts);
+        return launch_status();
+    }
     // short batches (decode): one workgroup, bins stored directly, one launch
     if (T <= DIRECT_MAX_TOKENS && (!coact || E <= LDS_COACT_MAX_E)) {
         if (coact)

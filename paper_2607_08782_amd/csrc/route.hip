@@ -246,7 +246,10 @@ __global__ __launch_bounds__(ROUTE_THREADS) void route_simple_kernel(
 // Token rows per workgroup of the bf16 score kernel, by expert count.
 int route_rows(int E) {
     const int E_pad = (E + 15) & ~15;
-    return 16 * (E_pad <= 16 ? 4 : (E_pad <= 128 ? 2 : 1));
+    // E <= 16: 16 tokens per workgroup (the router rows are a few KB, so small
+    // token blocks cost little re-reading, and a long batch then fills the chip
+    // without splitting K and a second launch)
+    return 16 * (E_pad <= 16 ? 1 : (E_pad <= 128 ? 2 : 1));
 }
 
 // Tokens per workgroup of route_simple_kernel: at most one pass of the top-k
@@ -295,7 +298,7 @@ int launch_kmv(const void* x, int dtype, const void* w, const float* bias, int64
                            (const bf16_t*)x, (const bf16_t*)w, bias, T, d, E, k, renorm,        \
                            logits, idx, gate, S, part);                                         \
     } while (0)
-        if constexpr (C == 0) MOE_RB_LAUNCH(4, 1);          // E <= 16
+        if constexpr (C == 0) MOE_RB_LAUNCH(1, 1);          // E <= 16
         else if constexpr (C <= 2) MOE_RB_LAUNCH(2, 4);     // E <= 64
         else if constexpr (C == 3) MOE_RB_LAUNCH(2, 8);     // E <= 128
         else MOE_RB_LAUNCH(1, 16);
