@@ -29,20 +29,72 @@ struct HostTable {
     int16_t expert_of_slot[MOE_MAX_GROUPS];
 };
 
-__device__ __forceinline__ void build_bits(const int32_t* __restrict__ idx, int64_t T, int k, int E,
-                                           const int16_t* __restrict__ slot_of, int n_local,
-                                           unsigned long long* bits, int lane, int64_t t) {
-    for (int s = lane; s < n_local; s += PERM_TOKENS) bits[s] = 0ull;
-    __syncthreads();
-    if (t < T) {
-        for (int r = 0; r < k; ++r) {
-            const int e = idx[t * k + r];
-            if ((unsigned)e >= (unsigned)E) continue;
-            const int s = slot_of[e];
-            if (s >= 0) atomicOr(&bits[s], 1ull << lane);
+// The k expert ids (and gates) of token t, every load issued before the first
+// use: k ids behind one wait instead of k dependent round trips.  Lanes past
+// k re-read id k-1 of the same row.
+__device__ __forceinline__ void load_ids(const int32_t* __restrict__ idx, int64_t t, int k,
+                                         int (&ev)[MOE_MAX_K]) {
+#pragma unroll
+    for (int r = 0; r < MOE_MAX_K; ++r) ev[r] = idx[t * k + (r < k ? r : k - 1)];
+}
+
+__device__ __forceinline__ void load_gates(const float* __restrict__ gate, int64_t t, int k,
+                                           float (&gv)[MOE_MAX_K]) {
+#pragma unroll
+    for (int r = 0; r < MOE_MAX_K; ++r) gv[r] = gate[t * k + (r < k ? r : k - 1)];
+}
+
+// Bit `lane` of bits[s] set iff this lane's token has an assignment to local slot s.
+__device__ __forceinline__ void set_bits(const int (&ev)[MOE_MAX_K], bool valid, int k, int E,
+                                         const int16_t* slot_of, unsigned long long* bits,
+                                         int lane) {
+    if (!valid) return;
+#pragma unroll
+    for (int r = 0; r < MOE_MAX_K; ++r) {
+        if (r >= k) break;
+        const int e = ev[r];
+        const int s = (unsigned)e < (unsigned)E ? (int)slot_of[e] : -1;
+        if (s >= 0) atomicOr(&bits[s], 1ull << lane);
+    }
+}
+
+// Rows of the replica range: of expert e's c assignments, the host of rank q
+// among its n hosts takes [q c / n, (q+1) c / n).
+__device__ __forceinline__ int64_t replica_lo(int q, int64_t c, int n) {
+    return (int64_t)q * c / n;
+}
+
+// send_s[j] += rows GPU j receives from every expert it hosts; the counts of
+// the E experts sit in cnt_s.  Integer adds, so the order does not matter.
+__device__ __forceinline__ void add_send_counts(const int32_t* cnt_s, const uint64_t* hosts,
+                                                int E, int tid, int nthr, int32_t* send_s) {
+    for (int e = tid; e < E; e += nthr) {
+        uint64_t h = hosts[e];
+        const int64_t c = cnt_s[e];
+        const int n = __popcll(h);
+        for (int q = 0; h; ++q, h &= h - 1ull) {
+            const int j = __builtin_ctzll(h);
+            atomicAdd(&send_s[j], (int32_t)(replica_lo(q + 1, c, n) - replica_lo(q, c, n)));
         }
     }
-    __syncthreads();
+}
+
+// off[0] = 0, off[i + 1] = size[0] + ... + size[i] for i < n; one whole wave.
+__device__ __forceinline__ void wave_offsets(const int32_t* size, int n, int32_t* off, int lane) {
+    int32_t carry = 0;
+    for (int c0 = 0; c0 < n; c0 += 64) {
+        const int i = c0 + lane;
+        const int32_t v = i < n ? size[i] : 0;
+        int32_t incl = v;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int32_t u = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += u;
+        }
+        if (i < n) off[i + 1] = carry + incl;
+        carry += __shfl(incl, 63, 64);
+    }
+    if (lane == 0) off[0] = 0;
 }
 
 __global__ __launch_bounds__(PERM_TOKENS) void perm_count_kernel(
@@ -51,69 +103,99 @@ __global__ __launch_bounds__(PERM_TOKENS) void perm_count_kernel(
     __shared__ unsigned long long bits[MOE_MAX_GROUPS];
     __shared__ int16_t slot_lds[MOE_MAX_E];
     const int lane = threadIdx.x;
-    for (int e = lane; e < E; e += PERM_TOKENS) slot_lds[e] = tab.slot_of[e];
     const int64_t blk = blockIdx.x;
-    build_bits(idx, T, k, E, slot_lds, n_local, bits, lane, blk * PERM_TOKENS + lane);
+    const int64_t t = blk * PERM_TOKENS + lane;
+    int ev[MOE_MAX_K];
+    if (t < T) load_ids(idx, t, k, ev);
+    for (int e = lane; e < E; e += PERM_TOKENS) slot_lds[e] = tab.slot_of[e];
+    for (int s = lane; s < n_local; s += PERM_TOKENS) bits[s] = 0ull;
+    __syncthreads();
+    set_bits(ev, t < T, k, E, slot_lds, bits, lane);
+    __syncthreads();
     for (int s = lane; s < n_local; s += PERM_TOKENS)
         blk_counts[blk * n_local + s] = __popcll(bits[s]);
 }
 
-__global__ __launch_bounds__(256) void perm_scan_kernel(
+constexpr int SCAN_THREADS = 1024;
+constexpr int SCAN_WAVES = SCAN_THREADS / 64;
+constexpr int SCAN_TILE = 8192;          // block counts staged in LDS per pass
+
+__global__ __launch_bounds__(SCAN_THREADS) void perm_scan_kernel(
     const int32_t* __restrict__ counts, HostTable tab, int E, int n_local, int G, int dev,
     int64_t nblk, int32_t* __restrict__ blk_counts, int32_t* __restrict__ group_offsets,
     int32_t* __restrict__ lo_out, int32_t* __restrict__ send_counts) {
-    __shared__ int32_t size_s[MOE_MAX_GROUPS];
-    const int tid = threadIdx.x;
-    const uint64_t below = dev == 0 ? 0ull : (~0ull >> (64 - dev));
+    __shared__ uint64_t hosts_s[MOE_MAX_E];
+    __shared__ int32_t cnt_s[MOE_MAX_E];
+    __shared__ int32_t size_s[MOE_MAX_GROUPS], carry_s[MOE_MAX_GROUPS];
+    __shared__ int32_t send_s[MOE_MAX_G];
+    __shared__ int32_t tile[SCAN_TILE];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    for (int e = tid; e < E; e += SCAN_THREADS) {
+        cnt_s[e] = counts[e];
+        hosts_s[e] = tab.hosts[e];
+    }
+    if (tid < MOE_MAX_G) send_s[tid] = 0;
+    if (tid < MOE_MAX_GROUPS) carry_s[tid] = 0;
+    __syncthreads();
     if (tid < n_local) {
         const int e = tab.expert_of_slot[tid];
-        const int64_t c = counts[e];
-        const uint64_t h = tab.hosts[e];
+        const uint64_t h = hosts_s[e];
         const int n = __popcll(h);
-        const int q = __popcll(h & below);
-        const int64_t lo = (int64_t)q * c / n;
-        const int64_t hi = (int64_t)(q + 1) * c / n;
-        size_s[tid] = (int32_t)(hi - lo);
+        const int q = dev == 0 ? 0 : __popcll(h & (~0ull >> (64 - dev)));
+        const int64_t lo = replica_lo(q, cnt_s[e], n);
+        size_s[tid] = (int32_t)(replica_lo(q + 1, cnt_s[e], n) - lo);
         lo_out[tid] = (int32_t)lo;
     }
-    if (send_counts && tid < G) {
-        const uint64_t below_j = tid == 0 ? 0ull : (~0ull >> (64 - tid));
-        int64_t sum = 0;
-        for (int e = 0; e < E; ++e) {
-            const uint64_t h = tab.hosts[e];
-            if (!((h >> tid) & 1ull)) continue;
-            const int64_t c = counts[e];
-            const int n = __popcll(h);
-            const int q = __popcll(h & below_j);
-            sum += (int64_t)(q + 1) * c / n - (int64_t)q * c / n;
-        }
-        send_counts[tid] = (int32_t)sum;
-    }
+    if (send_counts) add_send_counts(cnt_s, hosts_s, E, tid, SCAN_THREADS, send_s);
     __syncthreads();
-    if (tid == 0) {
-        int32_t run = 0;
-        group_offsets[0] = 0;
-        for (int s = 0; s < n_local; ++s) {
-            run += size_s[s];
-            group_offsets[s + 1] = run;
+    if (wave == 0) wave_offsets(size_s, n_local, group_offsets, lane);
+    if (send_counts && tid < G) send_counts[tid] = send_s[tid];
+
+    // Per-slot exclusive scan of the block counts [nblk][n_local], a tile of
+    // whole block rows at a time: coalesced loads into LDS, one wave per slot
+    // (each lane a run of rows), coalesced stores.
+    if (n_local <= 0 || nblk <= 0) return;
+    const int64_t rows_per = SCAN_TILE / n_local;
+    for (int64_t r0 = 0; r0 < nblk; r0 += rows_per) {
+        const int rows = (int)(nblk - r0 < rows_per ? nblk - r0 : rows_per);
+        const int n = rows * n_local;
+        int32_t* g = blk_counts + r0 * n_local;
+        int32_t v[SCAN_TILE / SCAN_THREADS];
+#pragma unroll
+        for (int u = 0; u < SCAN_TILE / SCAN_THREADS; ++u) {
+            const int i = u * SCAN_THREADS + tid;
+            v[u] = g[i < n ? i : 0];
         }
-    }
-    // per-slot exclusive scan of block counts, one wave per slot at a time
-    const int wave = tid >> 6, lane = tid & 63;
-    for (int s = wave; s < n_local; s += 4) {
-        int32_t running = 0;
-        for (int64_t c0 = 0; c0 < nblk; c0 += 64) {
-            const int64_t b = c0 + lane;
-            const int32_t v = b < nblk ? blk_counts[b * n_local + s] : 0;
-            int32_t incl = v;
+#pragma unroll
+        for (int u = 0; u < SCAN_TILE / SCAN_THREADS; ++u) tile[u * SCAN_THREADS + tid] = v[u];
+        __syncthreads();
+        const int per = (rows + 63) / 64;
+        for (int s = wave; s < n_local; s += SCAN_WAVES) {
+            const int b0 = lane * per;
+            int32_t sum = 0;
+            for (int i = 0; i < per; ++i)
+                if (b0 + i < rows) sum += tile[(b0 + i) * n_local + s];
+            int32_t incl = sum;
 #pragma unroll
             for (int o = 1; o < 64; o <<= 1) {
                 const int32_t u = __shfl_up(incl, o, 64);
                 if (lane >= o) incl += u;
             }
-            if (b < nblk) blk_counts[b * n_local + s] = running + incl - v;
-            running += __shfl(incl, 63, 64);
+            int32_t run = carry_s[s] + incl - sum;
+            for (int i = 0; i < per; ++i) {
+                if (b0 + i < rows) {
+                    int32_t* p = &tile[(b0 + i) * n_local + s];
+                    const int32_t c = *p;
+                    *p = run;
+                    run += c;
+                }
+            }
+            const int32_t total = __shfl(incl, 63, 64);
+            if (lane == 0) carry_s[s] += total;
         }
+        __syncthreads();
+        for (int i = tid; i < n; i += SCAN_THREADS) g[i] = tile[i];
+        __syncthreads();
     }
 }
 
@@ -125,26 +207,41 @@ __global__ __launch_bounds__(PERM_TOKENS) void perm_scatter_kernel(
     int32_t* __restrict__ token_row) {
     __shared__ unsigned long long bits[MOE_MAX_GROUPS];
     __shared__ int16_t slot_lds[MOE_MAX_E];
+    __shared__ int32_t base_s[MOE_MAX_GROUPS], lo_s[MOE_MAX_GROUPS], off_s[MOE_MAX_GROUPS + 1];
     const int lane = threadIdx.x;
-    for (int e = lane; e < E; e += PERM_TOKENS) slot_lds[e] = tab.slot_of[e];
     const int64_t blk = blockIdx.x;
     const int64_t t = blk * PERM_TOKENS + lane;
-    build_bits(idx, T, k, E, slot_lds, n_local, bits, lane, t);
+    int ev[MOE_MAX_K];
+    float gv[MOE_MAX_K];
+    if (t < T) {
+        load_ids(idx, t, k, ev);
+        load_gates(gate, t, k, gv);
+    }
+    for (int e = lane; e < E; e += PERM_TOKENS) slot_lds[e] = tab.slot_of[e];
+    for (int s = lane; s < n_local; s += PERM_TOKENS) {
+        bits[s] = 0ull;
+        base_s[s] = blk_base[blk * n_local + s];
+        lo_s[s] = lo_in[s];
+    }
+    for (int s = lane; s <= n_local; s += PERM_TOKENS) off_s[s] = group_offsets[s];
+    __syncthreads();
+    set_bits(ev, t < T, k, E, slot_lds, bits, lane);
+    __syncthreads();
     if (t >= T) return;
     const unsigned long long lower = (1ull << lane) - 1ull;
-    for (int r = 0; r < k; ++r) {
-        const int e = idx[t * k + r];
+#pragma unroll
+    for (int r = 0; r < MOE_MAX_K; ++r) {
+        if (r >= k) break;
+        const int e = ev[r];
         int32_t p = -1;
         const int s = (unsigned)e < (unsigned)E ? (int)slot_lds[e] : -1;
         if (s >= 0) {
-            const int32_t rank = blk_base[blk * n_local + s] + __popcll(bits[s] & lower);
-            const int32_t lo = lo_in[s];
-            const int32_t off = group_offsets[s];
-            const int32_t size = group_offsets[s + 1] - off;
-            if (rank >= lo && rank < lo + size) {
-                p = off + (rank - lo);
+            const int32_t rank = base_s[s] + __popcll(bits[s] & lower);
+            const int32_t lo = lo_s[s];
+            if (rank >= lo && rank < lo + (off_s[s + 1] - off_s[s])) {
+                p = off_s[s] + (rank - lo);
                 row_token[p] = (int32_t)t;
-                row_gate[p] = gate[t * k + r];
+                row_gate[p] = gv[r];
             }
         }
         token_row[t * k + r] = p;
@@ -166,24 +263,30 @@ __global__ __launch_bounds__(SMALL_T) void perm_small_kernel(
     __shared__ unsigned long long bits[SMALL_BLK][MOE_MAX_GROUPS];
     __shared__ int32_t base[SMALL_BLK][MOE_MAX_GROUPS];
     __shared__ int16_t slot_lds[MOE_MAX_E];
+    __shared__ uint64_t hosts_s[MOE_MAX_E];
+    __shared__ int32_t cnt_s[MOE_MAX_E], send_s[MOE_MAX_G];
     __shared__ int32_t lo_s[MOE_MAX_GROUPS], size_s[MOE_MAX_GROUPS], off_s[MOE_MAX_GROUPS + 1];
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int nblk = (int)ceil_div(T, PERM_TOKENS);
-    for (int e = tid; e < E; e += SMALL_T) slot_lds[e] = st.slot_of[e];
+    const int64_t t = (int64_t)wave * PERM_TOKENS + lane;
+    int ev[MOE_MAX_K];
+    float gv[MOE_MAX_K];
+    if (t < T) {
+        load_ids(idx, t, k, ev);
+        load_gates(gate, t, k, gv);
+    }
+    for (int e = tid; e < E; e += SMALL_T) {
+        slot_lds[e] = st.slot_of[e];
+        cnt_s[e] = counts[e];
+        hosts_s[e] = ht.hosts[e];
+    }
+    if (tid < MOE_MAX_G) send_s[tid] = 0;
     for (int i = tid; i < SMALL_BLK * MOE_MAX_GROUPS; i += SMALL_T)
         bits[i / MOE_MAX_GROUPS][i % MOE_MAX_GROUPS] = 0ull;
     __syncthreads();
-    const int64_t t = (int64_t)wave * PERM_TOKENS + lane;
-    if (t < T) {
-        for (int r = 0; r < k; ++r) {
-            const int e = idx[t * k + r];
-            if ((unsigned)e >= (unsigned)E) continue;
-            const int sl = slot_lds[e];
-            if (sl >= 0) atomicOr(&bits[wave][sl], 1ull << lane);
-        }
-    }
+    set_bits(ev, t < T, k, E, slot_lds, bits[wave], lane);
+    if (send_counts) add_send_counts(cnt_s, hosts_s, E, tid, SMALL_T, send_s);
     __syncthreads();
-    const uint64_t below = dev == 0 ? 0ull : (~0ull >> (64 - dev));
     if (tid < n_local) {
         int32_t run = 0;
         for (int b = 0; b < nblk; ++b) {
@@ -191,43 +294,24 @@ __global__ __launch_bounds__(SMALL_T) void perm_small_kernel(
             run += __popcll(bits[b][tid]);
         }
         const int e = ht.expert_of_slot[tid];
-        const int64_t c = counts[e];
-        const uint64_t h = ht.hosts[e];
+        const uint64_t h = hosts_s[e];
         const int n = __popcll(h);
-        const int q = __popcll(h & below);
-        const int64_t lo = (int64_t)q * c / n;
+        const int q = dev == 0 ? 0 : __popcll(h & (~0ull >> (64 - dev)));
+        const int64_t lo = replica_lo(q, cnt_s[e], n);
         lo_s[tid] = (int32_t)lo;
-        size_s[tid] = (int32_t)((int64_t)(q + 1) * c / n - lo);
+        size_s[tid] = (int32_t)(replica_lo(q + 1, cnt_s[e], n) - lo);
     }
-    if (send_counts && tid >= SMALL_T - 64 && tid - (SMALL_T - 64) < G) {
-        const int j = tid - (SMALL_T - 64);
-        const uint64_t below_j = j == 0 ? 0ull : (~0ull >> (64 - j));
-        int64_t sum = 0;
-        for (int e = 0; e < E; ++e) {
-            const uint64_t h = ht.hosts[e];
-            if (!((h >> j) & 1ull)) continue;
-            const int64_t c = counts[e];
-            const int n = __popcll(h);
-            const int q = __popcll(h & below_j);
-            sum += (int64_t)(q + 1) * c / n - (int64_t)q * c / n;
-        }
-        send_counts[j] = (int32_t)sum;
-    }
+    if (send_counts && tid < G) send_counts[tid] = send_s[tid];
     __syncthreads();
-    if (tid == 0) {
-        int32_t run = 0;
-        off_s[0] = 0;
-        for (int sl = 0; sl < n_local; ++sl) {
-            run += size_s[sl];
-            off_s[sl + 1] = run;
-        }
-    }
+    if (wave == 0) wave_offsets(size_s, n_local, off_s, lane);
     __syncthreads();
     for (int sl = tid; sl <= n_local; sl += SMALL_T) group_offsets[sl] = off_s[sl];
     if (t >= T) return;
     const unsigned long long lower = (1ull << lane) - 1ull;
-    for (int r = 0; r < k; ++r) {
-        const int e = idx[t * k + r];
+#pragma unroll
+    for (int r = 0; r < MOE_MAX_K; ++r) {
+        if (r >= k) break;
+        const int e = ev[r];
         int32_t p = -1;
         const int sl = (unsigned)e < (unsigned)E ? (int)slot_lds[e] : -1;
         if (sl >= 0) {
@@ -236,7 +320,7 @@ __global__ __launch_bounds__(SMALL_T) void perm_small_kernel(
             if (rank >= lo && rank < lo + size_s[sl]) {
                 p = off_s[sl] + (rank - lo);
                 row_token[p] = (int32_t)t;
-                row_gate[p] = gate[t * k + r];
+                row_gate[p] = gv[r];
             }
         }
         token_row[t * k + r] = p;
@@ -290,7 +374,7 @@ int launch_permute(const void* x, int dtype, const int32_t* idx, const float* ga
         if (n_local > 0)
             hipLaunchKernelGGL(perm_count_kernel, dim3((unsigned)nblk), dim3(PERM_TOKENS), 0, s,
                                idx, T, k, E, st, n_local, blk);
-        hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(256), 0, s, counts, ht, E, n_local, G,
+        hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(SCAN_THREADS), 0, s, counts, ht, E, n_local, G,
                            dev, n_local > 0 ? nblk : (int64_t)0, blk, group_offsets, lo_ws,
                            send_counts);
         hipLaunchKernelGGL(perm_scatter_kernel, dim3((unsigned)nblk), dim3(PERM_TOKENS), 0, s,

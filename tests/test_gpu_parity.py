@@ -200,6 +200,38 @@ def test_every_token_to_one_expert_and_a_gpu_with_no_rows():
             np.testing.assert_array_equal(go, pm["group_offsets"])
 
 
+@pytest.mark.parametrize("dev", [0, 2])
+@pytest.mark.parametrize("T", [9000, 700])
+def test_128_local_experts_with_replicas_on_three_gpus(T, dev):
+    """128 local slots on each of three GPUs, half of each GPU's experts replicated on
+    another: at T = 9000 the per-slot block scan holds 141 x 128 counts (two LDS tiles),
+    at T = 700 the one-workgroup path runs.  Routing outputs bit-exact vs the oracle."""
+    E, G = 256, 3
+    cfg = synth.custom_config(d=64, E=E, k=8, f=64, G=G)
+    pl = np.zeros((E, G), np.uint8)
+    pl[0:128, 0] = 1
+    pl[64:192, 1] = 1
+    pl[192:256, 2] = 1
+    pl[0:64, 2] = 1
+    inp, share = _share(cfg, T, placement=pl, dev=dev)
+    assert share.n_local == 128
+    rng = np.random.default_rng(T + dev)
+    L = (rng.standard_normal((T, E)) + np.linspace(2.0, 0.0, E)[None, :]).astype(np.float32)
+    share.run(logits_in=torch.from_numpy(L).cuda())
+    torch.cuda.synchronize()
+    idx, gate = oracle.topk(L, cfg.k, renorm=True)
+    np.testing.assert_array_equal(share.topk_idx.cpu().numpy(), idx)
+    pm = oracle.permute(np32(inp.X), idx, gate, E, pl, dev)
+    N = pm["rows"]
+    got = {k: v.cpu().numpy() for k, v in share.perm.items() if v is not None and k != "x_perm"}
+    np.testing.assert_array_equal(got["group_offsets"], pm["group_offsets"])
+    np.testing.assert_array_equal(got["row_token"][:N], pm["row_token"])
+    np.testing.assert_array_equal(got["token_row"], pm["token_row"])
+    np.testing.assert_array_equal(got["send_counts"], pm["send_counts"])
+    close(got["row_gate"][:N], pm["row_gate"], GATE_TOL, "row_gate")
+    np.testing.assert_array_equal(np32(share.perm["x_perm"][:N]), pm["x_perm"])
+
+
 def test_gpu_hosting_no_expert_returns_shared_output_only():
     cfg = synth.custom_config(d=128, E=4, k=2, f=64, shared_f=(128,), G=2)
     pl = np.zeros((4, 2), np.uint8)
