@@ -116,6 +116,23 @@ __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, int vof
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
+// s_tstart[g] = tiles of the groups before g, for g = 0..n_groups (a group of
+// more than small_rows rows has ceil(rows / BM) * n_tiles tiles, others none);
+// run by one whole wave.
+__device__ __forceinline__ void tile_starts(const int* s_off, int n_groups, int small_rows,
+                                            int n_tiles, int* s_tstart, int lane) {
+    int carry = 0;
+    for (int g0 = 0; g0 < n_groups; g0 += 64) {
+        const int g = g0 + lane;
+        const int rows = g < n_groups ? s_off[g + 1] - s_off[g] : 0;
+        const int v = rows > small_rows ? (int)ceil_div(rows, BM) * n_tiles : 0;
+        const int incl = wave_incl_scan(v, lane);
+        if (g < n_groups) s_tstart[g + 1] = carry + incl;
+        carry += __shfl(incl, 63, 64);
+    }
+    if (lane == 0) s_tstart[0] = 0;
+}
+
 // Persistent grouped NT GEMM.  Per tile: operands stream through per-tile
 // buffer descriptors (rows past the group's end fall outside the descriptor and
 // read as zero), are staged through registers into a double-buffered LDS
@@ -138,15 +155,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 
     for (int s = tid; s <= n_groups; s += GEMM_THREADS) s_off[s] = args.offsets[s];
     __syncthreads();
-    if (tid == 0) {
-        int acc = 0;
-        s_tstart[0] = 0;
-        for (int s = 0; s < n_groups; ++s) {
-            const int rows = s_off[s + 1] - s_off[s];
-            acc += rows > args.small_rows ? (int)ceil_div(rows, BM) * args.n_tiles : 0;
-            s_tstart[s + 1] = acc;
-        }
-    }
+    if (wave == 0) tile_starts(s_off, n_groups, args.small_rows, args.n_tiles, s_tstart, lane);
     __syncthreads();
     const int KT = args.K / BK;
     const int K = args.K;
@@ -181,8 +190,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
         const int kt0 = (int)((int64_t)kchunk * KT / S);
         const int nsteps = (int)((int64_t)(kchunk + 1) * KT / S) - kt0;
         if (tid == 0) {
-            int s = 0;
-            while (s + 1 < n_groups && s_tstart[s + 1] <= L) ++s;
+            const int s = last_le(s_tstart, n_groups, L);
             const int rows = s_off[s + 1] - s_off[s];
             const int mt = (int)ceil_div(rows, BM);
             const int local = L - s_tstart[s];
@@ -386,39 +394,42 @@ struct StreamPlan {
 __device__ void make_stream_plan(const StreamArgs& a, StreamPlan& P, int nthreads) {
     for (int g = threadIdx.x; g <= a.n_groups; g += nthreads) P.off[g] = a.offsets[g];
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (threadIdx.x < 64) {                          // one wave: prefix sums over the groups
+        const int lane = threadIdx.x;
         const int nt = (int)ceil_div(a.N, ST_N);
         const int KT = a.K / 64;
         int rows_small = 0, base = 0;
-        for (int g = 0; g < a.n_groups; ++g) {
-            const int rows = P.off[g + 1] - P.off[g];
-            P.qbase[g] = rows_small;
-            if (rows > 0 && rows <= SMALL_ROWS) {
-                rows_small += rows;
-                base += (int)ceil_div(rows, ST_M) * nt;
+        for (int g0 = 0; g0 < a.n_groups; g0 += 64) {
+            const int g = g0 + lane;
+            const int rows = g < a.n_groups ? P.off[g + 1] - P.off[g] : 0;
+            const bool small = rows > 0 && rows <= SMALL_ROWS;
+            const int rs = small ? rows : 0;
+            const int items = small ? (int)ceil_div(rows, ST_M) * nt : 0;
+            const int irs = wave_incl_scan(rs, lane), iit = wave_incl_scan(items, lane);
+            if (g < a.n_groups) {
+                P.qbase[g] = rows_small + irs - rs;
+                P.istart[g] = base + iit - items;    // scaled by S below
             }
+            rows_small += __shfl(irs, 63, 64);
+            base += __shfl(iit, 63, 64);
         }
-        P.qbase[a.n_groups] = rows_small;
         // split factor: as many K chunks as fit the grid in one round (every
         // workgroup streams one item; a partly filled extra round would leave
-        // most of HBM idle); each workgroup computes this plan before its
-        // first load, so it is kept to a few integer operations
+        // most of HBM idle)
         int S = base > 0 ? a.grid / base : 1;
         S = min(S, SPLIT_MAX);
         S = min(S, KT);
         if (rows_small > 0) S = min(S, a.part_rows / rows_small);
         S = max(S, 1);
-        int acc = 0;
-        for (int g = 0; g < a.n_groups; ++g) {
-            P.istart[g] = acc;
-            const int rows = P.off[g + 1] - P.off[g];
-            if (rows > 0 && rows <= SMALL_ROWS) acc += (int)ceil_div(rows, ST_M) * nt * S;
+        for (int g = lane; g < a.n_groups; g += 64) P.istart[g] *= S;
+        if (lane == 0) {
+            P.qbase[a.n_groups] = rows_small;
+            P.istart[a.n_groups] = base * S;
+            P.n_small = rows_small;
+            P.S = S;
+            P.total = base * S;
+            P.n_tiles = nt;
         }
-        P.istart[a.n_groups] = acc;
-        P.n_small = rows_small;
-        P.S = S;
-        P.total = acc;
-        P.n_tiles = nt;
     }
     __syncthreads();
 }
@@ -449,11 +460,7 @@ __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(S
 
     for (int it = i_begin + widx; it < i_end; it += wg_per_xcd) {
         if (tid == 0) {
-            int lo = 0, hi = args.n_groups - 1;      // group: last g with istart[g] <= it
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (P.istart[mid] <= it) lo = mid; else hi = mid - 1;
-            }
+            const int lo = last_le(P.istart, args.n_groups, it);   // the item's group
             s_item[0] = lo;
             s_item[1] = it - P.istart[lo];
         }
@@ -538,15 +545,7 @@ __device__ void tile_split_reduce(const GemmArgs& t, int* s_off, int* s_tstart) 
     const int n_groups = t.n_groups;
     for (int g = threadIdx.x; g <= n_groups; g += ST_THREADS) s_off[g] = t.offsets[g];
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int acc = 0;
-        s_tstart[0] = 0;
-        for (int g = 0; g < n_groups; ++g) {
-            const int rows = s_off[g + 1] - s_off[g];
-            acc += rows > t.small_rows ? (int)ceil_div(rows, BM) * t.n_tiles : 0;
-            s_tstart[g + 1] = acc;
-        }
-    }
+    if (threadIdx.x < 64) tile_starts(s_off, n_groups, t.small_rows, t.n_tiles, s_tstart, threadIdx.x);
     __syncthreads();
     const SplitPlan plan = split_plan(s_tstart[n_groups], t.K / BK, t.split_units);
     const int S = plan.S;
@@ -560,8 +559,7 @@ __device__ void tile_split_reduce(const GemmArgs& t, int* s_off, int* s_tstart) 
         const int L = plan.head + q;
         const int rem = (int)(i - (int64_t)q * BM * C4);
         const int row = rem / C4, j = (rem - row * C4) * 4;
-        int g = 0;
-        while (g + 1 < n_groups && s_tstart[g + 1] <= L) ++g;
+        const int g = last_le(s_tstart, n_groups, L);
         const int rows = s_off[g + 1] - s_off[g];
         const int mt = (int)ceil_div(rows, BM);
         const int local = L - s_tstart[g];
@@ -612,43 +610,49 @@ __device__ __forceinline__ void stream_reduce(const StreamArgs& args, const Stre
     if (n_small == 0) return;
     const int S = P.S;
     const int cols = SWIGLU ? args.N / 2 : args.N;
-    const int chunks = cols / 8;
+    const int chunks = cols / 4;                     // 4 output columns per item
     const int64_t total = (int64_t)n_small * chunks;
+    const int64_t cstride = (int64_t)n_small * args.N;
     for (int64_t i = (int64_t)blockIdx.x * ST_THREADS + threadIdx.x; i < total;
          i += (int64_t)gridDim.x * ST_THREADS) {
         const int q = (int)(i / chunks);
-        const int c8 = (int)(i - (int64_t)q * chunks) * 8;
-        int lo = 0, hi = args.n_groups - 1;          // group: last g with qbase[g] <= q
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (P.qbase[mid] <= q) lo = mid; else hi = mid - 1;
-        }
-        // skip forward over groups that hold no small rows (qbase does not advance there)
-        const int g = lo;                            // groups without small rows share qbase
+        const int c4 = (int)(i - (int64_t)q * chunks) * 4;
+        // the row's group: groups without small rows share qbase with the next one
+        const int g = last_le(P.qbase, args.n_groups, q);
         const int p = P.off[g] + (q - P.qbase[g]);
-        float x[8], y[8];
+        const float* pr = args.part + (int64_t)q * args.N + c4;
+        float4 x = make_float4(0.f, 0.f, 0.f, 0.f), y = x;
+        // chunks are added one after another in chunk order; the loads of up to
+        // RU chunks are issued together ahead of their adds
+        constexpr int RU = 8;
+        int c = 0;
+        for (; c + RU <= S; c += RU) {
+            float4 v[RU], u[RU];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) { x[e] = 0.f; y[e] = 0.f; }
-        for (int c = 0; c < S; ++c) {
-            const float* pr = args.part + ((int64_t)c * n_small + q) * args.N + c8;
-            const float4 v0 = *(const float4*)pr, v1 = *(const float4*)(pr + 4);
-            x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
-            x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
-            if (SWIGLU) {
-                const float4 u0 = *(const float4*)(pr + cols), u1 = *(const float4*)(pr + cols + 4);
-                y[0] += u0.x; y[1] += u0.y; y[2] += u0.z; y[3] += u0.w;
-                y[4] += u1.x; y[5] += u1.y; y[6] += u1.z; y[7] += u1.w;
+            for (int j = 0; j < RU; ++j) {
+                v[j] = *(const float4*)(pr + (c + j) * cstride);
+                if (SWIGLU) u[j] = *(const float4*)(pr + (c + j) * cstride + cols);
+            }
+#pragma unroll
+            for (int j = 0; j < RU; ++j) {
+                x.x += v[j].x; x.y += v[j].y; x.z += v[j].z; x.w += v[j].w;
+                if (SWIGLU) { y.x += u[j].x; y.y += u[j].y; y.z += u[j].z; y.w += u[j].w; }
             }
         }
-        float o[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = SWIGLU ? silu(x[e]) * y[e] : x[e];
-        uint4 pk;
-        pk.x = pack_bf16x2(o[0], o[1]);
-        pk.y = pack_bf16x2(o[2], o[3]);
-        pk.z = pack_bf16x2(o[4], o[5]);
-        pk.w = pack_bf16x2(o[6], o[7]);
-        *(uint4*)(args.out + (int64_t)p * args.ldo + c8) = pk;
+        for (; c < S; ++c) {
+            const float4 v = *(const float4*)(pr + c * cstride);
+            x.x += v.x; x.y += v.y; x.z += v.z; x.w += v.w;
+            if (SWIGLU) {
+                const float4 u = *(const float4*)(pr + c * cstride + cols);
+                y.x += u.x; y.y += u.y; y.z += u.z; y.w += u.w;
+            }
+        }
+        const float o0 = SWIGLU ? silu(x.x) * y.x : x.x, o1 = SWIGLU ? silu(x.y) * y.y : x.y;
+        const float o2 = SWIGLU ? silu(x.z) * y.z : x.z, o3 = SWIGLU ? silu(x.w) * y.w : x.w;
+        uint2 pk;
+        pk.x = pack_bf16x2(o0, o1);
+        pk.y = pack_bf16x2(o2, o3);
+        *(uint2*)(args.out + (int64_t)p * args.ldo + c4) = pk;
     }
 }
 
@@ -780,7 +784,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     float* tpart = tbase ? (float*)(tbase + 256) : nullptr;
     int* tinfo = tbase ? (int*)tbase : nullptr;
     const int sgrid = ((cus * ST_WG_PER_CU) / NUM_XCD) * NUM_XCD;
-    const int64_t red_items = rmax * ((f > d ? f : d) / 8);
+    const int64_t red_items = rmax * ((f > d ? f : d) / 4);
     int rgrid = (int)ceil_div(red_items, ST_THREADS);
     if (tpart != nullptr && rgrid < 2 * cus) rgrid = 2 * cus;   // room for split tiles
     if (rgrid > 4096) rgrid = 4096;
