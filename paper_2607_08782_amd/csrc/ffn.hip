@@ -276,7 +276,10 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
         gload(kt0 + (nsteps > 1 ? 1 : 0));
         __syncthreads();
         read(0, 0, fa0, fb0);
-        for (int t = 0; t < nsteps; ++t) {
+        // Every step but the last runs one straight path, so the MFMAs after the
+        // barrier (on fragments read before it) issue without waiting for the
+        // next stage's reads; the last step is peeled off below.
+        for (int t = 0; t + 1 < nsteps; ++t) {
             const int buf = t & 1;
             __builtin_amdgcn_iglp_opt(1);
             read(buf, 1, fa1, fb1);
@@ -285,12 +288,20 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
             mfma(fa1, fb1);
             read(buf, 3, fa1, fb1);
             mfma(fa0, fb0);
-            if (t + 1 < nsteps) {
-                sstore(buf ^ 1);
-                __syncthreads();
-                gload(kt0 + (t + 2 < nsteps ? t + 2 : nsteps - 1));
-                read(buf ^ 1, 0, fa0, fb0);
-            }
+            sstore(buf ^ 1);
+            __syncthreads();
+            gload(kt0 + (t + 2 < nsteps ? t + 2 : nsteps - 1));
+            read(buf ^ 1, 0, fa0, fb0);
+            mfma(fa1, fb1);
+        }
+        {
+            const int buf = (nsteps - 1) & 1;
+            read(buf, 1, fa1, fb1);
+            mfma(fa0, fb0);
+            read(buf, 2, fa0, fb0);
+            mfma(fa1, fb1);
+            read(buf, 3, fa1, fb1);
+            mfma(fa0, fb0);
             mfma(fa1, fb1);
         }
         __syncthreads();
