@@ -3,8 +3,9 @@
 // Sec. II-B), plus always-on shared experts with weight 1.
 //
 // Bandwidth-bound gather: each thread owns one 16-byte chunk of one token's
-// output row, reads the k expert rows it needs (skipping assignments placed
-// on other GPUs), accumulates in fp32 in ascending r, and stores once.
+// output row, reads the k expert rows it needs (all loads issued together;
+// assignments placed on other GPUs are skipped), accumulates in fp32 in
+// ascending r, and stores once.
 #include "common.h"
 
 namespace moe {
@@ -60,7 +61,8 @@ struct Vec<float, 1> {
     static __device__ __forceinline__ void store(float* p, const float* v) { *p = v[0]; }
 };
 
-template <typename Elem, int V>
+// KM: k rounded up to a power of two (compile-time trip counts, no spills)
+template <typename Elem, int V, int KM>
 __global__ __launch_bounds__(COMBINE_THREADS) void combine_kernel(
     const Elem* __restrict__ y_perm, const int32_t* __restrict__ token_row,
     const float* __restrict__ gate, const Elem* __restrict__ y_shared, int64_t T, int d, int k,
@@ -70,36 +72,57 @@ __global__ __launch_bounds__(COMBINE_THREADS) void combine_kernel(
     const int c = (int)(gid - t * chunks_per_row);
     if (t >= T) return;
     const int col = c * V;
+    // The k row indices and gates first, then every row load at once: an
+    // assignment with no row here (or a slot past k) reads this thread's own
+    // output chunk (always valid memory) and is dropped by the select, so no
+    // load sits behind a branch.
+    int32_t p[KM];
+    float g[KM];
+#pragma unroll
+    for (int r = 0; r < KM; ++r) {
+        const int rr = r < k ? r : k - 1;
+        p[r] = r < k ? token_row[t * k + rr] : -1;
+        g[r] = gate[t * k + rr];
+    }
+    const Elem* self = y + t * d + col;
+    float v[KM][V];
+#pragma unroll
+    for (int r = 0; r < KM; ++r)
+        Vec<Elem, V>::load(p[r] >= 0 ? y_perm + (int64_t)p[r] * d + col : self, v[r]);
     float acc[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) acc[i] = 0.f;
-    for (int r = 0; r < k; ++r) {
-        const int32_t p = token_row[t * k + r];
-        if (p < 0) continue;
-        const float g = gate[t * k + r];
-        float v[V];
-        Vec<Elem, V>::load(y_perm + (int64_t)p * d + col, v);
 #pragma unroll
-        for (int i = 0; i < V; ++i) acc[i] = fmaf(g, v[i], acc[i]);
-    }
+    for (int r = 0; r < KM; ++r)
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] = p[r] >= 0 ? fmaf(g[r], v[r][i], acc[i]) : acc[i];
     if (y_shared) {
-        float v[V];
-        Vec<Elem, V>::load(y_shared + t * d + col, v);
+        float w[V];
+        Vec<Elem, V>::load(y_shared + t * d + col, w);
 #pragma unroll
-        for (int i = 0; i < V; ++i) acc[i] += v[i];
+        for (int i = 0; i < V; ++i) acc[i] += w[i];
     }
     Vec<Elem, V>::store(y + t * d + col, acc);
+}
+
+template <typename Elem, int V, int KM>
+int launch_k(const void* y_perm, const int32_t* token_row, const float* gate, const void* y_shared,
+             int64_t T, int d, int k, void* y, hipStream_t s) {
+    const int chunks = d / V;
+    const int64_t blocks = ceil_div(T * chunks, COMBINE_THREADS);
+    hipLaunchKernelGGL((combine_kernel<Elem, V, KM>), dim3((unsigned)blocks), dim3(COMBINE_THREADS),
+                       0, s, (const Elem*)y_perm, token_row, gate, (const Elem*)y_shared, T, d, k,
+                       chunks, (Elem*)y);
+    return launch_status();
 }
 
 template <typename Elem, int V>
 int launch_v(const void* y_perm, const int32_t* token_row, const float* gate, const void* y_shared,
              int64_t T, int d, int k, void* y, hipStream_t s) {
-    const int chunks = d / V;
-    const int64_t blocks = ceil_div(T * chunks, COMBINE_THREADS);
-    hipLaunchKernelGGL((combine_kernel<Elem, V>), dim3((unsigned)blocks), dim3(COMBINE_THREADS), 0,
-                       s, (const Elem*)y_perm, token_row, gate, (const Elem*)y_shared, T, d, k,
-                       chunks, (Elem*)y);
-    return launch_status();
+    if (k <= 2) return launch_k<Elem, V, 2>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
+    if (k <= 4) return launch_k<Elem, V, 4>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
+    if (k <= 8) return launch_k<Elem, V, 8>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
+    return launch_k<Elem, V, MOE_MAX_K>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
 }
 
 }  // namespace
