@@ -150,7 +150,10 @@ __global__ __launch_bounds__(SC_THREADS) void score_tiles_kernel(
             wait_vm<(R - 2) * P>();       // stage t landed; the R - 2 after it may still fly
         else
             wait_vm<0>();
-        __syncthreads();                  // every wave's share of stage t is in; stage t-1 is free
+        // every wave's share of stage t is in; stage t-1 is free (its reads fed
+        // MFMAs already).  A bare barrier: the fence of __syncthreads would wait
+        // for all R - 1 stages in flight, draining the ring every step.
+        asm volatile("s_barrier" ::: "memory");
         if (t + R - 1 < nst) dma(t + R - 1);
         compute(t % R);
     }
