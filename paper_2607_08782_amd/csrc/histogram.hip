@@ -14,10 +14,14 @@ constexpr int HIST_THREADS = 256;
 constexpr int LDS_COACT_MAX_E = 128;     // E*E int32 bins fit in 64 KiB of LDS
 constexpr int DIRECT_MAX_TOKENS = 512;   // up to this many tokens one workgroup does it all
 
-__global__ void zero_i32_kernel(int32_t* __restrict__ p, int64_t n) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x)
-        p[i] = 0;
+// Clears a[0..na) and b[0..nb) in one launch (b may be null).
+__global__ void zero_i32_kernel(int32_t* __restrict__ a, int64_t na, int32_t* __restrict__ b,
+                                int64_t nb) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < na + nb;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        if (i < na) a[i] = 0;
+        else b[i - na] = 0;
+    }
 }
 
 // DIRECT: a single workgroup covers all tokens and stores its bins (zeros
@@ -109,6 +113,51 @@ __global__ __launch_bounds__(HF_THREADS) void histogram_flat_kernel(const int32_
     }
 }
 
+// Short batches with co-activation (T <= DIRECT_MAX_TOKENS, E <= LDS_COACT_MAX_E):
+// one 1024-thread workgroup, E*E bins in LDS cleared and stored 16 bytes at a
+// time; thread i takes assignment (t, r) = (i / k, i % k), loads the token's k
+// ids together (KM = k rounded up to a power of two, compile-time) and adds row
+// r of the token's k x k co-activation block.
+constexpr int HD_THREADS = 1024;
+
+template <int KM>
+__global__ __launch_bounds__(HD_THREADS) void histogram_coact_direct_kernel(
+    const int32_t* __restrict__ idx, int T, int k, int E, int32_t* __restrict__ counts,
+    int32_t* __restrict__ coact) {
+    extern __shared__ __attribute__((aligned(16))) int32_t co_lds[];   // [E][E]
+    __shared__ int32_t c_lds[MOE_MAX_E];
+    const int tid = threadIdx.x;
+    const int nb = E * E;
+    const int n4 = nb >> 2;
+    for (int i = tid; i < n4; i += HD_THREADS) ((int4*)co_lds)[i] = make_int4(0, 0, 0, 0);
+    for (int i = (n4 << 2) + tid; i < nb; i += HD_THREADS) co_lds[i] = 0;
+    for (int i = tid; i < E; i += HD_THREADS) c_lds[i] = 0;
+    __syncthreads();
+    for (int a = tid; a < T * k; a += HD_THREADS) {
+        const int t = a / k, r = a - t * k;
+        int sel[KM];
+#pragma unroll
+        for (int q = 0; q < KM; ++q) sel[q] = idx[(int64_t)t * k + (q < k ? q : k - 1)];
+        int e = sel[0];
+#pragma unroll
+        for (int q = 1; q < KM; ++q) e = q == r ? sel[q] : e;
+        // out-of-range expert ids are ignored rather than counted out of bounds
+        if ((unsigned)e >= (unsigned)E) continue;
+        atomicAdd(&c_lds[e], 1);
+#pragma unroll
+        for (int q = 0; q < KM; ++q)
+            if (q < k && (unsigned)sel[q] < (unsigned)E) atomicAdd(&co_lds[e * E + sel[q]], 1);
+    }
+    __syncthreads();
+    if (((uintptr_t)coact & 15) == 0) {
+        for (int i = tid; i < n4; i += HD_THREADS) ((int4*)coact)[i] = ((const int4*)co_lds)[i];
+        for (int i = (n4 << 2) + tid; i < nb; i += HD_THREADS) coact[i] = co_lds[i];
+    } else {
+        for (int i = tid; i < nb; i += HD_THREADS) coact[i] = co_lds[i];
+    }
+    for (int i = tid; i < E; i += HD_THREADS) counts[i] = c_lds[i];
+}
+
 }  // namespace
 
 int launch_histogram(const int32_t* idx, int64_t T, int k, int E, int32_t* counts, int32_t* coact,
@@ -121,21 +170,30 @@ int launch_histogram(const int32_t* idx, int64_t T, int k, int E, int32_t* count
     }
     // short batches (decode): one workgroup, bins stored directly, one launch
     if (T <= DIRECT_MAX_TOKENS && (!coact || E <= LDS_COACT_MAX_E)) {
-        if (coact)
-            hipLaunchKernelGGL((histogram_kernel<true, true, true>), dim3(1), dim3(HIST_THREADS),
-                               (size_t)E * E * sizeof(int32_t), s, idx, T, k, E, counts, coact);
-        else
+        if (coact) {
+            if (T == 0) {
+                hipLaunchKernelGGL(zero_i32_kernel, dim3((unsigned)ceil_div((int64_t)E * (E + 1), 256)),
+                                   dim3(256), 0, s, counts, (int64_t)E, coact, (int64_t)E * E);
+                return launch_status();
+            }
+            const size_t lds = (size_t)E * E * sizeof(int32_t);
+#define HD(KM) hipLaunchKernelGGL((histogram_coact_direct_kernel<KM>), dim3(1), dim3(HD_THREADS), \
+                                  lds, s, idx, (int)T, k, E, counts, coact)
+            if (k <= 2) HD(2);
+            else if (k <= 4) HD(4);
+            else if (k <= 8) HD(8);
+            else HD(MOE_MAX_K);
+#undef HD
+        } else
             hipLaunchKernelGGL((histogram_kernel<false, false, true>), dim3(1), dim3(HIST_THREADS),
                                0, s, idx, T, k, E, counts, coact);
         return launch_status();
     }
-    const int64_t nbins = (int64_t)E + (coact ? (int64_t)E * E : 0);
-    hipLaunchKernelGGL(zero_i32_kernel, dim3((unsigned)ceil_div(E, 256)), dim3(256), 0, s, counts,
-                       (int64_t)E);
-    if (coact)
-        hipLaunchKernelGGL(zero_i32_kernel, dim3((unsigned)ceil_div((int64_t)E * E, 256)),
-                           dim3(256), 0, s, coact, (int64_t)E * E);
-    (void)nbins;
+    const int64_t ncoact = coact ? (int64_t)E * E : 0;
+    int64_t zblocks = ceil_div((int64_t)E + ncoact, 256);
+    if (zblocks > 1024) zblocks = 1024;
+    hipLaunchKernelGGL(zero_i32_kernel, dim3((unsigned)zblocks), dim3(256), 0, s, counts,
+                       (int64_t)E, coact, ncoact);
     if (T == 0) return launch_status();
     int64_t blocks = ceil_div(T, HIST_THREADS);
     if (!coact) {

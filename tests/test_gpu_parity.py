@@ -232,6 +232,25 @@ def test_128_local_experts_with_replicas_on_three_gpus(T, dev):
     np.testing.assert_array_equal(np32(share.perm["x_perm"][:N]), pm["x_perm"])
 
 
+@pytest.mark.parametrize("T,k,E,offset", [(0, 4, 13, 0), (1, 3, 13, 1), (37, 5, 13, 0),
+                                            (64, 8, 128, 0), (512, 16, 128, 1), (513, 2, 7, 1),
+                                            (3000, 8, 128, 0)])
+def test_histogram_with_coactivation_every_bin(T, k, E, offset):
+    """Short batches take the one-workgroup co-activation kernel (odd E: E*E not a
+    multiple of 4; offset 1: an output not 16-byte aligned), longer ones the
+    multi-block path after one clearing launch.  Bit-exact vs the oracle."""
+    rng = np.random.default_rng(T * 31 + k + E)
+    idx = np.array([rng.permutation(E)[:k] for _ in range(T)], np.int32).reshape(T, k)
+    dev_idx = torch.from_numpy(idx).cuda()
+    coact = torch.full((E * E + offset,), -7, dtype=torch.int32, device="cuda")[offset:].view(E, E)
+    counts = torch.full((E,), -7, dtype=torch.int32, device="cuda")
+    moe.moe_expert_histogram(dev_idx, E, counts=counts, coact=coact)
+    torch.cuda.synchronize()
+    rc, rco = oracle.histogram(idx, E, True)
+    np.testing.assert_array_equal(counts.cpu().numpy(), rc)
+    np.testing.assert_array_equal(coact.cpu().numpy(), rco)
+
+
 def test_gpu_hosting_no_expert_returns_shared_output_only():
     cfg = synth.custom_config(d=128, E=4, k=2, f=64, shared_f=(128,), G=2)
     pl = np.zeros((4, 2), np.uint8)
