@@ -3,7 +3,10 @@
 A step is one pass of the whole share (gate scores + top-k, histograms,
 packaging, grouped SwiGLU FFN, weighted combine) over one batch of synthetic
 tokens already resident in HBM.  The headline is the prefill batch (T=4096);
-the decode batch (T=64) is reported beside it.  Prints ONE JSON line.
+the decode batch (T=64) is reported beside it.  `gather_in_ffn` reports the
+same step with the row copy x_perm elided (the expert FFN reads the token rows
+through the row map), and whether its output matches bit for bit; the
+headline keeps the packaged copy.  Prints ONE JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME:REGIME]
 """
@@ -38,6 +41,24 @@ def make_share(cfg, T, seed=0, weights=None):
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, w13, w2, shared=shared,
                        coact=cfg.coact)
     return inp, share, (w13, w2, shared)
+
+
+def gathered_variant(inp, share, weights, cfg, steps, warmup):
+    """The same share with the row copy x_perm elided (moe_permute writes the row maps
+    only, moe_grouped_ffn_rows reads the token rows through row_token): step time from
+    graph replays, and whether its output equals the packaged path's bit for bit."""
+    w13, w2, shared = weights
+    g = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, w13, w2, shared=shared,
+                   coact=cfg.coact, gather_in_ffn=True)
+    share.run()
+    g.run()
+    torch.cuda.synchronize()
+    equal = bool(torch.equal(share.y, g.y))
+    ms = time_replays(capture(g.run), steps, warmup)
+    return {"ms_per_step": ms, "tokens_per_s": share.T / (ms * 1e-3),
+            "bitwise_equal_output": equal,
+            "what": "row copy x_perm elided: moe_permute writes the row maps only and "
+                    "moe_grouped_ffn_rows reads the token rows through row_token"}
 
 
 def phase_calls(share):
@@ -237,6 +258,7 @@ def main():
             "algorithmic_flops_per_launch": flops, "avg_launch_us": t_ffn * 1e6,
         },
         "phases_us": {k: v * 1e3 for k, v in phases.items()},
+        "gather_in_ffn": gathered_variant(inp, share, weights, cfg, args.steps, args.warmup),
     }
     if args.decode and args.decode in dict(cfg.regimes) and args.decode != regime:
         Td = cfg.T(args.decode)
@@ -255,6 +277,8 @@ def main():
                          "traffic_unit": "bytes per launch",
                          "algorithmic_bytes_per_launch": dby, "avg_launch_us": dt * 1e6},
             "phases_us": {k: v * 1e3 for k, v in dph.items()},
+            "gather_in_ffn": gathered_variant(dinp, dshare, weights, cfg, max(args.steps * 5, 50),
+                                              args.warmup * 2),
         }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, inp, *weights, T)

@@ -186,6 +186,27 @@ int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets,
                     int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * moe_grouped_ffn_rows -- moe_grouped_ffn whose first product reads row p of
+ * its input straight from the token rows, x[row_token[p]], instead of from a
+ * packaged copy: the row map of the packaging step (Sec. II-B) is kept and the
+ * copy of the rows, x_perm, is never written or read.  This is the one-GPU
+ * part of fusing the dispatch gather into the expert GEMM; with moe_permute
+ * called with d = 0 (row maps only) the outputs are bitwise identical to
+ * moe_permute + moe_grouped_ffn.
+ *
+ * x          device [T][d] of `dtype`: the token rows
+ * row_token  device [cap_rows] int32 (moe_permute's row map): entries of rows
+ *            below group_offsets[n_groups] must lie in [0, T)
+ * other arguments, workspace (moe_grouped_ffn_ws_bytes) and outputs as for
+ * moe_grouped_ffn.  bf16 requires T * d * 2 < 2^31 (32-bit row offsets),
+ * else MOE_ERR_SHAPE, and 16-byte aligned x.
+ */
+int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int dtype,
+                         const int32_t* group_offsets, int n_groups, const void* const* w13,
+                         const void* const* w2, int d, int f, int64_t cap_rows, void* y_perm,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/*
  * moe_combine -- gate-weighted sum of the experts' outputs (Sec. II-A) back
  * in token order (the return trip of Sec. II-B), plus shared experts with
  * weight 1:

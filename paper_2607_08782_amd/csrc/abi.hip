@@ -139,6 +139,34 @@ int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets,
                               y_perm, ws, (hipStream_t)stream);
 }
 
+int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int dtype,
+                         const int32_t* group_offsets, int n_groups, const void* const* w13,
+                         const void* const* w2, int d, int f, int64_t cap_rows, void* y_perm,
+                         void* ws, size_t ws_bytes, void* stream) {
+    if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
+    if (T < 0 || n_groups < 1 || n_groups > MOE_MAX_GROUPS || d < 1 || f < 1 || cap_rows < 0)
+        return MOE_ERR_ARG;
+    if (cap_rows > 0x7fffffff) return MOE_ERR_ARG;
+    if (!group_offsets || !w13 || !w2) return MOE_ERR_ARG;
+    for (int s = 0; s < n_groups; ++s)
+        if (!w13[s] || !w2[s]) return MOE_ERR_ARG;
+    if (cap_rows > 0 && (!x || !row_token || !y_perm || T < 1)) return MOE_ERR_ARG;
+    if (dtype == MOE_BF16) {
+        if (d % 64 || f % 64) return MOE_ERR_SHAPE;
+        // token rows are addressed through 32-bit buffer offsets
+        if (T * (int64_t)d * 2 > 0x7fffffffLL) return MOE_ERR_SHAPE;
+        if (!aligned16(x) || !aligned16(y_perm)) return MOE_ERR_ARG;
+        for (int s = 0; s < n_groups; ++s)
+            if (!aligned16(w13[s]) || !aligned16(w2[s])) return MOE_ERR_ARG;
+    }
+    if (cap_rows > 0 &&
+        (!ws || ws_bytes < grouped_ffn_ws_bytes(dtype, cap_rows, d, f, n_groups) ||
+         ((uintptr_t)ws & 255u)))
+        return MOE_ERR_SHAPE;
+    return launch_grouped_ffn(x, dtype, group_offsets, n_groups, w13, w2, d, f, cap_rows, y_perm,
+                              ws, (hipStream_t)stream, row_token, T);
+}
+
 int moe_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* topk_gate,
                 const void* y_shared, int64_t T, int d, int k, void* y, void* stream) {
     if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;

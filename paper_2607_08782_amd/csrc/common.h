@@ -126,9 +126,12 @@ int launch_permute(const void* x, int dtype, const int32_t* idx, const float* ga
                    int32_t* send_counts, void* ws, hipStream_t s);
 size_t permute_ws_bytes(int64_t T, int k, int E);
 
+// a_rows (nullable): row p of the first product's input is row a_rows[p] of
+// x_perm, which then holds a_total rows (the token rows; no packaged copy).
 int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, int n_groups,
                        const void* const* w13, const void* const* w2, int d, int f,
-                       int64_t cap_rows, void* y_perm, void* ws, hipStream_t s);
+                       int64_t cap_rows, void* y_perm, void* ws, hipStream_t s,
+                       const int32_t* a_rows = nullptr, int64_t a_total = 0);
 size_t grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_groups);
 
 int launch_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* gate,

@@ -37,6 +37,7 @@ constexpr int A_PER = BM / ROWS_PER_PASS;          // 16-byte loads per thread p
 constexpr int B_PER = BNW / ROWS_PER_PASS;         // (B)
 constexpr int NUM_XCD = 8;
 constexpr uint32_t RSRC_WORD3 = 0x00020000;        // raw buffer: 32-bit data format
+constexpr int A_OOB = 0x7fffff00;                  // offset past any descriptor: reads zero
 
 struct GemmArgs {
     const bf16_t* w[MOE_MAX_GROUPS];   // per-group weight matrix, rows contiguous along K
@@ -54,6 +55,8 @@ struct GemmArgs {
     float* part;                       // fp32 partial tiles for split K (nullptr: never split)
     int* split_info;                   // the kernel records its split factor here for the reduce
     int split_units;                   // workgroups split K aims to occupy (<= TILE_SPLIT_UNITS)
+    const int32_t* a_rows;             // gather: row p of A is a[a_rows[p]] (a holds a_total rows)
+    int a_total;
 };
 
 // With fewer tiles than half the workgroups (mid-sized groups: a few 256-row
@@ -139,7 +142,9 @@ __device__ __forceinline__ void tile_starts(const int* s_off, int n_groups, int 
 // stage, and MFMA fragments are double-buffered per 16-wide K sub-step, so the
 // LDS reads of sub-step q+1 (including across the stage barrier) overlap the
 // MFMAs of sub-step q.
-template <bool SWIGLU>
+// GATHER: row p of A is row a_rows[p] of args.a (the token rows themselves, so
+// the packaged copy of them is never materialised).
+template <bool SWIGLU, bool GATHER = false>
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs args) {
     __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LDK];
     __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BNW * LDK];
@@ -209,8 +214,22 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
         const int rows_valid = __builtin_amdgcn_readfirstlane(min(BM, s_off[g + 1] - row0));
         const bf16_t* __restrict__ W = args.w[g];
 
-        const __amdgpu_buffer_rsrc_t arsrc = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)(args.a + (int64_t)row0 * K), (short)0, rows_valid * K * 2, RSRC_WORD3);
+        const __amdgpu_buffer_rsrc_t arsrc =
+            GATHER ? __builtin_amdgcn_make_buffer_rsrc((void*)args.a, (short)0, args.a_total * K * 2,
+                                                      RSRC_WORD3)
+                   : __builtin_amdgcn_make_buffer_rsrc((void*)(args.a + (int64_t)row0 * K), (short)0,
+                                                      rows_valid * K * 2, RSRC_WORD3);
+        // per-thread A row offsets; rows past the group fall outside the descriptor
+        int avoff[A_PER];
+#pragma unroll
+        for (int i = 0; i < A_PER; ++i) {
+            if constexpr (GATHER) {
+                const int rin = (tid >> 3) + ROWS_PER_PASS * i;
+                avoff[i] = rin < rows_valid ? (args.a_rows[row0 + rin] * K + kc) * 2 : A_OOB;
+            } else {
+                avoff[i] = voff + i * vstep;
+            }
+        }
         const int bvalid = min(BN_OUT, args.N - n0);
         const int bup = SWIGLU ? args.up_row + n0 : n0;
         const __amdgpu_buffer_rsrc_t brsrc_lo = __builtin_amdgcn_make_buffer_rsrc(
@@ -222,7 +241,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
         auto gload = [&](int kt) {
             const int so = kt * BK * 2;
 #pragma unroll
-            for (int i = 0; i < A_PER; ++i) ra[i] = buffer_load16(arsrc, voff + i * vstep, so);
+            for (int i = 0; i < A_PER; ++i) ra[i] = buffer_load16(arsrc, avoff[i], so);
 #pragma unroll
             for (int i = 0; i < B_PER; ++i) {
                 if (SWIGLU && i >= B_PER / 2)
@@ -393,6 +412,8 @@ struct StreamArgs {
     int ldo;
     int part_rows;                       // capacity of `part` in rows (S * n_small <= part_rows)
     int grid;                            // workgroups of the streaming launch
+    const int32_t* a_rows;               // gather: row p of A is a[a_rows[p]] (a holds a_total rows)
+    int a_total;
 };
 
 struct StreamPlan {
@@ -449,6 +470,7 @@ __device__ void make_stream_plan(const StreamArgs& a, StreamPlan& P, int nthread
 // takes 64 of the weight rows.  Loads are coalesced (8 lanes read one
 // 128-byte row segment) and run ST_RING K steps ahead in registers; one LDS
 // stage holds the step being multiplied.
+template <bool GATHER = false>
 __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(StreamArgs args) {
     __shared__ __attribute__((aligned(16))) bf16_t As[ST_M * LDK];
     __shared__ __attribute__((aligned(16))) bf16_t Bs[ST_N * LDK];
@@ -489,15 +511,20 @@ __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(S
         const int bvalid = min(ST_N, args.N - n0);
         const int kt0 = (int)((int64_t)c * KT / S), kt1 = (int)((int64_t)(c + 1) * KT / S);
 
-        const __amdgpu_buffer_rsrc_t ar = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)(args.a + (int64_t)row0 * K), (short)0, rows_valid * K * 2, RSRC_WORD3);
+        const __amdgpu_buffer_rsrc_t ar =
+            GATHER ? __builtin_amdgcn_make_buffer_rsrc((void*)args.a, (short)0, args.a_total * K * 2,
+                                                      RSRC_WORD3)
+                   : __builtin_amdgcn_make_buffer_rsrc((void*)(args.a + (int64_t)row0 * K), (short)0,
+                                                      rows_valid * K * 2, RSRC_WORD3);
+        const int avoff = !GATHER ? voff
+                          : lrow < rows_valid ? (args.a_rows[row0 + lrow] * K + kc) * 2 : A_OOB;
         const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
             (void*)(args.w[g] + (int64_t)n0 * K), (short)0, bvalid * K * 2, RSRC_WORD3);
 
         uint4 ring_a[ST_RING + 1], ring_b[ST_RING + 1][ST_B_PER];
         auto load = [&](int kt, uint4& ra, uint4* rb) {
             const int so = kt * 128;
-            ra = buffer_load16(ar, voff, so);
+            ra = buffer_load16(ar, avoff, so);
 #pragma unroll
             for (int i = 0; i < ST_B_PER; ++i) rb[i] = buffer_load16(br, voff + i * vstep, so);
         };
@@ -681,6 +708,7 @@ __device__ __forceinline__ int find_group(const int* off, int n_groups, int p) {
 }
 
 __global__ __launch_bounds__(256) void ffn1_f32_kernel(const float* __restrict__ x,
+                                                       const int32_t* __restrict__ a_rows,
                                                        const int32_t* __restrict__ offsets,
                                                        int n_groups, PtrTable w13, int d, int f,
                                                        float* __restrict__ h) {
@@ -693,7 +721,7 @@ __global__ __launch_bounds__(256) void ffn1_f32_kernel(const float* __restrict__
         const int p = (int)(i / f), j = (int)(i % f);
         const int s = find_group(s_off, n_groups, p);
         const float* W = w13.p[s];
-        const float* xr = x + (int64_t)p * d;
+        const float* xr = x + (int64_t)(a_rows ? a_rows[p] : p) * d;
         float a = 0.f, b = 0.f;
         for (int q = 0; q < d; ++q) {
             a = fmaf(W[(int64_t)j * d + q], xr[q], a);
@@ -763,7 +791,8 @@ size_t grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_gro
 
 int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, int n_groups,
                        const void* const* w13, const void* const* w2, int d, int f,
-                       int64_t cap_rows, void* y_perm, void* ws, hipStream_t s) {
+                       int64_t cap_rows, void* y_perm, void* ws, hipStream_t s,
+                       const int32_t* a_rows, int64_t a_total) {
     if (cap_rows == 0) return MOE_OK;
     if (dtype == MOE_F32) {
         PtrTable t13, t2;
@@ -776,7 +805,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
         if (b1 > 4096) b1 = 4096;
         if (b2 > 4096) b2 = 4096;
         hipLaunchKernelGGL(ffn1_f32_kernel, dim3((unsigned)b1), dim3(256), 0, s,
-                           (const float*)x_perm, offsets, n_groups, t13, d, f, h);
+                           (const float*)x_perm, a_rows, offsets, n_groups, t13, d, f, h);
         hipLaunchKernelGGL(ffn2_f32_kernel, dim3((unsigned)b2), dim3(256), 0, s, (const float*)h,
                            offsets, n_groups, t2, d, f, (float*)y_perm);
         return launch_status();
@@ -817,7 +846,12 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a1.part = tpart;
     a1.split_info = tinfo;
     a1.split_units = grid < TILE_SPLIT_UNITS ? grid : TILE_SPLIT_UNITS;
-    hipLaunchKernelGGL(grouped_gemm_kernel<true>, dim3(grid), dim3(GEMM_THREADS), 0, s, a1);
+    a1.a_rows = a_rows;
+    a1.a_total = (int)a_total;
+    if (a_rows)
+        hipLaunchKernelGGL((grouped_gemm_kernel<true, true>), dim3(grid), dim3(GEMM_THREADS), 0, s, a1);
+    else
+        hipLaunchKernelGGL((grouped_gemm_kernel<true, false>), dim3(grid), dim3(GEMM_THREADS), 0, s, a1);
     StreamArgs s1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) s1.w[i] = a1.w[i];
     s1.offsets = offsets;
@@ -830,7 +864,12 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s1.ldo = f;
     s1.part_rows = (int)(PART_FACTOR * rmax);
     s1.grid = sgrid;
-    hipLaunchKernelGGL(stream_gemm_kernel, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
+    s1.a_rows = a_rows;
+    s1.a_total = (int)a_total;
+    if (a_rows)
+        hipLaunchKernelGGL(stream_gemm_kernel<true>, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
+    else
+        hipLaunchKernelGGL(stream_gemm_kernel<false>, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
     hipLaunchKernelGGL(split_reduce_kernel<true>, dim3(rgrid), dim3(ST_THREADS), 0, s, s1, a1);
 
     // down product
@@ -844,7 +883,8 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a2.up_row = 0;
     a2.n_tiles = (int)ceil_div(d, BNW);
     a2.split_info = tinfo ? tinfo + 1 : nullptr;
-    hipLaunchKernelGGL(grouped_gemm_kernel<false>, dim3(grid), dim3(GEMM_THREADS), 0, s, a2);
+    a2.a_rows = nullptr;
+    hipLaunchKernelGGL((grouped_gemm_kernel<false, false>), dim3(grid), dim3(GEMM_THREADS), 0, s, a2);
     StreamArgs s2 = s1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) s2.w[i] = a2.w[i];
     s2.a = h;
@@ -852,7 +892,8 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s2.K = f;
     s2.N = d;
     s2.ldo = d;
-    hipLaunchKernelGGL(stream_gemm_kernel, dim3(sgrid), dim3(ST_THREADS), 0, s, s2);
+    s2.a_rows = nullptr;
+    hipLaunchKernelGGL(stream_gemm_kernel<false>, dim3(sgrid), dim3(ST_THREADS), 0, s, s2);
     hipLaunchKernelGGL(split_reduce_kernel<false>, dim3(rgrid), dim3(ST_THREADS), 0, s, s2, a2);
     return launch_status();
 }

@@ -43,7 +43,8 @@ class LayerShare:
     def __init__(self, X: torch.Tensor, Wr: torch.Tensor, bias: Optional[torch.Tensor], k: int,
                  placement: np.ndarray, dev: int, w13: Sequence[torch.Tensor],
                  w2: Sequence[torch.Tensor], shared=(), renorm: bool = True,
-                 coact: bool = False, want_logits: bool = True, cap_rows: Optional[int] = None):
+                 coact: bool = False, want_logits: bool = True, cap_rows: Optional[int] = None,
+                 gather_in_ffn: bool = False):
         self.device = X.device
         self.X = X
         self.Wr = Wr
@@ -54,6 +55,9 @@ class LayerShare:
         self.dev = dev
         self.renorm = renorm
         self.want_coact = coact
+        # gather_in_ffn: the permute step writes only the row maps and the expert
+        # FFN reads its rows from X through row_token (moe_grouped_ffn_rows)
+        self.gather_in_ffn = gather_in_ffn
         self.placement = np.ascontiguousarray(placement, dtype=np.uint8)
         self.G = self.placement.shape[1]
         self.n_local = int(self.placement[:, dev].sum())
@@ -70,7 +74,7 @@ class LayerShare:
         self.coact = torch.empty((E, E), dtype=torch.int32, device=dv) if coact else None
         cap = max(self.cap_rows, 1)
         self.perm = {
-            "x_perm": torch.empty((cap, d), dtype=dt, device=dv),
+            "x_perm": None if gather_in_ffn else torch.empty((cap, d), dtype=dt, device=dv),
             "group_offsets": torch.empty((self.n_local + 1,), dtype=torch.int32, device=dv),
             "row_token": torch.empty((cap,), dtype=torch.int32, device=dv),
             "row_gate": torch.empty((cap,), dtype=torch.float32, device=dv),
@@ -127,10 +131,16 @@ class LayerShare:
         self.route(logits_in)
         moe.moe_expert_histogram(self.topk_idx, self.E, counts=self.counts, coact=self.coact)
         moe.moe_permute(self.X, self.topk_idx, self.topk_gate, self.counts, self.placement,
-                        self.dev, E=self.E, cap_rows=self.cap_rows, out=self.perm, ws=self.ws_perm)
+                        self.dev, E=self.E, cap_rows=self.cap_rows, out=self.perm, ws=self.ws_perm,
+                        copy_rows=not self.gather_in_ffn)
         if self.weights is not None:
-            moe.moe_grouped_ffn(self.perm["x_perm"], self.perm["group_offsets"], self.weights,
-                                cap_rows=self.cap_rows, y_perm=self.y_perm, ws=self.ws_ffn)
+            if self.gather_in_ffn:
+                moe.moe_grouped_ffn_rows(self.X, self.perm["row_token"], self.perm["group_offsets"],
+                                         self.weights, cap_rows=self.cap_rows, y_perm=self.y_perm,
+                                         ws=self.ws_ffn)
+            else:
+                moe.moe_grouped_ffn(self.perm["x_perm"], self.perm["group_offsets"], self.weights,
+                                    cap_rows=self.cap_rows, y_perm=self.y_perm, ws=self.ws_ffn)
         if self.shared_weights is not None:
             moe.moe_grouped_ffn(self.X, self.shared_offsets, self.shared_weights, cap_rows=self.T,
                                 y_perm=self.y_shared, ws=self.ws_shared)

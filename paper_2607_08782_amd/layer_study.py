@@ -4,8 +4,9 @@ For each shape (Mixtral-8x7B, DeepSeek-V2-Lite, Qwen1.5-MoE-A2.7B and
 Qwen3-30B-A3B-shaped shares; prefill and decode batches) and each seed 0-4:
 synthetic inputs of that shape (seeded normal hidden states and weights, Zipf
 popularity bias, the benchmark placement), the five calls captured in one HIP
-graph, and the step timed over graph replays; the grouped FFN call is timed the
-same way on its own.  Reported: tokens/s, the FFN's rate against the bf16 MFMA
+graph, and the step timed over graph replays (also with the row copy x_perm
+elided: the expert FFN reading token rows through the row map); the grouped
+FFN call is timed the same way on its own.  Reported: tokens/s, the FFN's rate against the bf16 MFMA
 peak (6 d f N flop) and against HBM (weights of the active local experts read
 once plus x_perm in and y_perm out), mean and spread over the seeds.
 
@@ -68,13 +69,15 @@ def measure(name, regime, seed, steps):
     inp = synth.make_layer(cfg, T, seed=seed, device="cuda")
     wbytes = sum(w.numel() * 2 for w in inp.w13) + sum(w.numel() * 2 for w in inp.w2)
     copies = 1 if wbytes >= 1e9 else int(math.ceil(1e9 / max(wbytes, 1)))
-    shares = []
+    shares, gshares = [], []
     for c in range(copies):
         w13 = inp.w13 if c == 0 else [w.clone() for w in inp.w13]
         w2 = inp.w2 if c == 0 else [w.clone() for w in inp.w2]
         shares.append(LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, w13, w2,
                                  shared=inp.shared, coact=cfg.coact))
-    for s in shares:
+        gshares.append(LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, w13, w2,
+                                  shared=inp.shared, coact=cfg.coact, gather_in_ffn=True))
+    for s in shares + gshares:
         s.run()
     torch.cuda.synchronize()
     s0 = shares[0]
@@ -82,19 +85,22 @@ def measure(name, regime, seed, steps):
     sizes = np.diff(go)
     N, active = int(go[-1]), int((sizes > 0).sum())
     step_graphs = [_graph(s.run) for s in shares]
+    gather_graphs = [_graph(s.run) for s in gshares]
 
     def ffn(s):
         return lambda: moe.moe_grouped_ffn(s.perm["x_perm"], s.perm["group_offsets"], s.weights,
                                            cap_rows=s.cap_rows, y_perm=s.y_perm, ws=s.ws_ffn)
     ffn_graphs = [_graph(ffn(s)) for s in shares]
     step_us = _time(step_graphs, steps)
+    gather_us = _time(gather_graphs, steps)
     ffn_us = _time(ffn_graphs, steps)
     flops = 6.0 * cfg.d * cfg.f * N
     fbytes = active * 3.0 * cfg.d * cfg.f * 2 + 2.0 * N * cfg.d * 2
     out = {"T": T, "N": N, "active": active, "slots": len(sizes), "copies": copies,
            "step_us": step_us, "tok_s": T / (step_us * 1e-6), "ffn_us": ffn_us,
+           "gather_us": gather_us,
            "ffn_tflops": flops / (ffn_us * 1e-6) / 1e12, "ffn_gbs": fbytes / (ffn_us * 1e-6) / 1e9}
-    del step_graphs, ffn_graphs, shares
+    del step_graphs, gather_graphs, ffn_graphs, shares, gshares
     torch.cuda.synchronize()
     return out
 
@@ -122,8 +128,9 @@ def main(argv=None):
         sd = lambda k: statistics.pstdev(r[k] for r in res)
         row = {"name": name, "regime": regime, "res": res, "m": m, "sd": sd}
         rows.append(row)
-        print("%s/%s: step %.1f us (%.3g tok/s), FFN %.1f us = %.0f TFLOP/s, %.0f GB/s; N %.0f, "
-              "active %.1f, copies %d" % (name, regime, m("step_us"), m("tok_s"), m("ffn_us"),
+        print("%s/%s: step %.1f us (%.3g tok/s), gathered step %.1f us, FFN %.1f us = %.0f TFLOP/s, "
+              "%.0f GB/s; N %.0f, active %.1f, copies %d" % (name, regime, m("step_us"), m("tok_s"),
+                                                            m("gather_us"), m("ffn_us"),
                                           m("ffn_tflops"), m("ffn_gbs"), m("N"), m("active"),
                                           res[0]["copies"]), flush=True)
     lines = ["# The layer share at every model shape and regime", "",
@@ -136,16 +143,20 @@ def main(argv=None):
              % (args.steps * 10),
              "(2.5 PFLOP/s, algorithmic 6·d·f·N flop) and against HBM (8 TB/s, algorithmic bytes: the",
              "active local experts' weights once, x_perm in, y_perm out).  Weight copies: replays",
-             "cycle through this many copies of the local expert weights (≥ 1 GB touched).", "",
+             "cycle through this many copies of the local expert weights (≥ 1 GB touched).",
+             "Gathered step: the same share with the row copy x_perm elided (moe_permute writes the",
+             "row maps only and moe_grouped_ffn_rows reads the token rows through row_token;",
+             "bitwise the same output).", "",
              "Command: `python -m paper_2607_08782_amd.layer_study --seeds %d --steps %d --out %s`"
              % (args.seeds, args.steps, args.out), "",
-             "| shape / regime | T | rows here N | active / local experts | weight copies | step us | tokens/s | FFN us | FFN TFLOP/s (% bf16 peak) | FFN GB/s (% HBM peak) |",
-             "|---|---|---|---|---|---|---|---|---|---|"]
+             "| shape / regime | T | rows here N | active / local experts | weight copies | step us | tokens/s | gathered step us | FFN us | FFN TFLOP/s (% bf16 peak) | FFN GB/s (% HBM peak) |",
+             "|---|---|---|---|---|---|---|---|---|---|---|"]
     for r in rows:
         m, sd, res = r["m"], r["sd"], r["res"]
-        lines.append("| %s/%s | %d | %.0f | %.1f / %d | %d | %.1f ± %.1f | %.3g | %.1f ± %.1f | %.0f (%.1f %%) | %.0f (%.1f %%) |" % (
+        lines.append("| %s/%s | %d | %.0f | %.1f / %d | %d | %.1f ± %.1f | %.3g | %.1f | %.1f ± %.1f | %.0f (%.1f %%) | %.0f (%.1f %%) |" % (
             r["name"], r["regime"], res[0]["T"], m("N"), m("active"), res[0]["slots"],
-            res[0]["copies"], m("step_us"), sd("step_us"), m("tok_s"), m("ffn_us"), sd("ffn_us"),
+            res[0]["copies"], m("step_us"), sd("step_us"), m("tok_s"), m("gather_us"), m("ffn_us"),
+            sd("ffn_us"),
             m("ffn_tflops"), 100 * m("ffn_tflops") * 1e12 / PEAK_BF16_FLOPS, m("ffn_gbs"),
             100 * m("ffn_gbs") * 1e9 / PEAK_HBM_BYTES))
     lines.append("")

@@ -26,7 +26,8 @@ MOE_MAX_E, MOE_MAX_K, MOE_MAX_G, MOE_MAX_GROUPS = 256, 16, 64, 128
 
 EXPORTS = ("moe_status_string", "moe_route_topk", "moe_route_topk_ws_bytes",
            "moe_expert_histogram", "moe_permute_ws_bytes",
-           "moe_permute", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_combine",
+           "moe_permute", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_grouped_ffn_rows",
+           "moe_combine",
            "moe_quantize_e4m3", "moe_route_topk_e4m3")
 
 _lib = None
@@ -63,6 +64,8 @@ def load_library(path: str = LIB_PATH):
     lib.moe_grouped_ffn_ws_bytes.restype = S
     lib.moe_grouped_ffn.argtypes = [P, I, P, I, P, P, I, I, L, P, P, S, P]
     lib.moe_grouped_ffn.restype = I
+    lib.moe_grouped_ffn_rows.argtypes = [P, L, P, I, P, I, P, P, I, I, L, P, P, S, P]
+    lib.moe_grouped_ffn_rows.restype = I
     lib.moe_combine.argtypes = [P, I, P, P, P, L, I, I, P, P]
     lib.moe_combine.restype = I
     lib.moe_quantize_e4m3.argtypes = [P, I, L, I, P, P, P]
@@ -240,9 +243,12 @@ def workspace(nbytes: int, device) -> torch.Tensor:
 def moe_permute(x: torch.Tensor, topk_idx: torch.Tensor, topk_gate: torch.Tensor,
                 counts: torch.Tensor, placement: np.ndarray, dev: int, *, E: int,
                 cap_rows: Optional[int] = None, c_max: int = 0, out: Optional[dict] = None,
-                ws: Optional[torch.Tensor] = None, want_send_counts: bool = True, stream=None):
+                ws: Optional[torch.Tensor] = None, want_send_counts: bool = True,
+                copy_rows: bool = True, stream=None):
     """Package tokens for the experts on GPU `dev`.  Returns a dict of device tensors
-    (x_perm, group_offsets, row_token, row_gate, token_row, send_counts)."""
+    (x_perm, group_offsets, row_token, row_gate, token_row, send_counts).  With
+    copy_rows=False only the row maps are produced (x_perm is not written; for
+    moe_grouped_ffn_rows)."""
     lib = load_library()
     T, d = x.shape
     k = topk_idx.shape[1]
@@ -255,8 +261,9 @@ def moe_permute(x: torch.Tensor, topk_idx: torch.Tensor, topk_gate: torch.Tensor
         cap_rows = T * min(k, n_local)
     device = x.device
     o = {} if out is None else out
-    if "x_perm" not in o:
-        o["x_perm"] = _empty((max(cap_rows, 1), d), x.dtype, device)
+    if "group_offsets" not in o:
+        if copy_rows:
+            o["x_perm"] = _empty((max(cap_rows, 1), d), x.dtype, device)
         o["group_offsets"] = _empty((n_local + 1,), torch.int32, device)
         o["row_token"] = _empty((max(cap_rows, 1),), torch.int32, device)
         o["row_gate"] = _empty((max(cap_rows, 1),), torch.float32, device)
@@ -264,11 +271,12 @@ def moe_permute(x: torch.Tensor, topk_idx: torch.Tensor, topk_gate: torch.Tensor
         o["send_counts"] = _empty((G,), torch.int32, device) if want_send_counts else None
     if ws is None:
         ws = workspace(moe_permute_ws_bytes(T, k, E), device)
-    st = lib.moe_permute(_dev(x, "x"), _dtype_code(x), _dev(topk_idx, "topk_idx", torch.int32),
+    st = lib.moe_permute(_dev(x, "x") if copy_rows else None, _dtype_code(x),
+                         _dev(topk_idx, "topk_idx", torch.int32),
                          _dev(topk_gate, "topk_gate", torch.float32),
-                         _dev(counts, "counts", torch.int32), T, d, k, E,
+                         _dev(counts, "counts", torch.int32), T, d if copy_rows else 0, k, E,
                          placement.ctypes.data_as(ctypes.c_void_p), G, dev, c_max,
-                         _dev(o["x_perm"], "x_perm", x.dtype), cap_rows,
+                         _dev(o["x_perm"], "x_perm", x.dtype) if copy_rows else None, cap_rows,
                          _dev(o["group_offsets"], "group_offsets", torch.int32),
                          _dev(o["row_token"], "row_token", torch.int32),
                          _dev(o["row_gate"], "row_gate", torch.float32),
@@ -327,6 +335,33 @@ def moe_grouped_ffn(x_perm: torch.Tensor, group_offsets: torch.Tensor, weights: 
                              _dev(y_perm, "y_perm", x_perm.dtype), _dev(ws, "ws"), ws.numel(),
                              _stream(stream))
     _check("moe_grouped_ffn", st)
+    return y_perm
+
+
+def moe_grouped_ffn_rows(x: torch.Tensor, row_token: torch.Tensor, group_offsets: torch.Tensor,
+                         weights: WeightTable, *, cap_rows: int,
+                         y_perm: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                         stream=None) -> torch.Tensor:
+    """moe_grouped_ffn reading row p from x[row_token[p]] (no x_perm).  Returns y_perm."""
+    lib = load_library()
+    T = x.shape[0]
+    d, f = weights.d, weights.f
+    dtype = _dtype_code(x)
+    if x.dtype != weights.dtype or x.shape[1] != d:
+        raise ValueError("x must be [T, d] of the weights' dtype")
+    if group_offsets.numel() != len(weights) + 1:
+        raise ValueError("group_offsets must hold n_groups + 1 entries")
+    if y_perm is None:
+        y_perm = _empty((max(cap_rows, 1), d), x.dtype, x.device)
+    if ws is None:
+        ws = workspace(moe_grouped_ffn_ws_bytes(dtype, cap_rows, d, f, len(weights)), x.device)
+    st = lib.moe_grouped_ffn_rows(_dev(x, "x"), T, _dev(row_token, "row_token", torch.int32),
+                                  dtype, _dev(group_offsets, "group_offsets", torch.int32),
+                                  len(weights), ctypes.cast(weights.p13, ctypes.c_void_p),
+                                  ctypes.cast(weights.p2, ctypes.c_void_p), d, f, cap_rows,
+                                  _dev(y_perm, "y_perm", x.dtype), _dev(ws, "ws"), ws.numel(),
+                                  _stream(stream))
+    _check("moe_grouped_ffn_rows", st)
     return y_perm
 
 

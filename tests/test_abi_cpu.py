@@ -138,6 +138,25 @@ def test_grouped_ffn_validation(lib):
     assert call(dtype=3) == moe.MOE_ERR_ARG
 
 
+def test_grouped_ffn_rows_validation(lib):
+    f = lib.moe_grouped_ffn_rows
+    arr = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    P = ctypes.cast(arr, ctypes.c_void_p)
+
+    def call(T=64, rows=FAKE, dtype=1, d=128, f_=64, cap=16, x=FAKE, ws=0x100000, ws_bytes=1 << 30):
+        return f(x, T, rows, dtype, FAKE, 2, P, P, d, f_, cap, FAKE, ctypes.c_void_p(ws), ws_bytes,
+                 None)
+    assert call(rows=None) == moe.MOE_ERR_ARG               # no row map
+    assert call(x=None) == moe.MOE_ERR_ARG
+    assert call(T=-1) == moe.MOE_ERR_ARG
+    assert call(T=0) == moe.MOE_ERR_ARG                     # rows to compute but no token rows
+    assert call(T=1 << 24, d=128) == moe.MOE_ERR_SHAPE      # T*d*2 past 32-bit row offsets
+    assert call(d=100) == moe.MOE_ERR_SHAPE
+    assert call(x=FAKE.value + 8) == moe.MOE_ERR_ARG        # bf16 rows not 16-byte aligned
+    assert call(ws_bytes=10) == moe.MOE_ERR_SHAPE
+    assert call(dtype=3) == moe.MOE_ERR_ARG
+
+
 def test_combine_validation(lib):
     f = lib.moe_combine
     assert f(FAKE, 1, FAKE, FAKE, None, 4, 64, 0, FAKE, None) == moe.MOE_ERR_ARG

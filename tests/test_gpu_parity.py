@@ -251,6 +251,71 @@ def test_histogram_with_coactivation_every_bin(T, k, E, offset):
     np.testing.assert_array_equal(coact.cpu().numpy(), rco)
 
 
+def _both_paths(cfg, T, logits=None, seed=1):
+    """The same share run with x_perm materialised and with the gather in the FFN."""
+    inp = synth.make_layer(cfg, T, seed=seed, device="cuda")
+    outs = []
+    for gather in (False, True):
+        share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                           shared=inp.shared, coact=cfg.coact, gather_in_ffn=gather)
+        share.run(logits_in=logits)
+        torch.cuda.synchronize()
+        N = int(share.perm["group_offsets"][-1])
+        outs.append((share.y.clone(), share.y_perm[:N].clone(), share.perm["row_token"][:N].clone()))
+    return outs
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_gather_in_ffn_is_bitwise_equal_to_the_packaged_path(name):
+    """moe_permute with row maps only + moe_grouped_ffn_rows gives the same bits as
+    moe_permute + moe_grouped_ffn (which the oracle checks): the rows are read from X
+    through row_token instead of from the packaged copy."""
+    cfg, T = SMALL[name]
+    say("[gather]", name, "T=%d" % T)
+    (y0, yp0, rt0), (y1, yp1, rt1) = _both_paths(cfg, T)
+    assert torch.equal(rt0, rt1)
+    assert torch.equal(yp0, yp1)
+    assert torch.equal(y0, y1)
+
+
+@pytest.mark.parametrize("sizes,d,f", [([64, 65, 1, 0, 200, 33], 256, 192),
+                                       ([300, 96, 0, 70], 1024, 2048),
+                                       ([5, 17, 1300], 256, 128)])
+def test_gather_in_ffn_across_the_streaming_and_split_paths(sizes, d, f):
+    """Group sizes on both sides of the 64-row streaming threshold and mid-sized groups
+    whose tiles split K: the gathered path matches the packaged one bit for bit and
+    the oracle's FFN of the packaged rows within the bf16 tolerance."""
+    E = len(sizes)
+    cfg = synth.custom_config(d=d, E=E, k=1, f=f, G=1)
+    T = sum(sizes)
+    owner = np.repeat(np.arange(E), sizes)
+    np.random.default_rng(11).shuffle(owner)
+    L = np.zeros((T, E), np.float32)
+    L[np.arange(T), owner] = 1.0
+    Lg = torch.from_numpy(L).cuda()
+    (y0, yp0, _), (y1, yp1, rt) = _both_paths(cfg, T, logits=Lg)
+    assert torch.equal(yp0, yp1) and torch.equal(y0, y1)
+    inp = synth.make_layer(cfg, T, seed=1, device="cuda")
+    X = np32(inp.X)
+    idx, gate = oracle.topk(L, 1)
+    pm = oracle.permute(X, idx, gate, E, inp.placement, 0)
+    go = pm["group_offsets"]
+    for s_ in range(E):
+        if sizes[s_]:
+            ref = oracle.expert_ffn(pm["x_perm"][go[s_]:go[s_ + 1]], np32(inp.w13[s_]), np32(inp.w2[s_]))
+            close(np32(yp1[go[s_]:go[s_ + 1]]), ref, OUT_TOL["bf16"], "group %d" % s_)
+
+
+@pytest.mark.parametrize("name,regime", [("mixtral_8x7b", "prefill"), ("mixtral_8x7b", "decode"),
+                                         ("qwen3_30b_a3b", "prefill")])
+def test_gather_in_ffn_at_model_shapes(name, regime):
+    cfg = synth.CONFIGS[name]
+    T = cfg.T(regime)
+    say("[gather-full]", name, regime, "T=%d" % T)
+    (y0, yp0, _), (y1, yp1, _) = _both_paths(cfg, T, seed=0)
+    assert torch.equal(yp0, yp1) and torch.equal(y0, y1)
+
+
 def test_gpu_hosting_no_expert_returns_shared_output_only():
     cfg = synth.custom_config(d=128, E=4, k=2, f=64, shared_f=(128,), G=2)
     pl = np.zeros((4, 2), np.uint8)
