@@ -198,6 +198,9 @@ def main():
     ap.add_argument("--workload", default="mixtral_8x7b:prefill")
     ap.add_argument("--decode", default="decode", help="regime reported beside the headline ('' = none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gather-variant", action="store_true",
+                    help="skip the gather_in_ffn timing (a profiled run then dispatches only the "
+                         "packaged path, in the order profsum expects)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run a plain elementwise copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -258,8 +261,9 @@ def main():
             "algorithmic_flops_per_launch": flops, "avg_launch_us": t_ffn * 1e6,
         },
         "phases_us": {k: v * 1e3 for k, v in phases.items()},
-        "gather_in_ffn": gathered_variant(inp, share, weights, cfg, args.steps, args.warmup),
     }
+    if not args.no_gather_variant:
+        out["gather_in_ffn"] = gathered_variant(inp, share, weights, cfg, args.steps, args.warmup)
     if args.decode and args.decode in dict(cfg.regimes) and args.decode != regime:
         Td = cfg.T(args.decode)
         dinp, dshare, _ = make_share(cfg, Td, weights=weights)
@@ -277,9 +281,10 @@ def main():
                          "traffic_unit": "bytes per launch",
                          "algorithmic_bytes_per_launch": dby, "avg_launch_us": dt * 1e6},
             "phases_us": {k: v * 1e3 for k, v in dph.items()},
-            "gather_in_ffn": gathered_variant(dinp, dshare, weights, cfg, max(args.steps * 5, 50),
-                                              args.warmup * 2),
         }
+        if not args.no_gather_variant:
+            out["decode"]["gather_in_ffn"] = gathered_variant(
+                dinp, dshare, weights, cfg, max(args.steps * 5, 50), args.warmup * 2)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, inp, *weights, T)
     print(json.dumps(out), flush=True)

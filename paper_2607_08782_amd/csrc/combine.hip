@@ -73,9 +73,9 @@ __global__ __launch_bounds__(COMBINE_THREADS) void combine_kernel(
     if (t >= T) return;
     const int col = c * V;
     // The k row indices and gates first, then every row load at once: an
-    // assignment with no row here (or a slot past k) reads this thread's own
-    // output chunk (always valid memory) and is dropped by the select, so no
-    // load sits behind a branch.
+    // assignment with no row here (or a slot past k) re-reads the token's first
+    // row here (a cache hit) and is dropped by the select, so no load sits
+    // behind a branch; a token with no row here loads none.
     int32_t p[KM];
     float g[KM];
 #pragma unroll
@@ -84,18 +84,22 @@ __global__ __launch_bounds__(COMBINE_THREADS) void combine_kernel(
         p[r] = r < k ? token_row[t * k + rr] : -1;
         g[r] = gate[t * k + rr];
     }
-    const Elem* self = y + t * d + col;
-    float v[KM][V];
+    int32_t first = -1;
 #pragma unroll
-    for (int r = 0; r < KM; ++r)
-        Vec<Elem, V>::load(p[r] >= 0 ? y_perm + (int64_t)p[r] * d + col : self, v[r]);
+    for (int r = KM - 1; r >= 0; --r) first = p[r] >= 0 ? p[r] : first;
     float acc[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) acc[i] = 0.f;
+    if (first >= 0) {
+        float v[KM][V];
 #pragma unroll
-    for (int r = 0; r < KM; ++r)
+        for (int r = 0; r < KM; ++r)
+            Vec<Elem, V>::load(y_perm + (int64_t)(p[r] >= 0 ? p[r] : first) * d + col, v[r]);
 #pragma unroll
-        for (int i = 0; i < V; ++i) acc[i] = p[r] >= 0 ? fmaf(g[r], v[r][i], acc[i]) : acc[i];
+        for (int r = 0; r < KM; ++r)
+#pragma unroll
+            for (int i = 0; i < V; ++i) acc[i] = p[r] >= 0 ? fmaf(g[r], v[r][i], acc[i]) : acc[i];
+    }
     if (y_shared) {
         float w[V];
         Vec<Elem, V>::load(y_shared + t * d + col, w);

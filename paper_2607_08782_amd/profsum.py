@@ -1,8 +1,9 @@
 """Summaries of rocprofv3 runs of the default benchmark (`bench.py`).
 
-The benchmark runs the prefill batch first (27 dispatches of every kernel:
-3 warm-up + 10 eager timed + 3 + 10 graph replays + 1 final run), then the
-decode batch; the 28th gate-score dispatch marks the boundary.
+The benchmark (run with --no-gather-variant) runs the prefill batch first (27
+dispatches of every kernel: 3 warm-up + 10 eager timed + 3 + 10 graph replays
++ 1 final run), then the decode batch; the 28th gate-score dispatch marks the
+boundary.
 
     # per-call HBM traffic of moe_grouped_ffn, read by bench.py for `roofline.traffic`
     python -m paper_2607_08782_amd.profsum traffic <FETCH_SIZE csv> <WRITE_SIZE csv> \
@@ -26,8 +27,7 @@ import json
 import os
 
 PREFILL_DISPATCHES = 27
-FFN_KERNELS = ("grouped_gemm_kernel<true>", "stream_gemm_kernel", "split_reduce_kernel<true>",
-               "grouped_gemm_kernel<false>", "split_reduce_kernel<false>")
+FFN_KERNELS = ("grouped_gemm_kernel", "stream_gemm_kernel", "split_reduce_kernel")   # prefixes
 FFN_SOURCE = "paper_2607_08782_amd/csrc/ffn.hip"
 
 
@@ -70,13 +70,14 @@ def traffic(fetch_csv, write_csv, ff, wf, out, repo="."):
                                     ("write", write_csv, "WRITE_SIZE", wf)):
         pre, dec = counter_by_regime(path, counter, fac)
         for regime, per in (("prefill", pre), ("decode", dec)):
-            tot = sum(_mean(per[k]) * (2 if k.startswith("stream") else 1) for k in FFN_KERNELS)
+            tot = sum(_mean(v) * (2 if k.startswith("stream") else 1)
+                      for k, v in per.items() if k.startswith(FFN_KERNELS))
             res.setdefault("mixtral_8x7b:" + regime, {})[key] = tot
     res["commands"] = [
         "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pf -o pf -- python -u "
-        "bench.py --steps 10 --warmup 3 --no-cpu-baseline --calibrate-copy 1024",
+        "bench.py --steps 10 --warmup 3 --no-cpu-baseline --no-gather-variant --calibrate-copy 1024",
         "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pw -o pw -- python -u "
-        "bench.py --steps 10 --warmup 3 --no-cpu-baseline --calibrate-copy 1024"]
+        "bench.py --steps 10 --warmup 3 --no-cpu-baseline --no-gather-variant --calibrate-copy 1024"]
     with open(out, "w") as fh:
         json.dump(res, fh, indent=1)
     return res
