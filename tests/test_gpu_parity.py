@@ -38,6 +38,10 @@ SMALL = {
     "bf16_T1": (synth.custom_config(d=128, E=8, k=2, f=128, G=2), 1),
     "fp32_ragged": (synth.custom_config(dtype="f32", d=72, E=6, k=2, f=40, shared_f=(24,), G=2,
                                         replicas=1, zipf=1.0), 77),
+    "bf16_k16_max": (synth.custom_config(d=128, E=64, k=16, f=64, G=3, replicas=2, zipf=1.1,
+                                         coact=True), 150),
+    "bf16_k12": (synth.custom_config(d=64, E=40, k=12, f=64, shared_f=(64,), G=2, replicas=1,
+                                     zipf=1.0), 300),
 }
 
 
@@ -314,6 +318,19 @@ def test_gather_in_ffn_at_model_shapes(name, regime):
     say("[gather-full]", name, regime, "T=%d" % T)
     (y0, yp0, _), (y1, yp1, _) = _both_paths(cfg, T, seed=0)
     assert torch.equal(yp0, yp1) and torch.equal(y0, y1)
+
+
+def test_very_long_batch_routing_and_packaging_every_element():
+    """T = 100000 tokens at a small width: the long-batch paths of the gate (tiled
+    scores), histogram (several workgroups), permute (count / scan / scatter over
+    1563 blocks) and combine, routing outputs bit-exact and the combined output on
+    sampled tokens within the bf16 tolerance."""
+    cfg = synth.custom_config(d=64, E=48, k=4, f=64, G=2, replicas=1, zipf=1.2, coact=True)
+    say("[long]", "T=100000")
+    case = Case(cfg, 100000)
+    ref_logits, _ = check_logits(case)
+    idx, gate, pm = check_routing(case, ref_logits)
+    check_ffn_and_combine(case, idx, gate, pm, sample=64)
 
 
 def test_gpu_hosting_no_expert_returns_shared_output_only():
