@@ -50,8 +50,12 @@ struct GemmArgs {
     int ldo;
     int up_row;                        // SWIGLU: first row of W3 inside w[s] (= f)
     int n_tiles;                       // output-column tiles per group
-    int small_rows;                    // groups with at most this many rows are left to the
-                                       // split-K streaming kernel (no tiles here)
+    int* limits;                       // [2] row limits of the streamed groups of the gate/up and
+                                       // the down product (small_limits): the gate/up launch
+                                       // writes both, later launches read theirs; nullptr: no
+                                       // group exceeds SMALL_ROWS
+    int product;                       // 0 gate/up, 1 down
+    int down_tiles;                    // gate/up launch: the down product's column tiles
     float* part;                       // fp32 partial tiles for split K (nullptr: never split)
     int* split_info;                   // the kernel records its split factor here for the reduce
     int split_units;                   // workgroups split K aims to occupy (<= TILE_SPLIT_UNITS)
@@ -67,6 +71,11 @@ struct GemmArgs {
 // round trip, about 1/20 of a stage per unit (256 KB written and read back).
 constexpr int TILE_SPLIT_UNITS = 256;
 constexpr int TILE_SPLIT_MIN_STEPS = 8;
+
+// Groups of at most SMALL_ROWS rows always go to the split-K streaming kernel;
+// in a short call (see small_limits) groups of up to SMALL_ROWS_MAX rows do too.
+constexpr int SMALL_ROWS = 64;
+constexpr int SMALL_ROWS_MAX = 256;
 
 __host__ __device__ __forceinline__ int tile_split(int total, int KT, int split_units) {
     if (total <= 0 || 2 * total > split_units) return 1;
@@ -136,6 +145,28 @@ __device__ __forceinline__ void tile_starts(const int* s_off, int n_groups, int 
     if (lane == 0) s_tstart[0] = 0;
 }
 
+// Row limits of the streamed groups of the two products, run by one whole wave.
+// When the groups above SMALL_ROWS rows make so few tiles (a quarter of the
+// split units or fewer) that the tiled kernel would split K over them, its
+// launch is short and latency-bound: every workgroup still runs several K
+// stages of a 256 x 256 tile, on a fraction of the CUs.  Streaming every group
+// of up to SMALL_ROWS_MAX rows instead spreads the weight reads over all CUs
+// (a DeepSeek-V2-Lite-shaped decode step: 219 -> 188 us).
+__device__ __forceinline__ void small_limits(const int* s_off, int n_groups, int tiles_up,
+                                             int tiles_down, int split_units, int lane,
+                                             int& lim_up, int& lim_down) {
+    int mt = 0;                                      // 256-row tiles of the groups > SMALL_ROWS
+    for (int g0 = 0; g0 < n_groups; g0 += 64) {
+        const int g = g0 + lane;
+        const int rows = g < n_groups ? s_off[g + 1] - s_off[g] : 0;
+        mt += rows > SMALL_ROWS ? (int)ceil_div(rows, BM) : 0;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mt += __shfl_xor(mt, o, 64);
+    lim_up = 4 * mt * tiles_up <= split_units ? SMALL_ROWS_MAX : SMALL_ROWS;
+    lim_down = 4 * mt * tiles_down <= split_units ? SMALL_ROWS_MAX : SMALL_ROWS;
+}
+
 // Persistent grouped NT GEMM.  Per tile: operands stream through per-tile
 // buffer descriptors (rows past the group's end fall outside the descriptor and
 // read as zero), are staged through registers into a double-buffered LDS
@@ -158,9 +189,23 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
     const int n_groups = args.n_groups;
     const int BN_OUT = SWIGLU ? BNW / 2 : BNW;      // output columns per tile
 
+    // the down launch reads its row limit from the gate/up launch (no group can
+    // exceed SMALL_ROWS when there is nowhere to keep it)
+    int lim = args.limits != nullptr && args.product == 1 ? args.limits[1] : SMALL_ROWS;
     for (int s = tid; s <= n_groups; s += GEMM_THREADS) s_off[s] = args.offsets[s];
     __syncthreads();
-    if (wave == 0) tile_starts(s_off, n_groups, args.small_rows, args.n_tiles, s_tstart, lane);
+    if (wave == 0) {
+        if (args.limits != nullptr && args.product == 0) {
+            int lim_down;
+            small_limits(s_off, n_groups, args.n_tiles, args.down_tiles, args.split_units, lane, lim,
+                         lim_down);
+            if (blockIdx.x == 0 && lane == 0) {
+                args.limits[0] = lim;
+                args.limits[1] = lim_down;
+            }
+        }
+        tile_starts(s_off, n_groups, lim, args.n_tiles, s_tstart, lane);
+    }
     __syncthreads();
     const int KT = args.K / BK;
     const int K = args.K;
@@ -378,8 +423,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 }
 
 // ---------------------------------------------------------------------------
-// Small groups (decode-sized, at most SMALL_ROWS rows): weight streaming with
-// split-K.  Here the weights dominate the traffic (each weight byte is used by
+// Small groups (decode-sized: at most SMALL_ROWS rows, or SMALL_ROWS_MAX in a
+// short call, see small_limits): weight streaming with split-K.  Here the weights dominate the traffic (each weight byte is used by
 // a handful of rows), so the aim is to read every weight byte once, from all
 // CUs at once.  Work item = (group, 256 weight rows, K chunk, 32 rows); one
 // workgroup per item, fp32 partial sums per K chunk.  A second kernel adds the
@@ -388,7 +433,6 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 // The split factor S is derived on the device from the group sizes; both
 // kernels derive the same plan from the same inputs.
 // ---------------------------------------------------------------------------
-constexpr int SMALL_ROWS = 64;
 constexpr int ST_M = 32;                 // rows per item
 constexpr int ST_N = 256;                // weight rows per item (64 per wave)
 constexpr int ST_THREADS = 256;
@@ -414,6 +458,8 @@ struct StreamArgs {
     int grid;                            // workgroups of the streaming launch
     const int32_t* a_rows;               // gather: row p of A is a[a_rows[p]] (a holds a_total rows)
     int a_total;
+    const int* limits;                   // row limits written by the gate/up tiled launch (nullptr:
+    int product;                         // SMALL_ROWS); this product's index, 0 gate/up, 1 down
 };
 
 struct StreamPlan {
@@ -424,6 +470,7 @@ struct StreamPlan {
 };
 
 __device__ void make_stream_plan(const StreamArgs& a, StreamPlan& P, int nthreads) {
+    const int lim = a.limits != nullptr ? a.limits[a.product] : SMALL_ROWS;
     for (int g = threadIdx.x; g <= a.n_groups; g += nthreads) P.off[g] = a.offsets[g];
     __syncthreads();
     if (threadIdx.x < 64) {                          // one wave: prefix sums over the groups
@@ -434,7 +481,7 @@ __device__ void make_stream_plan(const StreamArgs& a, StreamPlan& P, int nthread
         for (int g0 = 0; g0 < a.n_groups; g0 += 64) {
             const int g = g0 + lane;
             const int rows = g < a.n_groups ? P.off[g + 1] - P.off[g] : 0;
-            const bool small = rows > 0 && rows <= SMALL_ROWS;
+            const bool small = rows > 0 && rows <= lim;
             const int rs = small ? rows : 0;
             const int items = small ? (int)ceil_div(rows, ST_M) * nt : 0;
             const int irs = wave_incl_scan(rs, lane), iit = wave_incl_scan(items, lane);
@@ -583,7 +630,8 @@ __device__ void tile_split_reduce(const GemmArgs& t, int* s_off, int* s_tstart) 
     const int n_groups = t.n_groups;
     for (int g = threadIdx.x; g <= n_groups; g += ST_THREADS) s_off[g] = t.offsets[g];
     __syncthreads();
-    if (threadIdx.x < 64) tile_starts(s_off, n_groups, t.small_rows, t.n_tiles, s_tstart, threadIdx.x);
+    const int lim = t.limits != nullptr ? t.limits[t.product] : SMALL_ROWS;
+    if (threadIdx.x < 64) tile_starts(s_off, n_groups, lim, t.n_tiles, s_tstart, threadIdx.x);
     __syncthreads();
     const SplitPlan plan = split_plan(s_tstart[n_groups], t.K / BK, t.split_units);
     const int S = plan.S;
@@ -816,8 +864,8 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     float* part = (float*)((char*)ws + align256(cap_rows * (int64_t)f * 2));
     const int64_t rmax = small_rows_bound(cap_rows, n_groups);
     const int64_t ncols = 2 * (int64_t)f > d ? 2 * (int64_t)f : d;
-    // tiled split K: two split factors (one per product) in a 256-byte header,
-    // then the partial tiles
+    // tiled split K: two split factors (one per product) and the two products'
+    // streamed-group row limits in a 256-byte header, then the partial tiles
     char* tbase = tile_part_bytes(cap_rows) > 0
                       ? (char*)part + align256((int64_t)PART_FACTOR * rmax * ncols * 4)
                       : nullptr;
@@ -842,7 +890,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a1.ldo = f;
     a1.up_row = f;
     a1.n_tiles = (int)ceil_div(f, BNW / 2);
-    a1.small_rows = SMALL_ROWS;
+    a1.limits = tinfo ? tinfo + 2 : nullptr;
+    a1.product = 0;
+    a1.down_tiles = (int)ceil_div(d, BNW);
     a1.part = tpart;
     a1.split_info = tinfo;
     a1.split_units = grid < TILE_SPLIT_UNITS ? grid : TILE_SPLIT_UNITS;
@@ -866,6 +916,8 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s1.grid = sgrid;
     s1.a_rows = a_rows;
     s1.a_total = (int)a_total;
+    s1.limits = a1.limits;
+    s1.product = 0;
     if (a_rows)
         hipLaunchKernelGGL(stream_gemm_kernel<true>, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
     else
@@ -883,6 +935,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a2.up_row = 0;
     a2.n_tiles = (int)ceil_div(d, BNW);
     a2.split_info = tinfo ? tinfo + 1 : nullptr;
+    a2.product = 1;
     a2.a_rows = nullptr;
     hipLaunchKernelGGL((grouped_gemm_kernel<false, false>), dim3(grid), dim3(GEMM_THREADS), 0, s, a2);
     StreamArgs s2 = s1;
@@ -893,6 +946,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s2.N = d;
     s2.ldo = d;
     s2.a_rows = nullptr;
+    s2.product = 1;
     hipLaunchKernelGGL(stream_gemm_kernel<false>, dim3(sgrid), dim3(ST_THREADS), 0, s, s2);
     hipLaunchKernelGGL(split_reduce_kernel<false>, dim3(rgrid), dim3(ST_THREADS), 0, s, s2, a2);
     return launch_status();

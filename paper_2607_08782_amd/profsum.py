@@ -13,6 +13,9 @@ boundary.
         <WRITE_SIZE csv> --fetch-factor 2 --write-factor 1
     # tiled-GEMM utilisation from a GRBM_GUI_ACTIVE / SQ_* counter run
     python -m paper_2607_08782_amd.profsum mfma <counter csv>
+    # where one step's time goes, per kernel, for kernel traces of
+    # `bench.py --workload NAME:REGIME --decode '' --no-gather-variant` runs
+    python -m paper_2607_08782_amd.profsum breakdown LABEL=<kernel-trace csv> ...
 
 The factors scale the counters to bytes: a plain copy kernel of known size
 (`bench.py --calibrate-copy`) reads back FETCH_SIZE x factor = its bytes.
@@ -144,6 +147,33 @@ def mfma(counter_csv, cus=256, simds=1024, xcds=8):
     return "\n".join(lines) + "\n"
 
 
+def breakdown(runs, steps=PREFILL_DISPATCHES):
+    """Markdown table per run: each kernel's launches per step, mean duration and
+    time per step (every dispatch of a run belongs to one of its `steps` steps)."""
+    lines = []
+    for label, path in runs:
+        with open(path) as fh:
+            rows = sorted(csv.DictReader(fh), key=lambda r: int(r["Start_Timestamp"]))
+        per, order = collections.defaultdict(list), []
+        for r in rows:
+            k = short(r["Kernel_Name"])
+            if k.startswith("at::") or "rocclr" in k:
+                continue
+            if k not in order:
+                order.append(k)
+            per[k].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0)
+        total = sum(sum(v) for v in per.values()) / steps
+        lines += ["#### %s" % label, "",
+                  "| kernel | launches per step | mean us | us per step | share |",
+                  "|---|---|---|---|---|"]
+        for k in order:
+            v = per[k]
+            lines.append("| `%s` | %.2f | %.1f | %.1f | %.1f %% |" % (
+                k, len(v) / steps, _mean(v), sum(v) / steps, 100 * sum(v) / steps / total))
+        lines += ["| all kernels | | | %.1f | |" % total, ""]
+    return "\n".join(lines)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -160,8 +190,12 @@ def main(argv=None):
         p.add_argument("--write-factor", type=float, required=True)
     u = sub.add_parser("mfma")
     u.add_argument("counter_csv")
+    b = sub.add_parser("breakdown")
+    b.add_argument("runs", nargs="+", help="LABEL=kernel-trace csv")
     args = ap.parse_args(argv)
-    if args.cmd == "mfma":
+    if args.cmd == "breakdown":
+        print(breakdown([r.split("=", 1) for r in args.runs]), end="")
+    elif args.cmd == "mfma":
         print(mfma(args.counter_csv), end="")
     elif args.cmd == "traffic":
         print(json.dumps(traffic(args.fetch_csv, args.write_csv, args.fetch_factor,

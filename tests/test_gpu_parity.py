@@ -284,11 +284,18 @@ def test_gather_in_ffn_is_bitwise_equal_to_the_packaged_path(name):
 
 @pytest.mark.parametrize("sizes,d,f", [([64, 65, 1, 0, 200, 33], 256, 192),
                                        ([300, 96, 0, 70], 1024, 2048),
-                                       ([5, 17, 1300], 256, 128)])
+                                       ([5, 17, 1300], 256, 128),
+                                       ([257, 256, 129, 65, 64, 3], 256, 256),
+                                       ([200, 200, 200, 200, 200, 65, 64], 256, 2048)])
 def test_gather_in_ffn_across_the_streaming_and_split_paths(sizes, d, f):
-    """Group sizes on both sides of the 64-row streaming threshold and mid-sized groups
-    whose tiles split K: the gathered path matches the packaged one bit for bit and
-    the oracle's FFN of the packaged rows within the bf16 tolerance."""
+    """Group sizes on both sides of the streaming limits and mid-sized groups whose
+    tiles split K: in a short call (few tiles) groups of up to 256 rows stream and a
+    257-row group is tiled; with 16 gate/up column tiles per group (f = 2048) the
+    200-row and 65-row groups make enough tiles to stay on the tiled kernel for that
+    product, while the down product (one column tile per group at d = 256) streams
+    them, so the two products split the groups differently.  The gathered path
+    matches the packaged one bit for bit and the oracle's FFN of the packaged rows
+    within the bf16 tolerance."""
     E = len(sizes)
     cfg = synth.custom_config(d=d, E=E, k=1, f=f, G=1)
     T = sum(sizes)
@@ -373,8 +380,9 @@ def test_doubling_w2_doubles_expert_outputs_exactly():
 
 
 def test_group_sizes_around_the_streaming_threshold():
-    """Groups of 64 and fewer rows take the split-K streaming kernels, larger ones the
-    tiled kernel; sizes 64 / 65 / 1 / 0 / 200 / 33 check both sides of the boundary."""
+    """Sizes 64 / 65 / 1 / 0 / 200 / 33 at f = 192: the two groups above 64 rows make
+    only 4 gate/up tiles, so this short call streams every group (the 65- and 200-row
+    ones included); each group must match the oracle."""
     sizes = [64, 65, 1, 0, 200, 33]
     E = len(sizes)
     cfg = synth.custom_config(d=256, E=E, k=1, f=192, G=1)
@@ -400,10 +408,11 @@ def test_group_sizes_around_the_streaming_threshold():
 
 
 def test_mid_sized_groups_split_k_in_the_tiled_kernel():
-    """Groups of 300 / 96 / 0 / 70 rows at d=1024, f=2048 give the tiled kernel 64
-    gate/up tiles (16 K stages) and 16 down tiles (32 K stages) for 256 CUs, so both
-    products split K (2 and 4 chunks) and finish in the reduce kernel.  Each group must
-    match the oracle, and two runs must agree bit for bit (chunks are summed in order)."""
+    """Groups of 300 / 96 / 0 / 70 rows at d=1024, f=2048: the 96- and 70-row groups
+    stream (a short call), the 300-row group gives the tiled kernel 32 gate/up tiles
+    (16 K stages) and 8 down tiles (32 K stages) for 256 CUs, so both products split K
+    (2 and 4 chunks) and finish in the reduce kernel.  Each group must match the
+    oracle, and two runs must agree bit for bit (chunks are summed in order)."""
     sizes = [300, 96, 0, 70]
     E = len(sizes)
     cfg = synth.custom_config(d=1024, E=E, k=1, f=2048, G=1)
