@@ -407,6 +407,56 @@ def test_group_sizes_around_the_streaming_threshold():
             close(np32(share.y_perm[go[s]:go[s + 1]]), ref, OUT_TOL["bf16"], "group %d" % s)
 
 
+def _random_sizes(rng):
+    """1-12 groups drawn from empty, <= 64, 65-256 and 257-600 rows."""
+    n = int(rng.integers(1, 13))
+    kinds = rng.choice(4, size=n, p=[0.15, 0.35, 0.35, 0.15])
+    lo, hi = (0, 1, 65, 257), (0, 64, 256, 600)
+    sizes = [int(rng.integers(lo[c], hi[c] + 1)) for c in kinds]
+    if sum(sizes) == 0:
+        sizes[0] = 1
+    return sizes
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_group_sizes_across_the_streaming_limits(seed):
+    """Random mixes of group sizes and shapes: which groups stream and which are tiled
+    is decided on the device per product (64 or 256 rows, by the tile count), and every
+    launch of the call must agree on it, or rows of H or y_perm would be left unwritten
+    or written twice.  Every group must match the oracle, and two runs must agree bit
+    for bit."""
+    rng = np.random.default_rng(100 + seed)
+    sizes = _random_sizes(rng)
+    d = int(rng.choice([128, 256, 512]))
+    f = int(rng.choice([128, 384, 1024, 2048]))
+    say("[random groups]", "seed", seed, "d", d, "f", f, "sizes", sizes)
+    E = len(sizes)
+    cfg = synth.custom_config(d=d, E=E, k=1, f=f, G=1)
+    T = sum(sizes)
+    owner = np.repeat(np.arange(E), sizes)
+    rng.shuffle(owner)
+    L = np.zeros((T, E), np.float32)
+    L[np.arange(T), owner] = 1.0
+    inp, share = _share(cfg, T)
+    Lg = torch.from_numpy(L).cuda()
+    share.run(logits_in=Lg)
+    torch.cuda.synchronize()
+    first = share.y_perm[:T].clone()
+    share.run(logits_in=Lg)
+    torch.cuda.synchronize()
+    assert torch.equal(first, share.y_perm[:T])
+    go = share.perm["group_offsets"].cpu().numpy()
+    assert np.diff(go).tolist() == sizes
+    X = np32(inp.X)
+    idx, gate = oracle.topk(L, 1)
+    pm = oracle.permute(X, idx, gate, E, inp.placement, 0)
+    for s in range(E):
+        if sizes[s]:
+            ref = oracle.expert_ffn(pm["x_perm"][go[s]:go[s + 1]], np32(share.weights.w13[s]),
+                                    np32(share.weights.w2[s]))
+            close(np32(share.y_perm[go[s]:go[s + 1]]), ref, OUT_TOL["bf16"], "group %d" % s)
+
+
 def test_mid_sized_groups_split_k_in_the_tiled_kernel():
     """Groups of 300 / 96 / 0 / 70 rows at d=1024, f=2048: the 96- and 70-row groups
     stream (a short call), the 300-row group gives the tiled kernel 32 gate/up tiles
