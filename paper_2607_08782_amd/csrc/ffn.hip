@@ -426,23 +426,27 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 // Small groups (decode-sized: at most SMALL_ROWS rows, or SMALL_ROWS_MAX in a
 // short call, see small_limits): weight streaming with split-K.  Here the weights dominate the traffic (each weight byte is used by
 // a handful of rows), so the aim is to read every weight byte once, from all
-// CUs at once.  Work item = (group, 256 weight rows, K chunk, 32 rows); one
-// workgroup per item, fp32 partial sums per K chunk.  A second kernel adds the
+// CUs at once.  Work item = (group, 128 weight rows, K chunk, 64 rows); one
+// workgroup per item, four per CU, fp32 partial sums per K chunk.  HBM reads
+// reach their rate only with many independent streams in flight (a read-only
+// probe over 448 MiB: 4.3-5.1 TB/s with 224-448 workgroups, 5.4-5.7 TB/s with
+// 896 or more), so the item is narrow in weight rows and covers a whole
+// decode-sized group (a group of up to 64 rows reads its weights once).  A second kernel adds the
 // chunks in a fixed order (so results are deterministic) and, for the gate/up
 // product, applies SiLU(a) * b.
 // The split factor S is derived on the device from the group sizes; both
 // kernels derive the same plan from the same inputs.
 // ---------------------------------------------------------------------------
-constexpr int ST_M = 32;                 // rows per item
-constexpr int ST_N = 256;                // weight rows per item (64 per wave)
+constexpr int ST_M = 64;                 // rows per item (two 32-row MFMA tiles per wave)
+constexpr int ST_N = 128;                // weight rows per item (32 per wave)
 constexpr int ST_THREADS = 256;
-constexpr int ST_WG_PER_CU = 3;
+constexpr int ST_WG_PER_CU = 4;
 constexpr int ST_RING = 1;               // K steps of loads in flight beyond the one in LDS
 constexpr int ST_A_PER = ST_M * 64 / 8 / ST_THREADS;   // 16-byte loads per thread per K step
 constexpr int ST_B_PER = ST_N * 64 / 8 / ST_THREADS;
 constexpr int SPLIT_MAX = 32;
 constexpr int PART_FACTOR = 8;           // partial capacity = PART_FACTOR x bound on small rows
-static_assert(ST_A_PER == 1 && ST_B_PER == 8, "streaming tile");
+static_assert(ST_A_PER == 2 && ST_B_PER == 4, "streaming tile");
 
 struct StreamArgs {
     const bf16_t* w[MOE_MAX_GROUPS];     // per group [N][K]
@@ -513,10 +517,14 @@ __device__ void make_stream_plan(const StreamArgs& a, StreamPlan& P, int nthread
     __syncthreads();
 }
 
-// One workgroup per item (32 rows x 256 weight rows x one K chunk); each wave
-// takes 64 of the weight rows.  Loads are coalesced (8 lanes read one
-// 128-byte row segment) and run ST_RING K steps ahead in registers; one LDS
-// stage holds the step being multiplied.
+// One workgroup per item (64 rows x 128 weight rows x one K chunk); each wave
+// takes 32 of the weight rows against both 32-row halves of the rows.  Loads
+// are coalesced (8 lanes read one 128-byte row segment) and run ST_RING K
+// steps ahead in registers; one LDS stage holds the step being multiplied.
+// The partial-sum epilogue adds a uniform row offset per accumulator element to
+// one per-lane pointer: with a 64-bit row offset per element and lane, the
+// compiler kept all of them live across the item loop and spilled them to
+// scratch (decode steps 5 % slower).
 template <bool GATHER = false>
 __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(StreamArgs args) {
     __shared__ __attribute__((aligned(16))) bf16_t As[ST_M * LDK];
@@ -563,15 +571,21 @@ __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(S
                                                       RSRC_WORD3)
                    : __builtin_amdgcn_make_buffer_rsrc((void*)(args.a + (int64_t)row0 * K), (short)0,
                                                       rows_valid * K * 2, RSRC_WORD3);
-        const int avoff = !GATHER ? voff
-                          : lrow < rows_valid ? (args.a_rows[row0 + lrow] * K + kc) * 2 : A_OOB;
+        int avoff[ST_A_PER];
+#pragma unroll
+        for (int q = 0; q < ST_A_PER; ++q) {
+            const int rin = lrow + 32 * q;
+            avoff[q] = !GATHER ? voff + q * vstep
+                       : rin < rows_valid ? (args.a_rows[row0 + rin] * K + kc) * 2 : A_OOB;
+        }
         const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(
             (void*)(args.w[g] + (int64_t)n0 * K), (short)0, bvalid * K * 2, RSRC_WORD3);
 
-        uint4 ring_a[ST_RING + 1], ring_b[ST_RING + 1][ST_B_PER];
-        auto load = [&](int kt, uint4& ra, uint4* rb) {
+        uint4 ring_a[ST_RING + 1][ST_A_PER], ring_b[ST_RING + 1][ST_B_PER];
+        auto load = [&](int kt, uint4* ra, uint4* rb) {
             const int so = kt * 128;
-            ra = buffer_load16(ar, avoff, so);
+#pragma unroll
+            for (int q = 0; q < ST_A_PER; ++q) ra[q] = buffer_load16(ar, avoff[q], so);
 #pragma unroll
             for (int i = 0; i < ST_B_PER; ++i) rb[i] = buffer_load16(br, voff + i * vstep, so);
         };
@@ -588,7 +602,9 @@ __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(S
                 const int t = t0 + u;
                 if (t < nsteps) {
                     __syncthreads();                 // previous step's fragment reads are done
-                    *(uint4*)&As[lrow * LDK + kc] = ring_a[u];
+#pragma unroll
+                    for (int q = 0; q < ST_A_PER; ++q)
+                        *(uint4*)&As[(lrow + 32 * q) * LDK + kc] = ring_a[u][q];
 #pragma unroll
                     for (int i = 0; i < ST_B_PER; ++i)
                         *(uint4*)&Bs[(lrow + 32 * i) * LDK + kc] = ring_b[u][i];
@@ -596,11 +612,11 @@ __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(S
                     if (t + ST_RING + 1 < nsteps) load(kt0 + t + ST_RING + 1, ring_a[u], ring_b[u]);
 #pragma unroll
                     for (int kk = 0; kk < 4; ++kk) {
-                        const bf16x8 af = *(const bf16x8*)&As[frag_row * LDK + frag_col + kk * 8];
-                        const bf16x8 b0 = *(const bf16x8*)&Bs[(wave * 64 + frag_row) * LDK + frag_col + kk * 8];
-                        const bf16x8 b1 = *(const bf16x8*)&Bs[(wave * 64 + 32 + frag_row) * LDK + frag_col + kk * 8];
-                        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, b0, acc0, 0, 0, 0);
-                        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, b1, acc1, 0, 0, 0);
+                        const bf16x8 a0 = *(const bf16x8*)&As[frag_row * LDK + frag_col + kk * 8];
+                        const bf16x8 a1 = *(const bf16x8*)&As[(32 + frag_row) * LDK + frag_col + kk * 8];
+                        const bf16x8 bw = *(const bf16x8*)&Bs[(wave * 32 + frag_row) * LDK + frag_col + kk * 8];
+                        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, bw, acc0, 0, 0, 0);
+                        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, bw, acc1, 0, 0, 0);
                     }
                 }
             }
@@ -608,15 +624,20 @@ __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(S
 
         // partial store: element r of a 32x32 tile is row 8*(r/4) + 4*(lane/32) + r%4, col lane%32
         float* prow = args.part + ((int64_t)c * P.n_small + P.qbase[g] + m * ST_M) * args.N + n0 +
-                      wave * 64;
-        const int cw = bvalid - wave * 64;           // valid columns of this wave
+                      wave * 32;
+        const int cw = bvalid - wave * 32;           // valid columns of this wave
+        if (frag_row < cw) {
+            // one per-lane base pointer; the row offset of each r is uniform
+            const int lr = (lane >> 5) * 4;
+            float* pl = prow + (int64_t)lr * args.N + frag_row;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-            if (row >= rows_valid) continue;
-            float* pr = prow + (int64_t)row * args.N;
-            if (frag_row < cw) pr[frag_row] = acc0[r];
-            if (32 + frag_row < cw) pr[32 + frag_row] = acc1[r];
+            for (int r = 0; r < 16; ++r) {
+                const int rc = (r >> 2) * 8 + (r & 3);
+                const int64_t o = (int64_t)__builtin_amdgcn_readfirstlane(rc * args.N);
+                const int64_t o32 = (int64_t)__builtin_amdgcn_readfirstlane((rc + 32) * args.N);
+                if (rc + lr < rows_valid) pl[o] = acc0[r];
+                if (rc + 32 + lr < rows_valid) pl[o32] = acc1[r];
+            }
         }
         __syncthreads();                             // s_item and LDS reuse by the next item
     }
