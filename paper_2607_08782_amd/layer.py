@@ -3,9 +3,13 @@
 `LayerShare` owns the device buffers of one share (allocated once with
 torch) and enqueues, on the current stream:
     moe_route_topk -> moe_expert_histogram -> moe_permute
-    -> moe_grouped_ffn (routed experts) [-> moe_grouped_ffn (shared experts)]
-    -> moe_combine
-with no host synchronisation in between.  The expert placement can be
+    -> moe_grouped_ffn (routed experts) -> moe_combine
+with no host synchronisation in between.  The shared experts' FFN
+(moe_grouped_ffn over every token), which does not depend on the routing,
+runs on a second stream forked from the current one and joined back before
+the combine, so it overlaps the short routing and packaging launches; the
+fork and join are stream events, so a graph capture of `run` holds both
+branches.  The expert placement can be
 swapped between batches (`set_placement`) by re-pointing the weight table;
 nothing is reallocated.
 """
@@ -44,7 +48,7 @@ class LayerShare:
                  placement: np.ndarray, dev: int, w13: Sequence[torch.Tensor],
                  w2: Sequence[torch.Tensor], shared=(), renorm: bool = True,
                  coact: bool = False, want_logits: bool = True, cap_rows: Optional[int] = None,
-                 gather_in_ffn: bool = False):
+                 gather_in_ffn: bool = False, overlap_shared: bool = True):
         self.device = X.device
         self.X = X
         self.Wr = Wr
@@ -98,6 +102,12 @@ class LayerShare:
         else:
             self.shared_weights = None
             self.y_shared = None
+        # second stream for the shared experts (default priority), fork/join events
+        self._side = None
+        if self.shared_weights is not None and overlap_shared:
+            self._side = torch.cuda.Stream(device=dv)
+            self._fork = torch.cuda.Event(enable_timing=False)
+            self._join = torch.cuda.Event(enable_timing=False)
         self.y = torch.empty((max(T, 1), d), dtype=dt, device=dv)
 
     def set_placement(self, placement: np.ndarray, w13: Sequence[torch.Tensor],
@@ -126,8 +136,20 @@ class LayerShare:
                                logits=self.logits, want_logits=self.logits is not None,
                                topk_idx=self.topk_idx, topk_gate=self.topk_gate, ws=self.ws_route)
 
+    def _shared_ffn(self, stream=None):
+        moe.moe_grouped_ffn(self.X, self.shared_offsets, self.shared_weights, cap_rows=self.T,
+                            y_perm=self.y_shared, ws=self.ws_shared, stream=stream)
+
     def run(self, logits_in: Optional[torch.Tensor] = None) -> torch.Tensor:
-        """Enqueue the whole share on the current stream; returns y [T, d]."""
+        """Enqueue the whole share after the current stream's earlier work; returns y
+        [T, d], complete on the current stream (the shared experts' branch, if
+        any, is joined back before the combine)."""
+        main = torch.cuda.current_stream(self.device)
+        if self._side is not None:
+            self._fork.record(main)
+            self._side.wait_event(self._fork)
+            self._shared_ffn(self._side)
+            self._join.record(self._side)
         self.route(logits_in)
         moe.moe_expert_histogram(self.topk_idx, self.E, counts=self.counts, coact=self.coact)
         moe.moe_permute(self.X, self.topk_idx, self.topk_gate, self.counts, self.placement,
@@ -141,9 +163,10 @@ class LayerShare:
             else:
                 moe.moe_grouped_ffn(self.perm["x_perm"], self.perm["group_offsets"], self.weights,
                                     cap_rows=self.cap_rows, y_perm=self.y_perm, ws=self.ws_ffn)
-        if self.shared_weights is not None:
-            moe.moe_grouped_ffn(self.X, self.shared_offsets, self.shared_weights, cap_rows=self.T,
-                                y_perm=self.y_shared, ws=self.ws_shared)
+        if self._side is not None:
+            main.wait_event(self._join)
+        elif self.shared_weights is not None:
+            self._shared_ffn()
         moe.moe_combine(self.y_perm, self.perm["token_row"], self.topk_gate, self.y_shared,
                         T=self.T, d=self.d, y=self.y)
         return self.y

@@ -492,6 +492,32 @@ def test_mid_sized_groups_split_k_in_the_tiled_kernel():
             close(np32(share.y_perm[go[s]:go[s + 1]]), ref, OUT_TOL["bf16"], "group %d" % s)
 
 
+def test_shared_expert_branch_on_a_second_stream_is_bitwise_equal():
+    """The shared experts' FFN forked onto a second stream (the default) gives the
+    same bits as the whole share on one stream, eagerly and over graph replays with
+    new hidden states copied in between."""
+    cfg = synth.custom_config(d=256, E=16, k=4, f=256, shared_f=(128, 64), G=2, replicas=1,
+                              zipf=1.1)
+    T = 300
+    inp = synth.make_layer(cfg, T, seed=4, device="cuda")
+    one, two = (LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                           shared=inp.shared, overlap_shared=ov) for ov in (False, True))
+    one.run()
+    two.run()
+    torch.cuda.synchronize()
+    assert torch.equal(one.y[:T], two.y[:T])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        two.run()
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    for _ in range(3):
+        inp.X.copy_(torch.randn(inp.X.shape, device="cuda", generator=gen).to(inp.X.dtype))
+        g.replay()
+        one.run()
+        torch.cuda.synchronize()
+        assert torch.equal(one.y[:T], two.y[:T])
+
+
 def test_graph_replays_match_eager_runs():
     """The whole share captured once in a HIP graph: every replay (with new hidden
     states copied in eagerly between replays) must equal an eager run bit for bit."""
