@@ -6,7 +6,9 @@
 //   phase 1  scores for its tokens x all E experts into LDS
 //            bf16: MFMA 16x16x32, K split over 16 waves, fixed-order reduction
 //            (long batches over more than 32 experts use the tiled kernel of
-//            score.hip instead);
+//            score.hip instead; short batches over more than 16 experts the
+//            per-wave partial tiles of route_wave_kernel, summed in a second
+//            launch with the top-k);
 //            f32:  plain FMA loops;  logits-in: read in place from global memory
 //   phase 2  bias added, scores written back coalesced (if requested)
 //   phase 3  a group of lanes per token: k rounds of a group-wide maximum, gates.
@@ -17,7 +19,7 @@ namespace moe {
 namespace {
 
 constexpr int ROUTE_THREADS = TOPK_THREADS;
-constexpr int ROUTE_MAX_SPLIT = 16;    // K chunks of the split score kernel
+constexpr int ROUTE_MAX_SPLIT = 32;    // K chunks of the split score kernel
 
 enum RouteMode { MODE_F32 = 1, MODE_LOGITS_IN = 2, MODE_PARTIALS = 3 };
 
@@ -190,11 +192,69 @@ __global__ __launch_bounds__(RB_THREADS) void route_bf16_kernel(
     }
 }
 
+// Partial bf16 gate scores of short batches (few token blocks, e.g. decode):
+// one wave per (16 tokens, 16 experts, K chunk) on MFMA 16x16x32, every operand
+// load of the chunk issued before the first product, and the 16 x 16 fp32
+// partial tile stored straight from the accumulators into part[chunk][t][e]
+// (no LDS, no barriers), so a batch of a few dozen tokens still spreads over
+// about a thousand waves.  Rows past the batch or past E, and K past d, read as
+// zero through the buffer descriptors.
+constexpr int RW_WAVES = 4;            // waves per workgroup
+constexpr int RW_STEPS = 8;            // 32-wide K steps of loads issued at once
+
+__global__ __launch_bounds__(RW_WAVES * 64) void route_wave_kernel(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ W, int64_t T, int d, int E, int S,
+    float* __restrict__ part) {
+    const int lane = threadIdx.x & 63;
+    const int64_t wid = (int64_t)blockIdx.x * RW_WAVES + (threadIdx.x >> 6);
+    const int ET = (E + 15) / 16;
+    const int64_t TT = (T + 15) / 16;
+    if (wid >= TT * ET * S) return;                  // the whole wave leaves together
+    const int c = (int)(wid % S);
+    const int64_t tile = wid / S;
+    const int e0 = (int)(tile % ET) * 16;
+    const int64_t t0 = (tile / ET) * 16;
+    const int nt = (int)((T - t0) < 16 ? (T - t0) : 16);
+    const int ne = E - e0 < 16 ? E - e0 : 16;
+    const int row = lane & 15, kq = (lane >> 4) * 8;
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(X + t0 * d), (short)0, nt * d * 2, RB_RSRC_WORD3);
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(W + (int64_t)e0 * d), (short)0, ne * d * 2, RB_RSRC_WORD3);
+    const int nsteps_all = (d + 31) / 32;
+    const int sbeg = (int)((int64_t)c * nsteps_all / S);
+    const int send = (int)((int64_t)(c + 1) * nsteps_all / S);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = sbeg; s0 < send; s0 += RW_STEPS) {
+        uint4 a[RW_STEPS], b[RW_STEPS];
+#pragma unroll
+        for (int i = 0; i < RW_STEPS; ++i) {
+            const int k = (s0 + i) * 32 + kq;
+            const int off = (s0 + i < send && k < d) ? (row * d + k) * 2 : RB_OOB;
+            a[i] = rb_load16(xr, off);
+            b[i] = rb_load16(wr, off);
+        }
+#pragma unroll
+        for (int i = 0; i < RW_STEPS; ++i)
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[i]),
+                                                          __builtin_bit_cast(bf16x8, b[i]), acc,
+                                                          0, 0, 0);
+    }
+    // accumulator element i of lane L: token 4 (L / 16) + i, expert L % 16
+    if (row < ne) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = 4 * (lane >> 4) + i;
+            if (r < nt) part[((int64_t)c * T + t0 + r) * E + e0 + row] = acc[i];
+        }
+    }
+}
+
 // fp32 scores (plain FMA loops), scores handed in (MOE_LOGITS_IN) or K-chunk
 // partial scores to be summed: `tpb` tokens per workgroup of 256 threads, one
 // token per top-k lane group (topk_tokens_per_block), so short batches still
-// spread over many workgroups.
-template <int MODE, int KM, int C>
+// spread over many workgroups.  MAXS: the most chunks a partial-sum launch adds.
+template <int MODE, int KM, int C, int MAXS = ROUTE_MAX_SPLIT>
 __global__ __launch_bounds__(ROUTE_THREADS) void route_simple_kernel(
     const float* __restrict__ X, const float* __restrict__ W, const float* __restrict__ bias,
     int64_t T, int d, int E, int k, int renorm, float* __restrict__ logits,
@@ -220,17 +280,17 @@ __global__ __launch_bounds__(ROUTE_THREADS) void route_simple_kernel(
     } else if (MODE == MODE_PARTIALS) {
         // K chunks summed in chunk order.  Chunks are split only for short
         // batches, where a thread has few elements: per element, all
-        // ROUTE_MAX_SPLIT chunk loads go out together (unconditionally, clamped to
+        // MAXS chunk loads go out together (unconditionally, clamped to
         // chunk S - 1 and masked by a 0/1 factor), one round trip per element
         const float* pb = part + t0 * E;
         const int64_t cs = T * E;                     // chunk stride
         for (int c = tid; c < nt * E; c += ROUTE_THREADS) {
-            float x[ROUTE_MAX_SPLIT];
+            float x[MAXS];
 #pragma unroll
-            for (int ch = 0; ch < ROUTE_MAX_SPLIT; ++ch) x[ch] = pb[(ch < S ? ch : S - 1) * cs + c];
+            for (int ch = 0; ch < MAXS; ++ch) x[ch] = pb[(ch < S ? ch : S - 1) * cs + c];
             float sum = 0.f;
 #pragma unroll
-            for (int ch = 0; ch < ROUTE_MAX_SPLIT; ++ch) sum = fmaf(x[ch], ch < S ? 1.0f : 0.0f, sum);
+            for (int ch = 0; ch < MAXS; ++ch) sum = fmaf(x[ch], ch < S ? 1.0f : 0.0f, sum);
             const int r = c / E, e = c - r * E;
             Sm[r * ldS + e] = sum;
         }
@@ -289,6 +349,11 @@ int launch_kmv(const void* x, int dtype, const void* w, const float* bias, int64
                                    nullptr, tpb);
                 return launch_status();
             }
+        } else if (S > 1 && E > 16) {
+            const int64_t waves = ceil_div(T, 16) * ((E + 15) / 16) * S;
+            hipLaunchKernelGGL(route_wave_kernel, dim3((unsigned)ceil_div(waves, RW_WAVES)),
+                               dim3(RW_WAVES * 64), 0, s, (const bf16_t*)x, (const bf16_t*)w, T, d,
+                               E, S, part);
         } else {
 #define MOE_RB_LAUNCH(RT, NTM)                                                                  \
     do {                                                                                        \
@@ -307,10 +372,17 @@ int launch_kmv(const void* x, int dtype, const void* w, const float* bias, int64
         if (S > 1) {
             const int tpb = simple_tokens_per_block(T, E);
             const size_t lds2 = (size_t)tpb * (E_pad + 1) * sizeof(float);
-            hipLaunchKernelGGL((route_simple_kernel<MODE_PARTIALS, KM, C>),
-                               dim3((unsigned)ceil_div(T, tpb)), dim3(ROUTE_THREADS), lds2, s,
-                               nullptr, nullptr, bias, T, d, E, k, renorm, logits, idx, gate, S,
-                               (const float*)part, tpb);
+            // as few clamped chunk loads per score as the split needs
+            if (S <= 16)
+                hipLaunchKernelGGL((route_simple_kernel<MODE_PARTIALS, KM, C, 16>),
+                                   dim3((unsigned)ceil_div(T, tpb)), dim3(ROUTE_THREADS), lds2, s,
+                                   nullptr, nullptr, bias, T, d, E, k, renorm, logits, idx, gate, S,
+                                   (const float*)part, tpb);
+            else
+                hipLaunchKernelGGL((route_simple_kernel<MODE_PARTIALS, KM, C, ROUTE_MAX_SPLIT>),
+                                   dim3((unsigned)ceil_div(T, tpb)), dim3(ROUTE_THREADS), lds2, s,
+                                   nullptr, nullptr, bias, T, d, E, k, renorm, logits, idx, gate, S,
+                                   (const float*)part, tpb);
         }
         return launch_status();
     }
@@ -330,15 +402,27 @@ int launch_kmv(const void* x, int dtype, const void* w, const float* bias, int64
 
 }  // namespace
 
-// K chunks of the bf16 score kernel: enough workgroups to spread the hidden
-// states over the chip when there are few token blocks (decode batches).
+// K chunks of the bf16 scores when there are few token blocks (decode batches);
+// 1 = the one-launch kernel with the top-k in its epilogue.  More than 16
+// experts: route_wave_kernel gets about 1024 waves of 16 x 16 tiles with at
+// least two K steps each (Qwen3-30B-A3B-shaped decode routing 16.8 -> 11.9 us).
+// At most 16 experts a 16-wide tile is mostly padding, and the block kernel
+// splits K into chunks of at least four steps instead (its LDS reduction sums
+// the waves of a block).
 int route_split(int64_t T, int d, int E) {
     const int64_t blocks = ceil_div(T, route_rows(E));
     if (blocks <= 0 || blocks >= 128) return 1;
     const int nsteps = (d + 31) / 32;
-    int64_t S = ceil_div(256, blocks);
-    if (S > ROUTE_MAX_SPLIT) S = ROUTE_MAX_SPLIT;
-    if (S > nsteps / 4) S = nsteps / 4;
+    int64_t S;
+    if (E <= 16) {
+        S = ceil_div(256, blocks);
+        if (S > 16) S = 16;
+        if (S > nsteps / 4) S = nsteps / 4;
+    } else {
+        S = ceil_div(1024, ceil_div(T, 16) * ((E + 15) / 16));
+        if (S > ROUTE_MAX_SPLIT) S = ROUTE_MAX_SPLIT;
+        if (S > nsteps / 2) S = nsteps / 2;
+    }
     return S < 1 ? 1 : (int)S;
 }
 

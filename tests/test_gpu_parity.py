@@ -97,6 +97,31 @@ def test_tiled_gate_scores_and_topk_every_element(T, d, E, k):
     close(np32(case.share.topk_gate), og, GATE_TOL, "gates")
 
 
+SHORT = [  # (T, d, E, k): short batches over > 16 experts take the per-wave split-K score tiles
+    (1, 2048, 128, 8),        # one token: 8 expert tiles x 32 K chunks
+    (17, 512, 20, 3),         # ragged token and expert tiles (2 x 2), 8 chunks of 2 steps
+    (64, 2048, 128, 8),       # Qwen3-30B-A3B-shaped decode
+    (256, 2048, 64, 6),       # DeepSeek-V2-Lite-shaped decode, 16 chunks
+    (100, 1024, 160, 4),      # E > 128 (ten expert tiles)
+    (33, 160, 48, 2),         # K of five 32-wide steps in two uneven chunks
+]
+
+
+@pytest.mark.parametrize("T,d,E,k", SHORT)
+def test_short_batch_gate_scores_and_topk_every_element(T, d, E, k):
+    """Scores of short batches as per-wave 16 x 16 partial tiles over K chunks, summed
+    in chunk order by the top-k launch: every logit against the oracle's, and the
+    selection and gates exact given those logits."""
+    cfg = synth.custom_config(d=d, E=E, k=k, f=64, G=1)
+    say("[short]", T, d, E, k)
+    case = Case(cfg, T)
+    check_logits(case)
+    gl = np32(case.share.logits)
+    oidx, og = oracle.topk(gl, k)
+    np.testing.assert_array_equal(case.share.topk_idx.cpu().numpy(), oidx)
+    close(np32(case.share.topk_gate), og, GATE_TOL, "gates")
+
+
 def test_drift_sequence_swaps_placement_without_reallocating():
     """Qwen1.5-MoE-shaped share: popularity re-ranked every 4 batches, placement
     swapped between batches by re-pointing the weight table."""
