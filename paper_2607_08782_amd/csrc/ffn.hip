@@ -427,7 +427,9 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 // short call, see small_limits): weight streaming with split-K.  Here the weights dominate the traffic (each weight byte is used by
 // a handful of rows), so the aim is to read every weight byte once, from all
 // CUs at once.  Work item = (group, 128 weight rows, K chunk, 64 rows); one
-// workgroup per item, four per CU, fp32 partial sums per K chunk.  HBM reads
+// workgroup per item, three per CU with three K steps of loads in flight
+// each (four per CU cannot hold that ring without spilling), fp32 partial sums
+// per K chunk.  HBM reads
 // reach their rate only with many independent streams in flight (a read-only
 // probe over 448 MiB: 4.3-5.1 TB/s with 224-448 workgroups, 5.4-5.7 TB/s with
 // 896 or more), so the item is narrow in weight rows and covers a whole
@@ -440,8 +442,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 constexpr int ST_M = 64;                 // rows per item (two 32-row MFMA tiles per wave)
 constexpr int ST_N = 128;                // weight rows per item (32 per wave)
 constexpr int ST_THREADS = 256;
-constexpr int ST_WG_PER_CU = 4;
-constexpr int ST_RING = 1;               // K steps of loads in flight beyond the one in LDS
+constexpr int ST_WG_PER_CU = 3;
+constexpr int ST_RING = 2;               // K steps of loads in flight beyond the one in LDS
 constexpr int ST_A_PER = ST_M * 64 / 8 / ST_THREADS;   // 16-byte loads per thread per K step
 constexpr int ST_B_PER = ST_N * 64 / 8 / ST_THREADS;
 constexpr int SPLIT_MAX = 32;
