@@ -85,7 +85,8 @@ const char* moe_status_string(int status);
  *           batches split the gate GEMM over K across workgroups and keep the
  *           per-chunk fp32 partial scores here; they are summed in chunk order.)
  * Requires 1 <= E <= MOE_MAX_E, 1 <= k <= min(E, MOE_MAX_K), T >= 0,
- * d >= 1 and, for MOE_BF16, d % 8 == 0.  Logits must be finite.
+ * d >= 1 and, for MOE_BF16, d % 8 == 0 and E * d * 2 < 2^31 (else
+ * MOE_ERR_SHAPE).  Logits must be finite.
  * Scores are deterministic: the same inputs give bitwise the same outputs.
  */
 int moe_route_topk(const void* x, int dtype, const void* w_router, const float* bias,
@@ -214,7 +215,8 @@ int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int
  *   y[t] = sum_{r ascending, token_row[t][r] >= 0} topk_gate[t][r] * y_perm[token_row[t][r]]
  *          + y_shared[t]
  *
- * y_perm    device [rows][d] of `dtype`;  token_row device [T][k] int32
+ * y_perm    device [rows][d] of `dtype`, required when T > 0 (it may hold
+ *           no rows that any token uses);  token_row device [T][k] int32
  * topk_gate device [T][k] float;  y_shared device [T][d] of `dtype`, nullable
  * y         device [T][d] of `dtype` output (fp32 accumulation, then stored).
  * Tokens with no local assignment get y_shared[t] (or 0).

@@ -46,6 +46,8 @@ int moe_route_topk(const void* x, int dtype, const void* w_router, const float* 
         if (T > 0 && (!x || !w_router)) return MOE_ERR_ARG;
         if (dtype == MOE_BF16) {
             if (d % 8) return MOE_ERR_SHAPE;
+            // the router matrix is addressed through one 32-bit buffer descriptor
+            if ((int64_t)E * d * 2 > 0x7fffffffLL) return MOE_ERR_SHAPE;
             if (!aligned16(x) || !aligned16(w_router)) return MOE_ERR_ARG;
         }
     }
@@ -171,7 +173,7 @@ int moe_combine(const void* y_perm, int dtype, const int32_t* token_row, const f
                 const void* y_shared, int64_t T, int d, int k, void* y, void* stream) {
     if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
     if (T < 0 || d < 1 || k < 1 || k > MOE_MAX_K) return MOE_ERR_ARG;
-    if (T > 0 && (!token_row || !topk_gate || !y)) return MOE_ERR_ARG;
+    if (T > 0 && (!token_row || !topk_gate || !y || !y_perm)) return MOE_ERR_ARG;
     const int V = dtype == MOE_BF16 ? 8 : 4;
     if (d % V == 0 && (!aligned16(y) || (y_perm && !aligned16(y_perm)) ||
                        (y_shared && !aligned16(y_shared))))

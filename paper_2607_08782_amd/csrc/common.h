@@ -4,7 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include <atomic>
+#include <mutex>
 
 #include "moe.h"
 
@@ -68,20 +68,22 @@ inline int launch_status() {
 
 // Raise kernel F's dynamic-LDS limit to `bytes` on the current device.  The
 // setting persists, so each device is configured once per size increase and
-// later launches skip the runtime call.
+// later launches skip the runtime call.  The check, the runtime call and the
+// record of the granted size happen under one lock per kernel, so concurrent
+// callers never leave a smaller limit set than the one recorded.
 template <auto F>
 inline int allow_dynamic_lds(size_t bytes) {
     constexpr int kMaxDevices = 64;
-    static std::atomic<int> granted[kMaxDevices];
+    static std::mutex lock;
+    static int granted[kMaxDevices];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return MOE_ERR_DEVICE;
-    int cur = granted[dev].load(std::memory_order_acquire);
-    if (cur >= (int)bytes) return MOE_OK;
+    std::lock_guard<std::mutex> guard(lock);
+    if (granted[dev] >= (int)bytes) return MOE_OK;
     if (hipFuncSetAttribute((const void*)F, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)bytes) != hipSuccess)
         return MOE_ERR_DEVICE;
-    while (cur < (int)bytes && !granted[dev].compare_exchange_weak(cur, (int)bytes)) {
-    }
+    granted[dev] = (int)bytes;
     return MOE_OK;
 }
 

@@ -74,6 +74,7 @@ def test_route_topk_validation(lib):
     assert call(d=12) == moe.MOE_ERR_SHAPE          # bf16 rows must be 16-byte multiples
     assert call(x=ctypes.c_void_p(0x1002)) == moe.MOE_ERR_ARG   # misaligned bf16 rows
     assert call(flags=3, lg=None) == moe.MOE_ERR_ARG             # logits-in without logits
+    assert call(E=256, k=2, d=4194304) == moe.MOE_ERR_SHAPE      # router past 32-bit offsets
     need = lib.moe_route_topk_ws_bytes(1, 4, 4096, 8, 1)
     assert need > 0                                              # a 4-token batch splits K
     assert call(d=4096) == moe.MOE_ERR_SHAPE                     # ... and needs its workspace
@@ -163,6 +164,7 @@ def test_combine_validation(lib):
     assert f(FAKE, 1, FAKE, FAKE, None, 4, 0, 2, FAKE, None) == moe.MOE_ERR_ARG
     assert f(FAKE, 1, None, FAKE, None, 4, 64, 2, FAKE, None) == moe.MOE_ERR_ARG
     assert f(FAKE, 1, FAKE, FAKE, None, 4, 64, 2, ctypes.c_void_p(0x1008), None) == moe.MOE_ERR_ARG
+    assert f(None, 1, FAKE, FAKE, None, 4, 64, 2, FAKE, None) == moe.MOE_ERR_ARG   # y_perm
 
 
 def test_workspace_sizes(lib):

@@ -2,8 +2,15 @@
 
 Small shapes check every output element and span several tiles with ragged
 tails; the model-shaped layer shares check routing bit for bit at full size
-and the FFN / combined outputs on sampled rows and tokens.
+and the FFN / combined outputs on every row of each group's first and last
+256-row tile (all rows at decode sizes) and the tokens those rows serve.
+Every shape is checked twice: with the oracle's logits handed in, and on the
+path the benchmark times (the library's own gate scores and top-k), where the
+oracle's routing of the HIP logits must equal the HIP routing bit for bit.
 """
+import json
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -13,7 +20,7 @@ from paper_2607_08782_amd import moe, synth
 from paper_2607_08782_amd.layer import LayerShare
 
 from parity import (Case, check_end_to_end_routing, check_ffn_and_combine, check_logits,
-                    check_routing, close, np32, say, GATE_TOL, OUT_TOL)
+                    check_routing, check_timed_path, close, np32, say, GATE_TOL, OUT_TOL)
 
 pytestmark = pytest.mark.gpu
 
@@ -54,6 +61,8 @@ def test_small_shapes_every_element(name):
     idx, gate, pm = check_routing(case, ref_logits)
     check_ffn_and_combine(case, idx, gate, pm, sample=None)
     check_end_to_end_routing(case, ref_logits)
+    idx, gate, pm = check_timed_path(case)
+    check_ffn_and_combine(case, idx, gate, pm, sample=None)
 
 
 FULL = [
@@ -73,9 +82,60 @@ def test_model_shaped_layer_share(name, regime):
     ref_logits, _ = check_logits(case)
     idx, gate, pm = check_routing(case, ref_logits)
     say("  rows here", pm["rows"], "send_counts", pm["send_counts"].tolist())
-    worst = check_ffn_and_combine(case, idx, gate, pm, sample=6)
+    worst = check_ffn_and_combine(case, idx, gate, pm, sample="tiles")
     differ = check_end_to_end_routing(case, ref_logits)
     say("  worst rel err %.2e, top-k sets differing from the oracle: %.4f" % (worst, differ))
+
+
+TIMED = [("tiny_fp32", "batch")] + FULL
+
+
+@pytest.mark.parametrize("name,regime", TIMED)
+def test_timed_path_matches_the_oracle(name, regime):
+    """The share exactly as the benchmark runs it (share.run(): the library's own
+    gate scores and top-k, e.g. the fused score + top-k epilogue at the Mixtral and
+    DeepSeek-V2-Lite prefill shapes, the fp32 path of the tiny layer, the tiled
+    score kernel at Qwen3 prefill, split-K partials at decode sizes).  The oracle
+    routes and packages the HIP logits: indices, counts, co-activation and every
+    row map bit for bit, gates within 1e-5; then its expert FFN and combine on
+    that routing give y_perm and y within the output tolerance (every row of each
+    group's first and last 256-row tile, all rows at decode sizes)."""
+    cfg = synth.CONFIGS[name]
+    T = cfg.T(regime)
+    say("[timed]", name, regime, "T=%d" % T)
+    case = Case(cfg, T)
+    idx, gate, pm = check_timed_path(case)
+    worst = check_ffn_and_combine(case, idx, gate, pm, sample=None if T <= 256 else "tiles")
+    say("  rows here", pm["rows"], "worst rel err %.2e" % worst)
+
+
+def test_replica_split_hand_example():
+    """The hand-evaluated replica split (tests/golden): expert 0 on three GPUs takes
+    blocks of 2, 2 and 3 of its 7 tokens, expert 2 on two GPUs 2 and 2; every GPU's
+    group offsets, row maps and send counts as written out by hand."""
+    fx = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                     "replica_split_hand_example.json")))
+    E, G, k = fx["E"], fx["G"], fx["k"]
+    idx = np.array(fx["idx"], np.int32)
+    T = idx.shape[0]
+    L = np.zeros((T, E), np.float32)
+    for t in range(T):
+        L[t, idx[t, 0]] = 2.0
+        L[t, idx[t, 1]] = 1.0
+    cfg = synth.custom_config(d=64, E=E, k=k, f=64, G=G)
+    pl = np.array(fx["placement"], np.uint8)
+    for g in fx["per_gpu"]:
+        inp, share = _share(cfg, T, placement=pl, dev=g["dev"])
+        share.run(logits_in=torch.from_numpy(L).cuda())
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(share.topk_idx.cpu().numpy(), idx)
+        N = g["group_offsets"][-1]
+        np.testing.assert_array_equal(share.perm["group_offsets"].cpu().numpy(), g["group_offsets"])
+        np.testing.assert_array_equal(share.perm["row_token"][:N].cpu().numpy(), g["row_token"])
+        np.testing.assert_array_equal(share.perm["token_row"].cpu().numpy(), g["token_row"])
+        np.testing.assert_array_equal(share.perm["send_counts"].cpu().numpy(), fx["send_counts"])
+        np.testing.assert_array_equal(np32(share.perm["x_perm"][:N]),
+                                      np32(inp.X)[g["row_token"]])
 
 
 TILED = [  # (T, d, E, k): batches of >= 192 64-token tiles over > 32 experts take the tiled kernel
@@ -140,7 +200,9 @@ def test_drift_sequence_swaps_placement_without_reallocating():
         case.X, case.Wr, case.b, case._w = np32(inp.X), np32(inp.Wr), np32(inp.bias), {}
         ref_logits, _ = check_logits(case)
         idx, gate, pm = check_routing(case, ref_logits)
-        check_ffn_and_combine(case, idx, gate, pm, sample=3, seed=b)
+        check_ffn_and_combine(case, idx, gate, pm, sample="tiles", seed=b, max_tokens=128)
+        idx, gate, pm = check_timed_path(case)
+        check_ffn_and_combine(case, idx, gate, pm, sample="tiles", seed=b, max_tokens=128)
     assert share.perm["x_perm"].data_ptr() == ptr_before
 
 

@@ -193,6 +193,28 @@ def test_permute_partition_over_gpus_with_replicas(seed):
                 assert host_tokens[(e, a)][-1] < host_tokens[(e, b)][0]
 
 
+def test_replica_split_hand_example():
+    """The replica load split, evaluated by hand (tests/golden): an expert with
+    c_e tokens on n_e hosts gives its q-th host (ascending GPU id) the ranks
+    [floor(q c_e / n_e), floor((q+1) c_e / n_e)).  At c_e = 7 over 3 hosts the
+    blocks are 2, 2, 3 rows; a ceiling rule (3, 2, 2) fails here."""
+    import json
+    import os
+    fx = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                     "replica_split_hand_example.json")))
+    idx = np.array(fx["idx"], np.int32)
+    pl = np.array(fx["placement"], np.uint8)
+    gate = np.ones(idx.shape)
+    X = np.arange(idx.shape[0] * 2, dtype=np.float32).reshape(-1, 2)
+    for g in fx["per_gpu"]:
+        pm = oracle.permute(X, idx, gate, fx["E"], pl, g["dev"])
+        np.testing.assert_array_equal(pm["group_offsets"], g["group_offsets"])
+        np.testing.assert_array_equal(pm["row_token"], g["row_token"])
+        np.testing.assert_array_equal(pm["token_row"], g["token_row"])
+        np.testing.assert_array_equal(pm["send_counts"], fx["send_counts"])
+        np.testing.assert_array_equal(pm["x_perm"], X[g["row_token"]])
+
+
 def test_send_counts_are_eq1_load_and_eq3_volume():
     r = _rng(6)
     T, E, k, G, d = 400, 20, 2, 4, 8
