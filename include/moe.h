@@ -59,6 +59,7 @@ extern "C" {
 #define MOE_MAX_K      16    /* experts per token */
 #define MOE_MAX_G      64    /* GPUs in the placement map */
 #define MOE_MAX_GROUPS 128   /* local expert groups per moe_grouped_ffn call */
+#define MOE_PERMUTE_NOALLOC_MAX_WS (4 << 20)   /* scratch bytes of moe_permute_noalloc */
 
 /* Human-readable name of a status code (static string). */
 const char* moe_status_string(int status);
@@ -153,6 +154,30 @@ int moe_permute(const void* x, int dtype, const int32_t* topk_idx, const float* 
                 void* x_perm, int64_t cap_rows, int32_t* group_offsets,
                 int32_t* row_token, float* row_gate, int32_t* token_row,
                 int32_t* send_counts, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * moe_permute_noalloc -- moe_permute without a workspace argument, for callers
+ * that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc).  It packages the tokens
+ * exactly as moe_permute does (same outputs, bit for bit) and keeps the
+ * per-block counts it needs in a scratch array of this library: one copy per
+ * GPU, MOE_PERMUTE_NOALLOC_MAX_WS (4 MiB) bytes, held until the process ends.
+ * The call allocates nothing; its first call on a GPU looks up that GPU's
+ * copy of the array.
+ *
+ * Arguments, outputs and errors as for moe_permute, without ws / ws_bytes.
+ * Returns MOE_ERR_SHAPE when moe_permute_ws_bytes(T, k, E) exceeds
+ * MOE_PERMUTE_NOALLOC_MAX_WS (more than about 524 000 tokens at 128 local
+ * slots), and MOE_ERR_DEVICE if the scratch cannot be located on the current
+ * device.  The scratch keeps the last call's contents; every call on one GPU
+ * shares it, so calls that overlap in time on one GPU (different streams, or
+ * different threads) race and must be serialised by the caller.
+ */
+int moe_permute_noalloc(const void* x, int dtype, const int32_t* topk_idx,
+                        const float* topk_gate, const int32_t* counts, int64_t T, int d, int k,
+                        int E, const uint8_t* placement, int G, int dev, int c_max, void* x_perm,
+                        int64_t cap_rows, int32_t* group_offsets, int32_t* row_token,
+                        float* row_gate, int32_t* token_row, int32_t* send_counts, void* stream);
 
 /* Workspace bytes moe_grouped_ffn needs. */
 size_t moe_grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_groups);

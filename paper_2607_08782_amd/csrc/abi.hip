@@ -69,11 +69,17 @@ size_t moe_permute_ws_bytes(int64_t T, int k, int E) {
     return permute_ws_bytes(T, k, E);
 }
 
-int moe_permute(const void* x, int dtype, const int32_t* topk_idx, const float* topk_gate,
-                const int32_t* counts, int64_t T, int d, int k, int E, const uint8_t* placement,
-                int G, int dev, int c_max, void* x_perm, int64_t cap_rows,
-                int32_t* group_offsets, int32_t* row_token, float* row_gate, int32_t* token_row,
-                int32_t* send_counts, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation shared by moe_permute and moe_permute_noalloc, and the slot /
+// host tables built from the placement map.
+int permute_check(const void* x, int dtype, const int32_t* topk_idx, const float* topk_gate,
+                  const int32_t* counts, int64_t T, int d, int k, int E,
+                  const uint8_t* placement, int G, int dev, int c_max, void* x_perm,
+                  int64_t cap_rows, int32_t* group_offsets, int32_t* row_token,
+                  float* row_gate, int32_t* token_row, PermuteTables& tab, int& n_local) {
     if (T < 0 || d < 0 || E < 1 || E > MOE_MAX_E || k < 1 || k > MOE_MAX_K || k > E)
         return MOE_ERR_ARG;
     if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
@@ -82,10 +88,9 @@ int moe_permute(const void* x, int dtype, const int32_t* topk_idx, const float* 
     if (G < 1 || G > MOE_MAX_G || dev < 0 || dev >= G) return MOE_ERR_PLACEMENT;
     if (T > 0 && (!topk_idx || !topk_gate || !token_row)) return MOE_ERR_ARG;
 
-    PermuteTables tab;
     memset(&tab, 0, sizeof(tab));
     for (int e = 0; e < MOE_MAX_E; ++e) tab.slot_of[e] = -1;
-    int n_local = 0;
+    n_local = 0;
     for (int e = 0; e < E; ++e) {
         uint64_t h = 0;
         for (int j = 0; j < G; ++j)
@@ -103,9 +108,46 @@ int moe_permute(const void* x, int dtype, const int32_t* topk_idx, const float* 
     const int64_t need_rows = T * (int64_t)(k < n_local ? k : n_local);
     if (cap_rows < need_rows) return MOE_ERR_SHAPE;
     if (dtype == MOE_BF16 && d % 8) return MOE_ERR_SHAPE;
-    if (!ws || ws_bytes < permute_ws_bytes(T, k, E) || ((uintptr_t)ws & 255u)) return MOE_ERR_SHAPE;
     if (need_rows > 0 && (!row_token || !row_gate || (d > 0 && (!x || !x_perm))))
         return MOE_ERR_ARG;
+    return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_permute(const void* x, int dtype, const int32_t* topk_idx, const float* topk_gate,
+                const int32_t* counts, int64_t T, int d, int k, int E, const uint8_t* placement,
+                int G, int dev, int c_max, void* x_perm, int64_t cap_rows,
+                int32_t* group_offsets, int32_t* row_token, float* row_gate, int32_t* token_row,
+                int32_t* send_counts, void* ws, size_t ws_bytes, void* stream) {
+    PermuteTables tab;
+    int n_local = 0;
+    const int st = permute_check(x, dtype, topk_idx, topk_gate, counts, T, d, k, E, placement, G,
+                                 dev, c_max, x_perm, cap_rows, group_offsets, row_token, row_gate,
+                                 token_row, tab, n_local);
+    if (st != MOE_OK) return st;
+    if (!ws || ws_bytes < permute_ws_bytes(T, k, E) || ((uintptr_t)ws & 255u)) return MOE_ERR_SHAPE;
+    return launch_permute(x, dtype, topk_idx, topk_gate, counts, T, d, k, E, tab, n_local, G, dev,
+                          x_perm, cap_rows, group_offsets, row_token, row_gate, token_row,
+                          send_counts, ws, (hipStream_t)stream);
+}
+
+int moe_permute_noalloc(const void* x, int dtype, const int32_t* topk_idx,
+                        const float* topk_gate, const int32_t* counts, int64_t T, int d, int k,
+                        int E, const uint8_t* placement, int G, int dev, int c_max, void* x_perm,
+                        int64_t cap_rows, int32_t* group_offsets, int32_t* row_token,
+                        float* row_gate, int32_t* token_row, int32_t* send_counts, void* stream) {
+    PermuteTables tab;
+    int n_local = 0;
+    const int st = permute_check(x, dtype, topk_idx, topk_gate, counts, T, d, k, E, placement, G,
+                                 dev, c_max, x_perm, cap_rows, group_offsets, row_token, row_gate,
+                                 token_row, tab, n_local);
+    if (st != MOE_OK) return st;
+    if (permute_ws_bytes(T, k, E) > (size_t)MOE_PERMUTE_NOALLOC_MAX_WS) return MOE_ERR_SHAPE;
+    void* ws = nullptr;
+    if (permute_scratch(&ws) != MOE_OK) return MOE_ERR_DEVICE;
     return launch_permute(x, dtype, topk_idx, topk_gate, counts, T, d, k, E, tab, n_local, G, dev,
                           x_perm, cap_rows, group_offsets, row_token, row_gate, token_row,
                           send_counts, ws, (hipStream_t)stream);

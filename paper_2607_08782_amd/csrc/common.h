@@ -127,6 +127,9 @@ int launch_permute(const void* x, int dtype, const int32_t* idx, const float* ga
                    int32_t* group_offsets, int32_t* row_token, float* row_gate, int32_t* token_row,
                    int32_t* send_counts, void* ws, hipStream_t s);
 size_t permute_ws_bytes(int64_t T, int k, int E);
+// Device address of the library's own permute scratch on the current device
+// (MOE_PERMUTE_NOALLOC_MAX_WS bytes, 256-byte aligned).
+int permute_scratch(void** ptr);
 
 // a_rows (nullable): row p of the first product's input is row a_rows[p] of
 // x_perm, which then holds a_total rows (the token rows; no packaged copy).

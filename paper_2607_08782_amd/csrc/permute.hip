@@ -341,7 +341,34 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(
     }
 }
 
+// Scratch of moe_permute_noalloc: the per-block slot counts and replica
+// offsets that moe_permute keeps in the caller's workspace, held instead in a
+// device array of this library (one copy per GPU, kept until the process
+// ends).  Every byte the kernels read is written earlier in the same call, so
+// nothing needs clearing; calls that overlap on one GPU race on it.
+static __device__ __align__(256) unsigned char scratch[MOE_PERMUTE_NOALLOC_MAX_WS];
+
 }  // namespace
+
+// Device address of `scratch` on the current device.  The array's name in host
+// code is a host-side stand-in, not a device address, so the address is looked
+// up once per device, with that device current, and kept.
+int permute_scratch(void** ptr) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex lock;
+    static void* addr[kMaxDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return MOE_ERR_DEVICE;
+    std::lock_guard<std::mutex> guard(lock);
+    if (addr[dev] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+            return MOE_ERR_DEVICE;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return MOE_OK;
+}
 
 size_t permute_ws_bytes(int64_t T, int k, int E) {
     (void)k;

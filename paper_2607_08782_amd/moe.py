@@ -23,10 +23,11 @@ MOE_F32, MOE_BF16 = 0, 1
 MOE_OK, MOE_ERR_ARG, MOE_ERR_PLACEMENT, MOE_ERR_SHAPE, MOE_ERR_DEVICE = 0, 1, 2, 3, 4
 MOE_RENORM, MOE_LOGITS_IN = 1, 2
 MOE_MAX_E, MOE_MAX_K, MOE_MAX_G, MOE_MAX_GROUPS = 256, 16, 64, 128
+MOE_PERMUTE_NOALLOC_MAX_WS = 4 << 20
 
 EXPORTS = ("moe_status_string", "moe_route_topk", "moe_route_topk_ws_bytes",
            "moe_expert_histogram", "moe_permute_ws_bytes",
-           "moe_permute", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_grouped_ffn_rows",
+           "moe_permute", "moe_permute_noalloc", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_grouped_ffn_rows",
            "moe_combine",
            "moe_quantize_e4m3", "moe_route_topk_e4m3")
 
@@ -60,6 +61,9 @@ def load_library(path: str = LIB_PATH):
     lib.moe_permute_ws_bytes.restype = S
     lib.moe_permute.argtypes = [P, I, P, P, P, L, I, I, I, P, I, I, I, P, L, P, P, P, P, P, P, S, P]
     lib.moe_permute.restype = I
+    lib.moe_permute_noalloc.argtypes = [P, I, P, P, P, L, I, I, I, P, I, I, I, P, L, P, P, P, P, P,
+                                        P]
+    lib.moe_permute_noalloc.restype = I
     lib.moe_grouped_ffn_ws_bytes.argtypes = [I, L, I, I, I]
     lib.moe_grouped_ffn_ws_bytes.restype = S
     lib.moe_grouped_ffn.argtypes = [P, I, P, I, P, P, I, I, L, P, P, S, P]
@@ -244,11 +248,12 @@ def moe_permute(x: torch.Tensor, topk_idx: torch.Tensor, topk_gate: torch.Tensor
                 counts: torch.Tensor, placement: np.ndarray, dev: int, *, E: int,
                 cap_rows: Optional[int] = None, c_max: int = 0, out: Optional[dict] = None,
                 ws: Optional[torch.Tensor] = None, want_send_counts: bool = True,
-                copy_rows: bool = True, stream=None):
+                copy_rows: bool = True, stream=None, noalloc: bool = False):
     """Package tokens for the experts on GPU `dev`.  Returns a dict of device tensors
     (x_perm, group_offsets, row_token, row_gate, token_row, send_counts).  With
     copy_rows=False only the row maps are produced (x_perm is not written; for
-    moe_grouped_ffn_rows)."""
+    moe_grouped_ffn_rows).  noalloc=True calls moe_permute_noalloc (no workspace:
+    the library's own scratch); outputs missing from `out` are still allocated here."""
     lib = load_library()
     T, d = x.shape
     k = topk_idx.shape[1]
@@ -269,21 +274,22 @@ def moe_permute(x: torch.Tensor, topk_idx: torch.Tensor, topk_gate: torch.Tensor
         o["row_gate"] = _empty((max(cap_rows, 1),), torch.float32, device)
         o["token_row"] = _empty((T, k), torch.int32, device)
         o["send_counts"] = _empty((G,), torch.int32, device) if want_send_counts else None
+    args = [_dev(x, "x") if copy_rows else None, _dtype_code(x),
+            _dev(topk_idx, "topk_idx", torch.int32), _dev(topk_gate, "topk_gate", torch.float32),
+            _dev(counts, "counts", torch.int32), T, d if copy_rows else 0, k, E,
+            placement.ctypes.data_as(ctypes.c_void_p), G, dev, c_max,
+            _dev(o["x_perm"], "x_perm", x.dtype) if copy_rows else None, cap_rows,
+            _dev(o["group_offsets"], "group_offsets", torch.int32),
+            _dev(o["row_token"], "row_token", torch.int32),
+            _dev(o["row_gate"], "row_gate", torch.float32),
+            _dev(o["token_row"], "token_row", torch.int32),
+            _dev(o.get("send_counts"), "send_counts", torch.int32)]
+    if noalloc:
+        _check("moe_permute_noalloc", lib.moe_permute_noalloc(*args, _stream(stream)))
+        return o
     if ws is None:
         ws = workspace(moe_permute_ws_bytes(T, k, E), device)
-    st = lib.moe_permute(_dev(x, "x") if copy_rows else None, _dtype_code(x),
-                         _dev(topk_idx, "topk_idx", torch.int32),
-                         _dev(topk_gate, "topk_gate", torch.float32),
-                         _dev(counts, "counts", torch.int32), T, d if copy_rows else 0, k, E,
-                         placement.ctypes.data_as(ctypes.c_void_p), G, dev, c_max,
-                         _dev(o["x_perm"], "x_perm", x.dtype) if copy_rows else None, cap_rows,
-                         _dev(o["group_offsets"], "group_offsets", torch.int32),
-                         _dev(o["row_token"], "row_token", torch.int32),
-                         _dev(o["row_gate"], "row_gate", torch.float32),
-                         _dev(o["token_row"], "token_row", torch.int32),
-                         _dev(o.get("send_counts"), "send_counts", torch.int32),
-                         _dev(ws, "ws"), ws.numel(), _stream(stream))
-    _check("moe_permute", st)
+    _check("moe_permute", lib.moe_permute(*args, _dev(ws, "ws"), ws.numel(), _stream(stream)))
     return o
 
 

@@ -121,6 +121,35 @@ def test_permute_placement_and_capacity_validation(lib):
     assert _permute(lib, big) == moe.MOE_ERR_PLACEMENT                # G > MOE_MAX_G
 
 
+def test_permute_noalloc_validation(lib):
+    """The same checks as moe_permute (nothing touches HIP before they pass), and
+    batches whose block counts exceed the library's scratch are refused."""
+    f = lib.moe_permute_noalloc
+
+    def call(pl, T=10, d=64, k=2, E=4, dev=0, cap=None, c_max=0):
+        pl = np.ascontiguousarray(pl, np.uint8)
+        G = pl.shape[1]
+        if cap is None:
+            cap = T * k
+        return f(FAKE, 1, FAKE, FAKE, FAKE, T, d, k, E, pl.ctypes.data_as(ctypes.c_void_p), G,
+                 dev, c_max, FAKE, cap, FAKE, FAKE, FAKE, FAKE, None, None)
+    pl = np.array([[1, 0], [0, 1], [1, 1], [0, 0]])
+    assert call(pl) == moe.MOE_ERR_PLACEMENT                       # expert 3 has no host
+    pl[3, 1] = 1
+    assert call(pl, dev=2) == moe.MOE_ERR_PLACEMENT
+    assert call(pl, c_max=1) == moe.MOE_ERR_PLACEMENT
+    assert call(pl, cap=19) == moe.MOE_ERR_SHAPE
+    assert call(pl, d=12) == moe.MOE_ERR_SHAPE
+    assert call(pl, k=0) == moe.MOE_ERR_ARG
+    E = 128
+    pl = np.ones((E, 1), np.uint8)
+    T = 600000                                                      # 9375 blocks x 128 slots
+    assert lib.moe_permute_ws_bytes(T, 8, E) > moe.MOE_PERMUTE_NOALLOC_MAX_WS
+    assert call(pl, T=T, k=8, E=E) == moe.MOE_ERR_SHAPE
+    T = 500000
+    assert lib.moe_permute_ws_bytes(T, 8, E) <= moe.MOE_PERMUTE_NOALLOC_MAX_WS
+
+
 def test_grouped_ffn_validation(lib):
     f = lib.moe_grouped_ffn
     arr = (ctypes.c_void_p * 2)(0x1000, 0x2000)
