@@ -50,6 +50,10 @@ extern "C" {
 #define MOE_ERR_SHAPE     3   /* unsupported d or f, cap_rows or workspace too small */
 #define MOE_ERR_DEVICE    4   /* a HIP launch failed */
 
+/* products of moe_grouped_ffn_products */
+#define MOE_FFN_GATE_UP 1   /* h = SiLU(W1 x) * (W3 x), kept in the workspace */
+#define MOE_FFN_DOWN    2   /* y = W2 h, from the workspace */
+
 /* flags of moe_route_topk */
 #define MOE_RENORM    1   /* gates = softmax over the k selected logits (else: full softmax, restricted) */
 #define MOE_LOGITS_IN 2   /* skip the gate GEMM: `logits` is an input holding T*E scores */
@@ -210,6 +214,27 @@ size_t moe_grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n
 int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets, int n_groups,
                     const void* const* w13, const void* const* w2, int d, int f,
                     int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * moe_grouped_ffn_products -- moe_grouped_ffn run one product at a time
+ * (Sec. II-A: the expert FFN is the two products of the SwiGLU block), for
+ * callers that schedule or time the two separately.  products is a mask:
+ *   MOE_FFN_GATE_UP  h = SiLU(W1_s x_perm[p]) * (W3_s x_perm[p]) for every row,
+ *                    kept in ws (with the call's group plan)
+ *   MOE_FFN_DOWN     y_perm[p] = W2_s h[p], reading h and the plan from ws
+ * MOE_FFN_GATE_UP | MOE_FFN_DOWN is exactly moe_grouped_ffn.  A
+ * MOE_FFN_DOWN call must follow a MOE_FFN_GATE_UP call on the same stream
+ * with the same ws, group_offsets (unchanged contents), n_groups, d, f and
+ * cap_rows; ws must not be used in between.  The two calls in sequence give
+ * bitwise the outputs of moe_grouped_ffn.  x_perm and w13 are read only with
+ * MOE_FFN_GATE_UP (may be NULL otherwise), y_perm and w2 only with
+ * MOE_FFN_DOWN.  Other arguments, requirements and errors as for
+ * moe_grouped_ffn; products outside {1, 2, 3} give MOE_ERR_ARG.
+ */
+int moe_grouped_ffn_products(const void* x_perm, int dtype, const int32_t* group_offsets,
+                             int n_groups, const void* const* w13, const void* const* w2, int d,
+                             int f, int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes,
+                             int products, void* stream);
 
 /*
  * moe_grouped_ffn_rows -- moe_grouped_ffn whose first product reads row p of

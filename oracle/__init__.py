@@ -71,6 +71,8 @@ def _load():
         lib.orc_combine.restype = None
         lib.orc_num_threads.argtypes = []
         lib.orc_num_threads.restype = i32
+        lib.orc_set_num_threads.argtypes = [i32]
+        lib.orc_set_num_threads.restype = None
         _lib = lib
         return lib
 
@@ -86,6 +88,11 @@ def _p(a):
 
 def num_threads() -> int:
     return int(_load().orc_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's OpenMP loops from now on (n >= 1)."""
+    _load().orc_set_num_threads(int(n))
 
 
 def router_logits(X, Wr, bias=None) -> np.ndarray:

@@ -267,6 +267,17 @@ void orc_combine(const double* y_perm, const int64_t* token_row, const double* g
     }
 }
 
+/* Threads of the oracle's OpenMP loops from now on (the benchmark times it at
+ * one thread as well as at all host threads). */
+void orc_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Number of OpenMP threads the oracle runs with (reported by the benchmark). */
 int orc_num_threads(void)
 {

@@ -158,29 +158,62 @@ size_t moe_grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n
     return grouped_ffn_ws_bytes(dtype, cap_rows, d, f, n_groups);
 }
 
-int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets, int n_groups,
-                    const void* const* w13, const void* const* w2, int d, int f, int64_t cap_rows,
-                    void* y_perm, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation of a grouped FFN call that runs `products` (a mask of
+// MOE_FFN_GATE_UP and MOE_FFN_DOWN): the operands of the products it runs.
+int ffn_check(const void* x_perm, int dtype, const int32_t* group_offsets, int n_groups,
+              const void* const* w13, const void* const* w2, int d, int f, int64_t cap_rows,
+              const void* y_perm, const void* ws, size_t ws_bytes, int products) {
     if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
+    if (products < 1 || products > (MOE_FFN_GATE_UP | MOE_FFN_DOWN)) return MOE_ERR_ARG;
+    const bool up = products & MOE_FFN_GATE_UP, down = products & MOE_FFN_DOWN;
     if (n_groups < 1 || n_groups > MOE_MAX_GROUPS || d < 1 || f < 1 || cap_rows < 0)
         return MOE_ERR_ARG;
     if (cap_rows > 0x7fffffff) return MOE_ERR_ARG;
-    if (!group_offsets || !w13 || !w2) return MOE_ERR_ARG;
+    if (!group_offsets || (up && !w13) || (down && !w2)) return MOE_ERR_ARG;
     for (int s = 0; s < n_groups; ++s)
-        if (!w13[s] || !w2[s]) return MOE_ERR_ARG;
-    if (cap_rows > 0 && (!x_perm || !y_perm)) return MOE_ERR_ARG;
+        if ((up && !w13[s]) || (down && !w2[s])) return MOE_ERR_ARG;
+    if (cap_rows > 0 && ((up && !x_perm) || (down && !y_perm))) return MOE_ERR_ARG;
     if (dtype == MOE_BF16) {
         if (d % 64 || f % 64) return MOE_ERR_SHAPE;
-        if (!aligned16(x_perm) || !aligned16(y_perm)) return MOE_ERR_ARG;
+        if ((x_perm && !aligned16(x_perm)) || (y_perm && !aligned16(y_perm))) return MOE_ERR_ARG;
         for (int s = 0; s < n_groups; ++s)
-            if (!aligned16(w13[s]) || !aligned16(w2[s])) return MOE_ERR_ARG;
+            if ((up && !aligned16(w13[s])) || (down && !aligned16(w2[s]))) return MOE_ERR_ARG;
     }
     if (cap_rows > 0 &&
         (!ws || ws_bytes < grouped_ffn_ws_bytes(dtype, cap_rows, d, f, n_groups) ||
          ((uintptr_t)ws & 255u)))
         return MOE_ERR_SHAPE;
+    return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets, int n_groups,
+                    const void* const* w13, const void* const* w2, int d, int f, int64_t cap_rows,
+                    void* y_perm, void* ws, size_t ws_bytes, void* stream) {
+    const int both = MOE_FFN_GATE_UP | MOE_FFN_DOWN;
+    const int st = ffn_check(x_perm, dtype, group_offsets, n_groups, w13, w2, d, f, cap_rows,
+                             y_perm, ws, ws_bytes, both);
+    if (st != MOE_OK) return st;
     return launch_grouped_ffn(x_perm, dtype, group_offsets, n_groups, w13, w2, d, f, cap_rows,
                               y_perm, ws, (hipStream_t)stream);
+}
+
+int moe_grouped_ffn_products(const void* x_perm, int dtype, const int32_t* group_offsets,
+                             int n_groups, const void* const* w13, const void* const* w2, int d,
+                             int f, int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes,
+                             int products, void* stream) {
+    const int st = ffn_check(x_perm, dtype, group_offsets, n_groups, w13, w2, d, f, cap_rows,
+                             y_perm, ws, ws_bytes, products);
+    if (st != MOE_OK) return st;
+    return launch_grouped_ffn(x_perm, dtype, group_offsets, n_groups, w13, w2, d, f, cap_rows,
+                              y_perm, ws, (hipStream_t)stream, nullptr, 0, products);
 }
 
 int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int dtype,

@@ -136,7 +136,8 @@ int permute_scratch(void** ptr);
 int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, int n_groups,
                        const void* const* w13, const void* const* w2, int d, int f,
                        int64_t cap_rows, void* y_perm, void* ws, hipStream_t s,
-                       const int32_t* a_rows = nullptr, int64_t a_total = 0);
+                       const int32_t* a_rows = nullptr, int64_t a_total = 0,
+                       int products = MOE_FFN_GATE_UP | MOE_FFN_DOWN);
 size_t grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_groups);
 
 int launch_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* gate,

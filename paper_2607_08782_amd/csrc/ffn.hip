@@ -863,8 +863,9 @@ size_t grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_gro
 int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, int n_groups,
                        const void* const* w13, const void* const* w2, int d, int f,
                        int64_t cap_rows, void* y_perm, void* ws, hipStream_t s,
-                       const int32_t* a_rows, int64_t a_total) {
+                       const int32_t* a_rows, int64_t a_total, int products) {
     if (cap_rows == 0) return MOE_OK;
+    const bool up = (products & MOE_FFN_GATE_UP) != 0, down = (products & MOE_FFN_DOWN) != 0;
     if (dtype == MOE_F32) {
         PtrTable t13, t2;
         for (int i = 0; i < MOE_MAX_GROUPS; ++i) {
@@ -875,10 +876,12 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
         int64_t b1 = ceil_div(cap_rows * (int64_t)f, 256), b2 = ceil_div(cap_rows * (int64_t)d, 256);
         if (b1 > 4096) b1 = 4096;
         if (b2 > 4096) b2 = 4096;
-        hipLaunchKernelGGL(ffn1_f32_kernel, dim3((unsigned)b1), dim3(256), 0, s,
-                           (const float*)x_perm, a_rows, offsets, n_groups, t13, d, f, h);
-        hipLaunchKernelGGL(ffn2_f32_kernel, dim3((unsigned)b2), dim3(256), 0, s, (const float*)h,
-                           offsets, n_groups, t2, d, f, (float*)y_perm);
+        if (up)
+            hipLaunchKernelGGL(ffn1_f32_kernel, dim3((unsigned)b1), dim3(256), 0, s,
+                               (const float*)x_perm, a_rows, offsets, n_groups, t13, d, f, h);
+        if (down)
+            hipLaunchKernelGGL(ffn2_f32_kernel, dim3((unsigned)b2), dim3(256), 0, s,
+                               (const float*)h, offsets, n_groups, t2, d, f, (float*)y_perm);
         return launch_status();
     }
     const int cus = num_cus();
@@ -903,7 +906,8 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
 
     // gate/up product: big groups on the tiled kernel, small groups streamed
     GemmArgs a1;
-    for (int i = 0; i < MOE_MAX_GROUPS; ++i) a1.w[i] = i < n_groups ? (const bf16_t*)w13[i] : nullptr;
+    for (int i = 0; i < MOE_MAX_GROUPS; ++i)
+        a1.w[i] = up && i < n_groups ? (const bf16_t*)w13[i] : nullptr;
     a1.offsets = offsets;
     a1.a = (const bf16_t*)x_perm;
     a1.out = h;
@@ -921,9 +925,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a1.split_units = grid < TILE_SPLIT_UNITS ? grid : TILE_SPLIT_UNITS;
     a1.a_rows = a_rows;
     a1.a_total = (int)a_total;
-    if (a_rows)
+    if (up && a_rows)
         hipLaunchKernelGGL((grouped_gemm_kernel<true, true>), dim3(grid), dim3(GEMM_THREADS), 0, s, a1);
-    else
+    else if (up)
         hipLaunchKernelGGL((grouped_gemm_kernel<true, false>), dim3(grid), dim3(GEMM_THREADS), 0, s, a1);
     StreamArgs s1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) s1.w[i] = a1.w[i];
@@ -941,11 +945,14 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s1.a_total = (int)a_total;
     s1.limits = a1.limits;
     s1.product = 0;
-    if (a_rows)
-        hipLaunchKernelGGL(stream_gemm_kernel<true>, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
-    else
-        hipLaunchKernelGGL(stream_gemm_kernel<false>, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
-    hipLaunchKernelGGL(split_reduce_kernel<true>, dim3(rgrid), dim3(ST_THREADS), 0, s, s1, a1);
+    if (up) {
+        if (a_rows)
+            hipLaunchKernelGGL(stream_gemm_kernel<true>, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
+        else
+            hipLaunchKernelGGL(stream_gemm_kernel<false>, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
+        hipLaunchKernelGGL(split_reduce_kernel<true>, dim3(rgrid), dim3(ST_THREADS), 0, s, s1, a1);
+    }
+    if (!down) return launch_status();
 
     // down product
     GemmArgs a2 = a1;

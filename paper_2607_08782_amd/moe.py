@@ -22,12 +22,13 @@ LIB_PATH = os.path.join(_HERE, "libmoe.so")
 MOE_F32, MOE_BF16 = 0, 1
 MOE_OK, MOE_ERR_ARG, MOE_ERR_PLACEMENT, MOE_ERR_SHAPE, MOE_ERR_DEVICE = 0, 1, 2, 3, 4
 MOE_RENORM, MOE_LOGITS_IN = 1, 2
+MOE_FFN_GATE_UP, MOE_FFN_DOWN = 1, 2
 MOE_MAX_E, MOE_MAX_K, MOE_MAX_G, MOE_MAX_GROUPS = 256, 16, 64, 128
 MOE_PERMUTE_NOALLOC_MAX_WS = 4 << 20
 
 EXPORTS = ("moe_status_string", "moe_route_topk", "moe_route_topk_ws_bytes",
            "moe_expert_histogram", "moe_permute_ws_bytes",
-           "moe_permute", "moe_permute_noalloc", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_grouped_ffn_rows",
+           "moe_permute", "moe_permute_noalloc", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_grouped_ffn_products", "moe_grouped_ffn_rows",
            "moe_combine",
            "moe_quantize_e4m3", "moe_route_topk_e4m3")
 
@@ -68,6 +69,8 @@ def load_library(path: str = LIB_PATH):
     lib.moe_grouped_ffn_ws_bytes.restype = S
     lib.moe_grouped_ffn.argtypes = [P, I, P, I, P, P, I, I, L, P, P, S, P]
     lib.moe_grouped_ffn.restype = I
+    lib.moe_grouped_ffn_products.argtypes = [P, I, P, I, P, P, I, I, L, P, P, S, I, P]
+    lib.moe_grouped_ffn_products.restype = I
     lib.moe_grouped_ffn_rows.argtypes = [P, L, P, I, P, I, P, P, I, I, L, P, P, S, P]
     lib.moe_grouped_ffn_rows.restype = I
     lib.moe_combine.argtypes = [P, I, P, P, P, L, I, I, P, P]
@@ -319,8 +322,11 @@ class WeightTable:
 
 def moe_grouped_ffn(x_perm: torch.Tensor, group_offsets: torch.Tensor, weights: WeightTable, *,
                     cap_rows: Optional[int] = None, y_perm: Optional[torch.Tensor] = None,
-                    ws: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """SwiGLU FFN of every group.  Returns y_perm [cap_rows, d]."""
+                    ws: Optional[torch.Tensor] = None, stream=None,
+                    products: int = 3) -> torch.Tensor:
+    """SwiGLU FFN of every group.  Returns y_perm [cap_rows, d].  products=1 or 2
+    runs one product (moe_grouped_ffn_products: gate/up into the workspace, or down
+    from it; the down call must follow a gate/up call with the same ws)."""
     lib = load_library()
     if cap_rows is None:
         cap_rows = x_perm.shape[0]
@@ -334,13 +340,15 @@ def moe_grouped_ffn(x_perm: torch.Tensor, group_offsets: torch.Tensor, weights: 
         y_perm = _empty((max(cap_rows, 1), d), x_perm.dtype, x_perm.device)
     if ws is None:
         ws = workspace(moe_grouped_ffn_ws_bytes(dtype, cap_rows, d, f, len(weights)), x_perm.device)
-    st = lib.moe_grouped_ffn(_dev(x_perm, "x_perm"), dtype,
-                             _dev(group_offsets, "group_offsets", torch.int32), len(weights),
-                             ctypes.cast(weights.p13, ctypes.c_void_p),
-                             ctypes.cast(weights.p2, ctypes.c_void_p), d, f, cap_rows,
-                             _dev(y_perm, "y_perm", x_perm.dtype), _dev(ws, "ws"), ws.numel(),
-                             _stream(stream))
-    _check("moe_grouped_ffn", st)
+    args = [_dev(x_perm, "x_perm"), dtype, _dev(group_offsets, "group_offsets", torch.int32),
+            len(weights), ctypes.cast(weights.p13, ctypes.c_void_p),
+            ctypes.cast(weights.p2, ctypes.c_void_p), d, f, cap_rows,
+            _dev(y_perm, "y_perm", x_perm.dtype), _dev(ws, "ws"), ws.numel()]
+    if products == MOE_FFN_GATE_UP | MOE_FFN_DOWN:
+        _check("moe_grouped_ffn", lib.moe_grouped_ffn(*args, _stream(stream)))
+    else:
+        _check("moe_grouped_ffn_products",
+               lib.moe_grouped_ffn_products(*args, products, _stream(stream)))
     return y_perm
 
 

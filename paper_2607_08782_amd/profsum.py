@@ -1,24 +1,24 @@
-"""Summaries of rocprofv3 runs of the default benchmark (`bench.py`).
+"""Summaries of rocprofv3 runs of `bench.py`, one workload per run.
 
-The benchmark (run with --no-gather-variant) runs the prefill batch first (27
-dispatches of every kernel: 3 warm-up + 10 eager timed + 3 + 10 graph replays
-+ 1 final run), then the decode batch; the 28th gate-score dispatch marks the
-boundary.
+Each profiled run measures one layer shape and regime alone
+(`bench.py --workload NAME:REGIME --decode '' --shapes none --no-cpu-baseline
+--no-gather-variant`), so every dispatch in its trace belongs to that workload.
 
-    # per-call HBM traffic of moe_grouped_ffn, read by bench.py for `roofline.traffic`
-    python -m paper_2607_08782_amd.profsum traffic <FETCH_SIZE csv> <WRITE_SIZE csv> \
-        --fetch-factor 2 --write-factor 1 --out profiles/ffn_traffic.json
-    # per-kernel table: durations (kernel trace) and calibrated read / write MiB
-    python -m paper_2607_08782_amd.profsum table <kernel-trace csv> <FETCH_SIZE csv> \
-        <WRITE_SIZE csv> --fetch-factor 2 --write-factor 1
+    # per-kernel launch counts and mean durations (kernel trace)
+    python -m paper_2607_08782_amd.profsum kernels <kernel_trace.csv>
+    # HBM traffic per launch of each FFN kernel and per moe_grouped_ffn call, from a
+    # FETCH_SIZE run and a WRITE_SIZE run of the same command with --calibrate-copy;
+    # merged into profiles/ffn_traffic.json under the workload's name
+    python -m paper_2607_08782_amd.profsum traffic NAME:REGIME <FETCH csv> <WRITE csv>
     # tiled-GEMM utilisation from a GRBM_GUI_ACTIVE / SQ_* counter run
     python -m paper_2607_08782_amd.profsum mfma <counter csv>
-    # where one step's time goes, per kernel, for kernel traces of
-    # `bench.py --workload NAME:REGIME --decode '' --no-gather-variant` runs
-    python -m paper_2607_08782_amd.profsum breakdown LABEL=<kernel-trace csv> ...
+    # where one step's time goes, per kernel (kernel traces of --steps S runs)
+    python -m paper_2607_08782_amd.profsum breakdown --steps N LABEL=<kernel_trace.csv> ...
 
-The factors scale the counters to bytes: a plain copy kernel of known size
-(`bench.py --calibrate-copy`) reads back FETCH_SIZE x factor = its bytes.
+Counter calibration: the run's first kernel is a plain elementwise copy of
+--calibrate-copy MiB (torch.neg: reads and writes that many bytes); the factors
+that turn its FETCH_SIZE and WRITE_SIZE (KiB) into those bytes scale every other
+dispatch's counters.
 """
 from __future__ import annotations
 
@@ -29,9 +29,13 @@ import hashlib
 import json
 import os
 
-PREFILL_DISPATCHES = 27
-FFN_KERNELS = ("grouped_gemm_kernel", "stream_gemm_kernel", "split_reduce_kernel")   # prefixes
 FFN_SOURCE = "paper_2607_08782_amd/csrc/ffn.hip"
+# kernels of one moe_grouped_ffn call and their launches per call (the streaming
+# kernel runs once per product)
+FFN_CALL = {"grouped_gemm_kernel<true, false>": 1, "grouped_gemm_kernel<false, false>": 1,
+            "stream_gemm_kernel<false>": 2, "split_reduce_kernel<true>": 1,
+            "split_reduce_kernel<false>": 1}
+COPY_KERNEL = "neg_kernel"     # torch.neg's elementwise kernel carries this in its name
 
 
 def short(name: str) -> str:
@@ -42,8 +46,30 @@ def _mean(v):
     return sum(v) / len(v) if v else 0.0
 
 
-def counter_by_regime(path: str, counter: str, factor: float):
-    """Per kernel: lists of counter x factor (KiB -> bytes) for prefill and decode dispatches."""
+def _med(v):
+    return sorted(v)[len(v) // 2] if v else 0.0
+
+
+def kernels(trace_csv):
+    """Markdown table: each library kernel's launches and mean / median duration."""
+    with open(trace_csv) as fh:
+        rows = sorted(csv.DictReader(fh), key=lambda r: int(r["Start_Timestamp"]))
+    per, order = collections.defaultdict(list), []
+    for r in rows:
+        k = short(r["Kernel_Name"])
+        if k.startswith("at::") or "rocclr" in k:
+            continue
+        if k not in order:
+            order.append(k)
+        per[k].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0)
+    lines = ["| kernel | launches | mean us | median us |", "|---|---|---|---|"]
+    for k in order:
+        lines.append("| `%s` | %d | %.1f | %.1f |" % (k, len(per[k]), _mean(per[k]), _med(per[k])))
+    return "\n".join(lines) + "\n"
+
+
+def _counter(path, counter):
+    """Per dispatch: (kernel name, counter value in KiB summed over its instances)."""
     per, names = collections.defaultdict(float), {}
     with open(path) as fh:
         for r in csv.DictReader(fh):
@@ -51,73 +77,52 @@ def counter_by_regime(path: str, counter: str, factor: float):
                 continue
             d = int(r["Dispatch_Id"])
             per[d] += float(r["Counter_Value"])
-            names[d] = short(r["Kernel_Name"])
-    gate = sorted(d for d in per if names[d].startswith("route_bf16_kernel"))
-    boundary = gate[PREFILL_DISPATCHES] if len(gate) > PREFILL_DISPATCHES else max(per) + 1
-    pre, dec = collections.defaultdict(list), collections.defaultdict(list)
-    for d in sorted(per):
-        if names[d].startswith("at::") or "rocclr" in names[d]:
-            continue
-        (pre if d < boundary else dec)[names[d]].append(per[d] * factor * 1024.0)
-    return pre, dec
+            names[d] = r["Kernel_Name"]
+    return [(names[d], per[d]) for d in sorted(per)]
 
 
-def traffic(fetch_csv, write_csv, ff, wf, out, repo="."):
-    """Bytes per moe_grouped_ffn call: the streaming kernel runs twice per call."""
+def traffic(workload, fetch_csv, write_csv, copy_mib, out, repo="."):
+    """Bytes per launch of each FFN kernel and per call, scaled by the copy kernel."""
+    res = {}
+    if os.path.exists(out):
+        with open(out) as fh:
+            res = json.load(fh)
     with open(os.path.join(repo, FFN_SOURCE), "rb") as fh:
         sha = hashlib.sha256(fh.read()).hexdigest()
-    res = {"kernel_source": FFN_SOURCE, "source_sha256": sha,
-           "unit": "bytes per moe_grouped_ffn call (calibrated FETCH_SIZE + WRITE_SIZE)",
-           "fetch_factor": ff, "write_factor": wf}
-    for key, path, counter, fac in (("read", fetch_csv, "FETCH_SIZE", ff),
-                                    ("write", write_csv, "WRITE_SIZE", wf)):
-        pre, dec = counter_by_regime(path, counter, fac)
-        for regime, per in (("prefill", pre), ("decode", dec)):
-            tot = sum(_mean(v) * (2 if k.startswith("stream") else 1)
-                      for k, v in per.items() if k.startswith(FFN_KERNELS))
-            res.setdefault("mixtral_8x7b:" + regime, {})[key] = tot
-    res["commands"] = [
-        "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pf -o pf -- python -u "
-        "bench.py --steps 10 --warmup 3 --no-cpu-baseline --no-gather-variant --calibrate-copy 1024",
-        "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pw -o pw -- python -u "
-        "bench.py --steps 10 --warmup 3 --no-cpu-baseline --no-gather-variant --calibrate-copy 1024"]
+    if res.get("source_sha256") != sha:
+        res = {"workloads": {}}
+    res.update({"kernel_source": FFN_SOURCE, "source_sha256": sha,
+                "unit": "bytes per launch (FETCH_SIZE and WRITE_SIZE, KiB, times the factor a "
+                        "plain copy of known size gives)"})
+    w = {"kernels": {}, "call": {"read": 0.0, "write": 0.0}}
+    copy_bytes = copy_mib * float(1 << 20)
+    for key, path, counter in (("read", fetch_csv, "FETCH_SIZE"), ("write", write_csv, "WRITE_SIZE")):
+        disp = _counter(path, counter)
+        copies = [v for n, v in disp if COPY_KERNEL in n]
+        if not copies:
+            raise SystemExit("no calibration copy kernel in %s (run with --calibrate-copy)" % path)
+        factor = copy_bytes / (copies[-1] * 1024.0)
+        w[key + "_factor"] = factor
+        per = collections.defaultdict(list)
+        for n, v in disp:
+            per[short(n)].append(v * 1024.0 * factor)
+        for k, v in per.items():
+            if k in FFN_CALL:
+                w["kernels"].setdefault(k, {})[key] = _mean(v)
+                w["call"][key] += _mean(v) * FFN_CALL[k]
+    res["workloads"][workload] = w
+    res.setdefault("commands", {})[workload] = [
+        "rocprofv3 --pmc %s --output-format csv -d gpurun_out/pmc -o %s -- python -u bench.py "
+        "--workload %s --decode '' --shapes none --steps 10 --warmup 3 --no-cpu-baseline "
+        "--no-gather-variant --calibrate-copy %d" % (c, c.lower(), workload, copy_mib)
+        for c in ("FETCH_SIZE", "WRITE_SIZE")]
     with open(out, "w") as fh:
         json.dump(res, fh, indent=1)
     return res
 
 
-def table(trace_csv, fetch_csv, write_csv, ff, wf):
-    """Markdown table: per kernel, calls and mean duration per regime, mean MiB per dispatch."""
-    with open(trace_csv) as fh:
-        rows = sorted(csv.DictReader(fh), key=lambda r: int(r["Start_Timestamp"]))
-    gate = [int(r["Start_Timestamp"]) for r in rows
-            if short(r["Kernel_Name"]).startswith("route_bf16_kernel")]
-    boundary = gate[PREFILL_DISPATCHES] if len(gate) > PREFILL_DISPATCHES else float("inf")
-    pre_t, dec_t, order = collections.defaultdict(list), collections.defaultdict(list), []
-    for r in rows:
-        k = short(r["Kernel_Name"])
-        if k.startswith("at::") or "rocclr" in k:
-            continue
-        if k not in order:
-            order.append(k)
-        dt = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0
-        (pre_t if int(r["Start_Timestamp"]) < boundary else dec_t)[k].append(dt)
-    frp, frd = counter_by_regime(fetch_csv, "FETCH_SIZE", ff)
-    wrp, wrd = counter_by_regime(write_csv, "WRITE_SIZE", wf)
-    mib = lambda v: _mean(v) / 2 ** 20
-    lines = ["| kernel | prefill calls | prefill avg us | decode calls | decode avg us | "
-             "prefill read MiB | prefill write MiB | decode read MiB | decode write MiB |",
-             "|---|---|---|---|---|---|---|---|---|"]
-    for k in order:
-        pre, dec = pre_t.get(k, []), dec_t.get(k, [])
-        lines.append("| `%s` | %d | %.1f | %d | %.1f | %.1f | %.1f | %.2f | %.2f |" % (
-            k, len(pre), _mean(pre), len(dec), _mean(dec), mib(frp.get(k, [])),
-            mib(wrp.get(k, [])), mib(frd.get(k, [])), mib(wrd.get(k, []))))
-    return "\n".join(lines) + "\n"
-
-
 def mfma(counter_csv, cus=256, simds=1024, xcds=8):
-    """Median over the prefill dispatches of each tiled GEMM: duration, clock, MFMA-busy share
+    """Median over the dispatches of each tiled GEMM: duration, clock, MFMA-busy share
     of SIMD cycles, CU-busy share, MFMA flop per launch (512 flop per bf16 MOP)."""
     per = collections.defaultdict(lambda: collections.defaultdict(float))
     meta = {}
@@ -129,25 +134,25 @@ def mfma(counter_csv, cus=256, simds=1024, xcds=8):
                        (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
     by_kernel = collections.defaultdict(list)
     for d in sorted(per):
-        by_kernel[meta[d][0]].append(d)
+        if meta[d][0].startswith("grouped_gemm_kernel"):
+            by_kernel[meta[d][0]].append(d)
     lines = ["| kernel | duration us | GPU clock | MFMA busy (of SIMD cycles) | CU busy | "
              "MFMA flop per launch | LDS bank conflicts |", "|---|---|---|---|---|---|---|"]
-    med = lambda v: sorted(v)[len(v) // 2]
     for k, ds in by_kernel.items():
-        ds = ds[:PREFILL_DISPATCHES]
         dur = [meta[d][1] for d in ds]
-        clk = [per[d]["GRBM_GUI_ACTIVE"] / xcds / meta[d][1] for d in ds]
         cyc = [per[d]["GRBM_GUI_ACTIVE"] / xcds for d in ds]
+        clk = [c / meta[d][1] for d, c in zip(ds, cyc)]
         busy = [per[d]["SQ_VALU_MFMA_BUSY_CYCLES"] / (c * simds) for d, c in zip(ds, cyc)]
         cub = [per[d]["SQ_BUSY_CU_CYCLES"] / (c * cus) for d, c in zip(ds, cyc)]
         fl = [per[d]["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512 for d in ds]
         bc = [per[d]["SQ_LDS_BANK_CONFLICT"] for d in ds]
         lines.append("| `%s` | %.1f | %.2f GHz | %.1f %% | %.1f %% | %.4g | %.0f |" % (
-            k, med(dur) * 1e6, med(clk) / 1e9, 100 * med(busy), 100 * med(cub), med(fl), med(bc)))
+            k, _med(dur) * 1e6, _med(clk) / 1e9, 100 * _med(busy), 100 * _med(cub), _med(fl),
+            _med(bc)))
     return "\n".join(lines) + "\n"
 
 
-def breakdown(runs, steps=PREFILL_DISPATCHES):
+def breakdown(runs, steps):
     """Markdown table per run: each kernel's launches per step, mean duration and
     time per step (every dispatch of a run belongs to one of its `steps` steps)."""
     lines = []
@@ -177,32 +182,29 @@ def breakdown(runs, steps=PREFILL_DISPATCHES):
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
+    k = sub.add_parser("kernels")
+    k.add_argument("trace_csv")
     t = sub.add_parser("traffic")
+    t.add_argument("workload")
     t.add_argument("fetch_csv")
     t.add_argument("write_csv")
+    t.add_argument("--copy-mib", type=int, default=1024)
     t.add_argument("--out", default="profiles/ffn_traffic.json")
-    k = sub.add_parser("table")
-    k.add_argument("trace_csv")
-    k.add_argument("fetch_csv")
-    k.add_argument("write_csv")
-    for p in (t, k):
-        p.add_argument("--fetch-factor", type=float, required=True)
-        p.add_argument("--write-factor", type=float, required=True)
     u = sub.add_parser("mfma")
     u.add_argument("counter_csv")
     b = sub.add_parser("breakdown")
+    b.add_argument("--steps", type=int, required=True)
     b.add_argument("runs", nargs="+", help="LABEL=kernel-trace csv")
     args = ap.parse_args(argv)
-    if args.cmd == "breakdown":
-        print(breakdown([r.split("=", 1) for r in args.runs]), end="")
+    if args.cmd == "kernels":
+        print(kernels(args.trace_csv), end="")
+    elif args.cmd == "breakdown":
+        print(breakdown([r.split("=", 1) for r in args.runs], args.steps), end="")
     elif args.cmd == "mfma":
         print(mfma(args.counter_csv), end="")
-    elif args.cmd == "traffic":
-        print(json.dumps(traffic(args.fetch_csv, args.write_csv, args.fetch_factor,
-                                 args.write_factor, args.out), indent=1))
     else:
-        print(table(args.trace_csv, args.fetch_csv, args.write_csv, args.fetch_factor,
-                    args.write_factor), end="")
+        print(json.dumps(traffic(args.workload, args.fetch_csv, args.write_csv, args.copy_mib,
+                                 args.out), indent=1))
 
 
 if __name__ == "__main__":

@@ -150,6 +150,24 @@ def test_permute_noalloc_validation(lib):
     assert lib.moe_permute_ws_bytes(T, 8, E) <= moe.MOE_PERMUTE_NOALLOC_MAX_WS
 
 
+def test_grouped_ffn_products_validation(lib):
+    f = lib.moe_grouped_ffn_products
+    arr = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    P = ctypes.cast(arr, ctypes.c_void_p)
+
+    def call(products=1, x=FAKE, y=FAKE, w13=P, w2=P, d=128, f_=64, ws_bytes=1 << 30):
+        return f(x, 1, FAKE, 2, w13, w2, d, f_, 16, y, ctypes.c_void_p(0x100000), ws_bytes,
+                 products, None)
+    assert call(products=0) == moe.MOE_ERR_ARG
+    assert call(products=4) == moe.MOE_ERR_ARG
+    assert call(products=1, x=None) == moe.MOE_ERR_ARG           # gate/up reads x_perm
+    assert call(products=1, w13=None) == moe.MOE_ERR_ARG
+    assert call(products=2, y=None) == moe.MOE_ERR_ARG           # down writes y_perm
+    assert call(products=2, w2=None) == moe.MOE_ERR_ARG
+    assert call(products=3, d=100) == moe.MOE_ERR_SHAPE
+    assert call(products=2, ws_bytes=10) == moe.MOE_ERR_SHAPE
+
+
 def test_grouped_ffn_validation(lib):
     f = lib.moe_grouped_ffn
     arr = (ctypes.c_void_p * 2)(0x1000, 0x2000)

@@ -414,6 +414,31 @@ def test_gather_in_ffn_at_model_shapes(name, regime):
     assert torch.equal(yp0, yp1) and torch.equal(y0, y1)
 
 
+@pytest.mark.parametrize("name,regime", [("mixtral_8x7b", "prefill"), ("mixtral_8x7b", "decode"),
+                                         ("deepseek_v2_lite", "decode"), ("tiny_fp32", "batch")])
+def test_ffn_products_one_at_a_time_equal_the_whole_call(name, regime):
+    """moe_grouped_ffn_products: the gate/up product, then the down product on the
+    same workspace, gives the bits of moe_grouped_ffn (the Mixtral prefill shape
+    splits K over its last tiles, the decode shapes stream every group)."""
+    cfg = synth.CONFIGS[name]
+    T = cfg.T(regime)
+    say("[products]", name, regime, "T=%d" % T)
+    inp = synth.make_layer(cfg, T, seed=2, device="cuda")
+    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                       shared=inp.shared, coact=cfg.coact)
+    share.run()
+    torch.cuda.synchronize()
+    N = int(share.perm["group_offsets"][-1])
+    whole = share.y_perm[:N].clone()
+    share.y_perm.zero_()
+    for products in (moe.MOE_FFN_GATE_UP, moe.MOE_FFN_DOWN):
+        moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
+                            cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn,
+                            products=products)
+    torch.cuda.synchronize()
+    assert torch.equal(share.y_perm[:N], whole)
+
+
 def test_very_long_batch_routing_and_packaging_every_element():
     """T = 100000 tokens at a small width: the long-batch paths of the gate (tiled
     scores), histogram (several workgroups), permute (count / scan / scatter over
