@@ -23,7 +23,12 @@ against the paper (arXiv 2607.08782, Sec. VI), with plain loops:
 Latency functions are convex piecewise-linear, given as a list of pieces
 (slope, intercept): f(z) = max over pieces of slope * z + intercept (the
 "standard piecewise linear approximation" of Sec. VI-C, read as convex so that
-the epigraph constraints are exact).
+the epigraph constraints are exact).  f_comp may also be given as pieces
+(slope, slope_active, intercept) of the GPU's load lambda_j and its number of
+active experts a_j (hosted experts with at least one token): Eq. 2 prices the
+computation by the load alone, but a decode-sized step streams the weights of
+every active expert, so its time grows with a_j, which is as linear in the
+placement as lambda_j is.
 
 Workload tensors are W[l][j][i]: tokens on GPU j routed to expert i in layer l
 (Sec. VI-A).  A placement is an integer array P[l][i] = host GPU of expert i.
@@ -38,6 +43,26 @@ import numpy as np
 def pwl(pieces, z):
     """f(z) = max over (slope, intercept) pieces."""
     return max(a * z + b for a, b in pieces)
+
+
+def comp(pieces, lam, act):
+    """f_comp of a GPU with load lam and act active experts: (slope, intercept)
+    pieces price the load alone, (slope, slope_active, intercept) pieces both."""
+    if len(pieces[0]) == 2:
+        return pwl(pieces, lam)
+    return max(a * lam + c * act + b for a, c, b in pieces)
+
+
+def active(W_l, P_l, G):
+    """Active experts of every GPU: hosted experts with a non-zero demand."""
+    act = [0] * G
+    for i in range(len(P_l)):
+        demand = 0.0
+        for k in range(G):
+            demand += W_l[k][i]
+        if demand != 0:
+            act[P_l[i]] += 1
+    return act
 
 
 def loads(W_l, P_l, G):
@@ -68,7 +93,8 @@ def latency(W, P, G, d, f_comp, f_comm):
     total_comm = 0.0
     for l in range(len(W)):
         lam = loads(W[l], P[l], G)
-        total_comp += max(pwl(f_comp, lam[j]) for j in range(G))
+        act = active(W[l], P[l], G)
+        total_comp += max(comp(f_comp, lam[j], act[j]) for j in range(G))
         D = volumes(W[l], P[l], G, d)
         worst = None
         for j in range(G):
@@ -127,11 +153,12 @@ def lp_optimum(W, G, C_max, d, f_comp, f_comm):
     for l in range(L):
         demand = [sum(W[l][k][i] for k in range(G)) for i in range(E)]
         for j in range(G):
-            # tau_comp >= slope * lambda_j(x) + intercept
-            for a, b0 in f_comp:
+            # tau_comp >= slope * lambda_j(x) [+ slope_active * a_j(x)] + intercept
+            for piece in f_comp:
+                a, c_act, b0 = piece if len(piece) == 3 else (piece[0], 0.0, piece[1])
                 row = np.zeros(nv)
                 for i in range(E):
-                    row[ix(l, i, j)] = a * demand[i]
+                    row[ix(l, i, j)] = a * demand[i] + (c_act if demand[i] != 0 else 0.0)
                 row[itc(l)] = -1.0
                 A.append(row)
                 b.append(-b0)

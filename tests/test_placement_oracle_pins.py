@@ -28,6 +28,30 @@ def test_hand_worked_example_of_eq1_to_eq4():
     assert op.latency(W, P, G, d, [(1.0, 0.0), (2.0, -5.0)], [(0.0, 1.0), (1.0, 0.0)]) == g["T_pwl"]
 
 
+def test_hand_worked_example_with_active_experts():
+    """f_comp of the load and the number of active experts, hand-evaluated in the
+    fixture; an expert with no tokens does not count as active."""
+    g = json.load(open(GOLDEN))
+    W, P, G, d = g["W"], g["P"], g["G"], g["d"]
+    f2 = [tuple(p) for p in g["f_comp_2d"]]
+    lin = [(1.0, 0.0)]
+    assert op.active(W[0], P[0], G) == g["active"]
+    assert op.latency(W, P, G, d, f2, lin) == g["T_2d"]
+    W4 = [[row + [0] for row in W[0]]]                 # a fourth expert, no tokens, on GPU 1
+    assert op.active(W4[0], P[0] + [1], G) == g["active"]
+    assert op.latency(W4, [P[0] + [1]], G, d, f2, lin) == g["T_2d"]
+    # pieces with no active-expert slope are the one-variable model
+    assert op.latency(W, P, G, d, [(1.0, 0.0, 0.0)], lin) == g["T_linear"]
+
+
+def test_lp_optimum_prices_active_experts_on_one_gpu():
+    """One GPU hosts every expert: lambda = the whole demand, a = the experts with
+    tokens; tau_comp = max(z + 4a, 2a) at z = 16, a = 2 (one expert has none) -> 24."""
+    W = [[[3, 0, 13]]]
+    beta, x = op.lp_optimum(W, 1, 3, 1.0, [(1.0, 4.0, 0.0), (0.0, 2.0, 0.0)], [(1.0, 0.0)])
+    assert beta == pytest.approx(24.0, abs=1e-9)
+
+
 def test_exhaustive_finds_the_placement_that_is_optimal_by_construction():
     # GPU 0's tokens go only to experts 0, 1 and GPU 1's only to 2, 3, with equal
     # demand: hosting {0,1} on GPU 0 and {2,3} on GPU 1 balances the load exactly
