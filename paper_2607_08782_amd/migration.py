@@ -18,6 +18,12 @@ so they finish before the next exchange.  This module does the one-GPU part:
   hide, and the compute stream waits for the chunks' completion event where
   the window closes (the point the all-to-all of the combine would start).
   When every chunk has landed, ``switch`` re-points the layer's weight table.
+* The bytes a window can hide are predicted from the last window: the copies
+  compete with the FFN for memory bandwidth (the FFN slows down and the copy
+  rate drops while both run), so the next window gets the bytes the last
+  window's copy rate moves in the last window's FFN time, times a margin.
+  The first window starts from the caller's estimate (f_comp of the step's
+  load at the uncontended copy rate).
 """
 from __future__ import annotations
 
@@ -55,6 +61,11 @@ class MigrationStats:
     windows: int = 0
     bytes: int = 0
     stall_ms: List[float] = field(default_factory=list)
+    budgets: List[int] = field(default_factory=list)
+
+
+# share of the last window's FFN time the next window's copies are sized to fill
+WINDOW_MARGIN = 0.85
 
 
 class Migrator:
@@ -83,6 +94,8 @@ class Migrator:
         self.target: Optional[np.ndarray] = None
         self.incoming: Dict[int, int] = {}
         self.stats = MigrationStats()
+        self.budget_bytes = self.chunk_bytes     # bytes the next window may take
+        self._sent = 0
 
     # -- current weights -------------------------------------------------------
     def weights(self, placement: Optional[np.ndarray] = None):
@@ -126,6 +139,7 @@ class Migrator:
             return None
         self.stream.wait_event(opened)
         sent = 0
+        self.stats.budgets.append(int(budget_bytes))
         with torch.cuda.stream(self.stream):
             while self.pending and (sent == 0 or sent + self.pending[0].nbytes <= budget_bytes):
                 c = self.pending.pop(0)
@@ -134,11 +148,28 @@ class Migrator:
                 src = (self.store.w13 if c.which == 0 else self.store.w2)[c.expert]
                 dst[c.start:c.stop].copy_(src[c.start:c.stop], non_blocking=True)
                 sent += c.nbytes
-        done = torch.cuda.Event()
+        done = torch.cuda.Event(enable_timing=True)
         done.record(self.stream)
         self.stats.windows += 1
         self.stats.bytes += sent
+        self._sent = sent
         return done
+
+    def empty_window(self, opened: torch.cuda.Event) -> torch.cuda.Event:
+        """The window's stream join with no copy in it: what a window costs the compute
+        stream by itself (an event on the migration stream after `opened`)."""
+        self.stream.wait_event(opened)
+        done = torch.cuda.Event(enable_timing=True)
+        done.record(self.stream)
+        return done
+
+    def observe(self, ffn_ms: float, copy_ms: float):
+        """Size the next window from the last one: its copies moved `_sent` bytes in
+        `copy_ms` while the FFN, slowed by them, took `ffn_ms`."""
+        if self._sent <= 0 or copy_ms <= 0:
+            return
+        rate = self._sent / copy_ms                          # bytes per ms under contention
+        self.budget_bytes = max(self.chunk_bytes, int(WINDOW_MARGIN * rate * ffn_ms))
 
     @property
     def finished(self) -> bool:
@@ -174,18 +205,28 @@ def measure_h2d_rate(nbytes: int = 64 << 20, device="cuda") -> float:
     return nbytes / (a.elapsed_time(b) * 1e3)
 
 
-def run_step(share, mig: Optional[Migrator], budget_bytes: int, timing: Optional[dict] = None):
+def run_step(share, mig: Optional[Migrator], budget_bytes: Optional[int] = None,
+             timing: Optional[dict] = None, empty: bool = False):
     """One layer step with the FFN window open to migration; returns the time (ms) the
     compute stream waited at the window's close for the copies (None if no copy).
-    With `timing`, the FFN window's own duration (ms) is appended to timing["ffn"]."""
+    The window takes `budget_bytes`, or the migrator's own prediction from the last
+    window (which this step then updates).  With `timing`, the FFN window's own
+    duration (ms) is appended to timing["ffn"] and the copies' to timing["copy"].
+    empty=True opens and closes the window with no copy (the join's own cost)."""
     cur = torch.cuda.current_stream()
     share.route()
     moe.moe_expert_histogram(share.topk_idx, share.E, counts=share.counts, coact=share.coact)
     moe.moe_permute(share.X, share.topk_idx, share.topk_gate, share.counts, share.placement,
                     share.dev, E=share.E, cap_rows=share.cap_rows, out=share.perm, ws=share.ws_perm)
-    opened = torch.cuda.Event(enable_timing=timing is not None)
+    opened = torch.cuda.Event(enable_timing=True)
     opened.record(cur)
-    done = mig.window(opened, budget_bytes) if mig is not None else None
+    adaptive = budget_bytes is None and not empty
+    if mig is not None and adaptive:
+        budget_bytes = mig.budget_bytes
+    if mig is not None and empty:
+        done = mig.empty_window(opened)
+    else:
+        done = mig.window(opened, budget_bytes) if mig is not None else None
     if share.weights is not None:
         moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
                             cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
@@ -201,6 +242,11 @@ def run_step(share, mig: Optional[Migrator], budget_bytes: int, timing: Optional
         after.record(cur)
         after.synchronize()
         stall = ffn_end.elapsed_time(after)
+        copy_ms = opened.elapsed_time(done)
+        if adaptive:
+            mig.observe(opened.elapsed_time(ffn_end), copy_ms)
+        if timing is not None:
+            timing.setdefault("copy", []).append(copy_ms)
     if timing is not None:
         ffn_end.synchronize()
         timing.setdefault("ffn", []).append(opened.elapsed_time(ffn_end))

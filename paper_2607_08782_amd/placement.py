@@ -52,6 +52,22 @@ def pwl_eval(pieces: Pieces, z):
     return np.max([a * z + b for a, b in pieces], axis=0)
 
 
+def comp_pieces(f_comp):
+    """f_comp as (slope of the load, slope of the active-expert count, intercept)
+    triples: (slope, intercept) pieces price the load alone."""
+    return [(p[0], 0.0, p[1]) if len(p) == 2 else (p[0], p[1], p[2]) for p in f_comp]
+
+
+def comp_eval(f_comp, lam, act):
+    """f_comp of a GPU with load lam and act active experts (hosted experts with
+    at least one token): a decode-sized step streams every active expert's
+    weights, so its time grows with act as well as with the load (Eq. 2 extended;
+    pieces of the load alone give Eq. 2 itself)."""
+    lam = np.asarray(lam, dtype=np.float64)
+    act = np.asarray(act, dtype=np.float64)
+    return np.max([a * lam + c * act + b for a, c, b in comp_pieces(f_comp)], axis=0)
+
+
 def fit_convex_pwl(z, t) -> List[Tuple[float, float]]:
     """Convex, non-decreasing piecewise-linear model through the lower convex hull of (z, t)."""
     pts = sorted(zip(np.asarray(z, float).tolist(), np.asarray(t, float).tolist()))
@@ -89,8 +105,9 @@ def layer_latencies(W: np.ndarray, P: np.ndarray, d: float, f_comp: Pieces, f_co
     onehot[np.arange(L)[:, None], np.arange(E)[None, :], P] = 1.0
     demand = W.sum(axis=1)                                   # [L][E]
     lam = np.einsum("le,leg->lg", demand, onehot)            # Eq. 1
+    act = np.einsum("le,leg->lg", (demand != 0).astype(np.float64), onehot)
     D = d * np.einsum("lje,lek->ljk", W, onehot)             # Eq. 3
-    comp = pwl_eval(f_comp, lam).max(axis=1)
+    comp = comp_eval(f_comp, lam, act).max(axis=1)
     fc = pwl_eval(f_comm, D)
     fc[:, np.arange(G), np.arange(G)] = 0.0
     comm = fc.sum(axis=2).max(axis=1)
@@ -133,10 +150,11 @@ def _build_lp(W: np.ndarray, d: float, C_max: int, f_comp: Pieces, f_comm: Piece
     demand = W.sum(axis=1)
     for l in range(L):
         for j in range(G):
-            for a, b0 in f_comp:                       # slope*lambda_j + b0 <= tau_comp
+            for a, c_act, b0 in comp_pieces(f_comp):   # a lambda_j + c a_j + b0 <= tau_comp
                 for i in range(E):
-                    if demand[l, i] != 0 and a != 0:
-                        rows.append(r); cols.append(xi(l, i, j)); vals.append(a * demand[l, i])
+                    v = a * demand[l, i] + (c_act if demand[l, i] != 0 else 0.0)
+                    if v != 0:
+                        rows.append(r); cols.append(xi(l, i, j)); vals.append(v)
                 rows.append(r); cols.append(itc[l]); vals.append(-1.0)
                 rhs.append(-b0); r += 1
             for p, (jj, k) in enumerate(pairs):        # sum_k u_jk <= tau_comm
@@ -276,10 +294,11 @@ def _min_aux(xl: np.ndarray, W: np.ndarray, d, f_comp, f_comm) -> np.ndarray:
     L, E, G = xl.shape
     demand = W.sum(axis=1)
     lam = np.einsum("le,leg->lg", demand, xl)
+    act = np.einsum("le,leg->lg", (demand != 0).astype(np.float64), xl)
     D = d * np.einsum("lje,lek->ljk", W, xl)
     u = pwl_eval(f_comm, D)
     off = ~np.eye(G, dtype=bool)
-    tau_c = pwl_eval(f_comp, lam).max(axis=1)
+    tau_c = comp_eval(f_comp, lam, act).max(axis=1)
     tau_m = np.where(off[None], u, 0.0).sum(axis=2).max(axis=1)
     u_pairs = u[:, off]                                       # (j, k != j), j-major
     return np.concatenate([tau_c, tau_m, u_pairs.reshape(-1)])
@@ -394,7 +413,15 @@ def place(W, G: int, C_max: int, d: float, f_comp: Pieces, f_comm: Pieces, eps: 
     P0 = _greedy(W, d, C_max, f_comp, f_comm)
     hi = total_latency(W, P0, d, f_comp, f_comm)
     demand = W.sum(axis=(1, 2))
-    lo = float(np.sum(pwl_eval(f_comp, demand / G)) + L * (G - 1) * float(pwl_eval(f_comm, 0.0)))
+    if all(c >= 0 for _, c, _ in comp_pieces(f_comp)):
+        # the straggler's f_comp is at least f_comp of the mean load and of the mean
+        # active-expert count (convex and non-decreasing in the count), every
+        # expert with tokens being active somewhere
+        n_act = (W.sum(axis=1) != 0).sum(axis=1)
+        lo = float(np.sum(comp_eval(f_comp, demand / G, n_act / G)) +
+                   L * (G - 1) * float(pwl_eval(f_comm, 0.0)))
+    else:
+        lo = 0.0
     lo = min(lo, hi) * (1.0 - 1e-12)
     x_best, _ = _feasible(lp, hi)
     if x_best is None:

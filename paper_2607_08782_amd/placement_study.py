@@ -39,6 +39,7 @@ if __package__ in (None, ""):
     __package__ = "paper_2607_08782_amd"
 
 from . import moe, placement as pl, synth  # noqa: E402
+from .migration import WINDOW_MARGIN  # noqa: E402
 from .layer import LayerShare  # noqa: E402
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -98,26 +99,35 @@ def migration_rows(cfg, G, T, weights, plans, f_comp, dev=0, reps=3):
         if not inc or x_new[:, dev].sum() != x_old[:, dev].sum():
             continue
         inp = synth.make_layer(cfg, T, seed=0, device="cuda", batch=b, experts="none")
-        mig = Migrator(store, x_old, dev, spare=len(inc))
+        mig = Migrator(store, x_old, dev, spare=len(inc), chunk_bytes=2 << 20)
         w13, w2 = mig.weights()
         share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, x_old, dev, w13, w2)
         base = {}
         for _ in range(reps):
             run_step(share, None, 0, base)
+        # what closing a window costs with nothing copied in it (the stream join)
+        join = [run_step(share, mig, 0, None, empty=True) * 1e3 for _ in range(2 * reps + 1)]
         lam = int(share.perm["group_offsets"][-1])
-        window_us = float(pl.pwl_eval(f_comp, lam))
+        act = int((torch.diff(share.perm["group_offsets"]) > 0).sum())
+        window_us = float(pl.comp_eval(f_comp, lam, act))
         moved = mig.plan(x_new)
+        # the first window from f_comp at the uncontended copy rate, the next ones from
+        # the last window's copy rate and FFN time with the copies in flight
+        mig.budget_bytes = int(window_us * rate)
         during, stalls, steps = {}, [], 0
         while not mig.finished:
-            st = run_step(share, mig, int(window_us * rate), during)
+            st = run_step(share, mig, None, during)
             stalls.append(0.0 if st is None else st * 1e3)
             steps += 1
         torch.cuda.synchronize()
+        ffn_alone = statistics.median(base["ffn"]) * 1e3
+        ffn_copy = statistics.median(during["ffn"]) * 1e3
         out.append({"batch": b, "experts_in": len(inc), "mbytes": moved / 1e6, "rate_gbs": rate / 1e3,
-                    "window_us": window_us, "steps": steps,
-                    "ffn_us": statistics.median(base["ffn"]) * 1e3,
-                    "ffn_copy_us": statistics.median(during["ffn"]) * 1e3,
-                    "max_stall_us": max(stalls)})
+                    "window_us": window_us, "steps": steps, "ffn_us": ffn_alone,
+                    "ffn_copy_us": ffn_copy, "slowdown": ffn_copy / ffn_alone - 1.0,
+                    "copy_rate_gbs": moved / (sum(during["copy"]) * 1e-3) / 1e9,
+                    "max_stall_us": max(stalls), "median_stall_us": statistics.median(stalls),
+                    "join_us": statistics.median(join)})
     return out
 
 
@@ -132,7 +142,8 @@ def main(argv=None):
     cfg = synth.CONFIGS["qwen15_moe_a27b"]
     G, T = cfg.G, cfg.T("batch")
     prof = json.load(open(os.path.join(ROOT, "profiles", "fcomp_qwen15_moe_a27b.json")))
-    f_comp = [tuple(p) for p in prof["pieces"]]
+    # f_comp of the load and the active-expert count when the profile has its grid
+    f_comp = [tuple(p) for p in prof.get("pieces_2d", prof["pieces"])]
     f_comm = [(1.0 / LINK_BYTES_PER_US, LINK_LATENCY_US)]
     d_bytes = cfg.d * 2.0
     weights = [synth.expert_weights(cfg, e, 0, "cuda") for e in range(cfg.E)]
@@ -144,11 +155,13 @@ def main(argv=None):
         t0 = time.perf_counter()
         res = pl.place(W[None], G, args.cmax, d_bytes, f_comp, f_comm, seed=b)
         opt_s.append(time.perf_counter() - t0)
+        # the paper's procedure alone: binary search, iterative rounding, completion
+        alg1 = pl.place(W[None], G, args.cmax, d_bytes, f_comp, f_comm, seed=b, polish=False)
         if P_static is None:
             P_static = res.P
         plans = {"static": P_static, "reactive": P_prev if P_prev is not None else P_static,
-                 "proactive": res.P}
-        row = {"batch": b, "beta_star": res.beta_star}
+                 "proactive": res.P, "alg1": alg1.P}
+        row = {"batch": b, "beta_star": res.beta_star, "alg1_beta_star": alg1.beta_star}
         for name, P in plans.items():
             comp, comm = pl.layer_latencies(W[None].astype(np.float64), P, d_bytes, f_comp, f_comm)
             x_map = np.zeros((cfg.E, G), np.uint8)
@@ -159,49 +172,66 @@ def main(argv=None):
         rows.append(row)
         P_prev = res.P
         proactive.append(res.P)
-        print("batch %2d: beta* %.1f | static %.1f | reactive %.1f | proactive %.1f (model us)" % (
-            b, res.beta_star, row["static"]["model_us"], row["reactive"]["model_us"],
-            row["proactive"]["model_us"]), flush=True)
+        print("batch %2d: beta* %.1f | static %.1f | reactive %.1f | proactive %.1f | Alg. 1 alone "
+              "%.1f (model us)" % (b, res.beta_star, row["static"]["model_us"],
+                                   row["reactive"]["model_us"], row["proactive"]["model_us"],
+                                   row["alg1"]["model_us"]), flush=True)
     mean = lambda k, f: statistics.mean(r[k][f] for r in rows)
     lines = ["# Proactive vs. reactive vs. static placement on a drifting workload", "",
              "Qwen1.5-MoE-A2.7B-shaped layer (d=2048, 60 experts, top-4, f=1408), 8 GPUs, C_max = %d,"
              % args.cmax,
              "%d batches of %d tokens (a GPU slice each of %d), popularity re-drawn every %d batches;"
              % (args.batches, T, T // G, cfg.drift_every),
-             "synthetic seeded inputs.  Model: Eq. 1-4 with f_comp profiled on this GPU and f_comm =",
-             "%.0f us + bytes / 153 GB/s per peer (modelled link).  Measured: the busiest GPU's"
+             "synthetic seeded inputs.  Model: Eq. 1-4 with f_comp profiled on this GPU (%s) and"
+             % ("a convex piecewise-linear function of the GPU's load and of its active experts"
+                if "pieces_2d" in prof else "a convex piecewise-linear function of the load"),
+             "f_comm = %.0f us + bytes / 153 GB/s per peer (modelled link).  Measured: the busiest"
              % LINK_LATENCY_US,
-             "`moe_grouped_ffn` step under each placement, median of 5 timed calls.", "",
+             "GPU's `moe_grouped_ffn` step under each placement, median of 5 timed calls.",
+             "Proactive = the optimizer as the library runs it (Alg. 1, then a move/swap polish that",
+             "is not the paper's, keeping the polished greedy placement when it is better); Alg. 1",
+             "alone = binary search, iterative rounding and completion only.", "",
              "Command: `python -m paper_2607_08782_amd.placement_study --batches %d --cmax %d --out %s`"
              % (args.batches, args.cmax, args.out), "",
-             "| batch | beta* (LP) | static model | reactive model | proactive model | static FFN | reactive FFN | proactive FFN |",
-             "|---|---|---|---|---|---|---|---|"]
+             "| batch | beta* (LP) | static model | reactive model | proactive model | Alg. 1 alone model | proactive T/beta* | Alg. 1 alone T/beta* | static FFN | reactive FFN | proactive FFN | Alg. 1 alone FFN |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|"]
     for r in rows:
-        lines.append("| %d | %.1f | %.1f | %.1f | %.1f | %.1f | %.1f | %.1f |" % (
+        lines.append("| %d | %.1f | %.1f | %.1f | %.1f | %.1f | %.3f | %.3f | %.1f | %.1f | %.1f | %.1f |" % (
             r["batch"], r["beta_star"], r["static"]["model_us"], r["reactive"]["model_us"],
-            r["proactive"]["model_us"], r["static"]["measured_ffn_us"],
-            r["reactive"]["measured_ffn_us"], r["proactive"]["measured_ffn_us"]))
-    lines.append("| mean | %.1f | %.1f | %.1f | %.1f | %.1f | %.1f | %.1f |" % (
+            r["proactive"]["model_us"], r["alg1"]["model_us"],
+            r["proactive"]["model_us"] / r["beta_star"], r["alg1"]["model_us"] / r["beta_star"],
+            r["static"]["measured_ffn_us"], r["reactive"]["measured_ffn_us"],
+            r["proactive"]["measured_ffn_us"], r["alg1"]["measured_ffn_us"]))
+    lines.append("| mean | %.1f | %.1f | %.1f | %.1f | %.1f | %.3f | %.3f | %.1f | %.1f | %.1f | %.1f |" % (
         statistics.mean(r["beta_star"] for r in rows), mean("static", "model_us"),
-        mean("reactive", "model_us"), mean("proactive", "model_us"),
+        mean("reactive", "model_us"), mean("proactive", "model_us"), mean("alg1", "model_us"),
+        statistics.mean(r["proactive"]["model_us"] / r["beta_star"] for r in rows),
+        statistics.mean(r["alg1"]["model_us"] / r["beta_star"] for r in rows),
         mean("static", "measured_ffn_us"), mean("reactive", "measured_ffn_us"),
-        mean("proactive", "measured_ffn_us")))
+        mean("proactive", "measured_ffn_us"), mean("alg1", "measured_ffn_us")))
     lines += ["", "All times in microseconds.  Optimizer wall time per batch (host CPU): "
               "median %.2f s, max %.2f s." % (statistics.median(opt_s), max(opt_s)), ""]
     mrows = migration_rows(cfg, G, T, weights, proactive, f_comp)
     lines += ["## Migrating to each new proactive placement (GPU 0, Sec. V-B)", "",
               "Incoming experts are copied from pinned host memory (standing in for the peer",
               "GPUs; a host-to-device copy on the DMA engines) into spare buffers, chunk by chunk,",
-              "inside the FFN window of the following steps: each window gets the bytes that",
-              "f_comp(lambda of GPU 0) at the measured copy rate predicts it can hide, and the",
-              "step waits for them where the window closes (where the combine's all-to-all",
-              "would start).  The batch keeps being served on the old placement meanwhile.", "",
-              "| batch | experts in | MB | copy GB/s | window us | steps | FFN us alone | FFN us with copies | max wait at close us |",
-              "|---|---|---|---|---|---|---|---|---|"]
+              "inside the FFN window of the following steps, and the step waits for them where",
+              "the window closes (where the combine's all-to-all would start).  The first window",
+              "gets the bytes that f_comp(lambda of GPU 0) at the uncontended copy rate predicts",
+              "it can hide; every later window the bytes the last window's copies moved per ms,",
+              "times the last window's FFN time with copies in flight, times %.2f.  The batch"
+              % WINDOW_MARGIN,
+              "keeps being served on the old placement meanwhile.  The wait at the window's",
+              "close includes the stream join itself, measured with windows that copy nothing",
+              "(join); late = wait - join.  Copy GB/s in windows = bytes over the windows' open-to-",
+              "last-copy times (joins included).", "",
+              "| batch | experts in | MB | copy GB/s alone | copy GB/s in windows | first window us | steps | FFN us alone | FFN us with copies | FFN slowdown | join us | median / max late us |",
+              "|---|---|---|---|---|---|---|---|---|---|---|---|"]
     for m in mrows:
-        lines.append("| %d | %d | %.1f | %.1f | %.1f | %d | %.1f | %.1f | %.1f |" % (
-            m["batch"], m["experts_in"], m["mbytes"], m["rate_gbs"], m["window_us"], m["steps"],
-            m["ffn_us"], m["ffn_copy_us"], m["max_stall_us"]))
+        lines.append("| %d | %d | %.1f | %.1f | %.1f | %.1f | %d | %.1f | %.1f | %.0f %% | %.1f | %.1f / %.1f |" % (
+            m["batch"], m["experts_in"], m["mbytes"], m["rate_gbs"], m["copy_rate_gbs"],
+            m["window_us"], m["steps"], m["ffn_us"], m["ffn_copy_us"], 100 * m["slowdown"],
+            m["join_us"], m["median_stall_us"] - m["join_us"], m["max_stall_us"] - m["join_us"]))
     lines.append("")
     text = "\n".join(lines)
     if args.out:

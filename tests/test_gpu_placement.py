@@ -10,9 +10,12 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 from oracle import placement as op
 from paper_2607_08782_amd import moe, placement as pl, synth
 from paper_2607_08782_amd.layer import LayerShare
+
+from parity import OUT_TOL, close, np32
 
 pytestmark = pytest.mark.gpu
 
@@ -59,11 +62,26 @@ def test_optimized_placement_sends_each_gpu_its_eq1_load():
         assert int(share.perm["group_offsets"][-1]) == int(lam[dev])
 
 
+def _against_oracle(share, inp, cfg, P, what):
+    """The share's last run against the oracle's layer on placement P, routed on the
+    share's own logits: routing and row map bit for bit, y within the bf16 tolerance."""
+    local = [int(e) for e in np.nonzero(P[:, share.dev])[0]]
+    ref = oracle.layer_share(np32(inp.X), np32(inp.Wr), np32(inp.bias), cfg.k, P, share.dev,
+                             [np32(inp.w13[e]) for e in local], [np32(inp.w2[e]) for e in local],
+                             logits_f32=np32(share.logits))
+    np.testing.assert_array_equal(share.topk_idx.cpu().numpy(), ref["idx"])
+    np.testing.assert_array_equal(share.perm["token_row"].cpu().numpy(), ref["token_row"])
+    np.testing.assert_array_equal(share.perm["send_counts"].cpu().numpy(), ref["send_counts"])
+    close(np32(share.y), ref["y"], OUT_TOL["bf16"], what)
+
+
 def test_migration_in_ffn_windows_keeps_serving_then_switches_exactly():
     """Experts moving in are copied, chunk by chunk, into spare buffers inside the FFN
     windows of successive steps (Sec. V-B); every step during the migration gives the
     old placement's output bit for bit, and after the switch the layer gives bit for bit
-    what a share built directly on the new placement gives."""
+    what a share built directly on the new placement gives.  The output before the
+    migration and after the switch matches the oracle's layer on the old and the new
+    placement."""
     from paper_2607_08782_amd.migration import ExpertStore, Migrator, run_step
 
     cfg = synth.custom_config(d=256, E=16, k=4, f=256, G=4, zipf=1.2)
@@ -82,6 +100,7 @@ def test_migration_in_ffn_windows_keeps_serving_then_switches_exactly():
     share.run()
     torch.cuda.synchronize()
     y0 = share.y.clone()
+    _against_oracle(share, inp, cfg, P0, "y before the migration")
     moved = mig.plan(P1)
     assert moved == 2 * store.nbytes(only(1)[0])
     steps = 0
@@ -95,6 +114,7 @@ def test_migration_in_ffn_windows_keeps_serving_then_switches_exactly():
     share.set_placement(P1, w13n, w2n)
     share.run()
     torch.cuda.synchronize()
+    _against_oracle(share, inp, cfg, P1, "y after the switch")
     local1 = [int(e) for e in np.nonzero(P1[:, 0])[0]]
     fresh = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, P1, 0, [inp.w13[e] for e in local1],
                        [inp.w2[e] for e in local1])

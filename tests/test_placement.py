@@ -50,6 +50,49 @@ def test_latency_matches_the_oracle(seed):
     assert ours == pytest.approx(ref, rel=1e-12)
 
 
+F_COMP_2D = [(1.0, 6.0, 0.0), (0.2, 20.0, 5.0)]     # load and active experts
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_active_expert_model_matches_the_oracle(seed):
+    """f_comp of the load and the active-expert count: exact latency as the oracle's
+    loops (some experts get no tokens), and the binary search's budget at the LP
+    optimum minimised directly; the integral placement is valid."""
+    rng = np.random.default_rng(50 + seed)
+    L, G, E = 1 + seed % 2, 3, 6
+    W = rng.integers(0, 30, size=(L, G, E))
+    W[:, :, rng.integers(0, E)] = 0                       # an expert nobody routes to
+    P = rng.integers(0, G, size=(L, E))
+    ours = pl.total_latency(W, P, 2.0, F_COMP_2D, F_COMM)
+    ref = op.latency(W.tolist(), P.tolist(), G, 2.0, F_COMP_2D, F_COMM)
+    assert ours == pytest.approx(ref, rel=1e-12)
+    C_max = 3
+    res = pl.place(W, G, C_max, 2.0, F_COMP_2D, F_COMM, seed=seed)
+    beta, _ = op.lp_optimum(W.tolist(), G, C_max, 2.0, F_COMP_2D, F_COMM)
+    assert res.beta_star == pytest.approx(beta, rel=2e-3)
+    _assert_valid(res.P, L, E, G, C_max)
+    assert res.latency == pytest.approx(
+        op.latency(W.tolist(), res.P.tolist(), G, 2.0, F_COMP_2D, F_COMM), rel=1e-12)
+
+
+def test_two_variable_fit_reproduces_a_roofline_and_passes_under_the_points():
+    """f(lambda, a) = max(20 + 15 a, 10 + 0.05 lambda + 2 a), the shape of a step bound
+    by streaming a experts' weights or by the rows' arithmetic: the fit reproduces
+    it on the grid; with noise added it stays at or under every point."""
+    from paper_2607_08782_amd.fcomp import fit_convex_pwl2
+    pts = [(lam, a, max(20 + 15 * a, 10 + 0.05 * lam + 2 * a)) for a in (1, 2, 4, 6, 8)
+           for lam in (8, 16, 64, 256, 1024, 4096) if lam >= a]
+    planes = fit_convex_pwl2(pts)
+    got = pl.comp_eval(planes, [p[0] for p in pts], [p[1] for p in pts])
+    assert np.allclose(got, [p[2] for p in pts], rtol=1e-9)
+    rng = np.random.default_rng(1)
+    noisy = [(lam, a, t * (1 + 0.05 * rng.random())) for lam, a, t in pts]
+    planes = fit_convex_pwl2(noisy)
+    got = pl.comp_eval(planes, [p[0] for p in noisy], [p[1] for p in noisy])
+    assert np.all(got <= np.array([p[2] for p in noisy]) * (1 + 1e-9))
+    assert all(a >= 0 and c >= 0 for a, c, _ in planes)
+
+
 def test_convex_fit_reproduces_a_convex_function_and_underestimates_otherwise():
     z = np.array([0, 16, 64, 128, 512, 1024, 4096], float)
     f = [(0.0, 190.0), (0.3, 0.0)]                       # max(190, 0.3 z)
