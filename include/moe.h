@@ -53,6 +53,7 @@ extern "C" {
 /* products of moe_grouped_ffn_products */
 #define MOE_FFN_GATE_UP 1   /* h = SiLU(W1 x) * (W3 x), kept in the workspace */
 #define MOE_FFN_DOWN    2   /* y = W2 h, from the workspace */
+#define MOE_FFN_SMALL_GROUPS 4   /* hint: no group has more than 64 rows */
 
 /* flags of moe_route_topk */
 #define MOE_RENORM    1   /* gates = softmax over the k selected logits (else: full softmax, restricted) */
@@ -230,6 +231,13 @@ int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets,
  * MOE_FFN_GATE_UP (may be NULL otherwise), y_perm and w2 only with
  * MOE_FFN_DOWN.  Other arguments, requirements and errors as for
  * moe_grouped_ffn; products outside {1, 2, 3} give MOE_ERR_ARG.
+ * Adding MOE_FFN_SMALL_GROUPS to products states that no group holds more
+ * than 64 rows (true of the routed experts of a batch of at most 64 tokens:
+ * a token reaches an expert at most once).  Such groups always take the
+ * weight-streaming kernels, so the call skips the launches of the tiled
+ * kernels and gives bitwise the outputs it gives without the flag; rows of a
+ * group that breaks the statement are left unwritten.  It must be passed the
+ * same way to the MOE_FFN_GATE_UP and the MOE_FFN_DOWN call of one pair.
  */
 int moe_grouped_ffn_products(const void* x_perm, int dtype, const int32_t* group_offsets,
                              int n_groups, const void* const* w13, const void* const* w2, int d,

@@ -866,6 +866,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
                        const int32_t* a_rows, int64_t a_total, int products) {
     if (cap_rows == 0) return MOE_OK;
     const bool up = (products & MOE_FFN_GATE_UP) != 0, down = (products & MOE_FFN_DOWN) != 0;
+    // every group within the streaming kernel's own limit: no tile, no split tile and
+    // no row limit to pass on, so the tiled launches are left out
+    const bool small = (products & MOE_FFN_SMALL_GROUPS) != 0;
     if (dtype == MOE_F32) {
         PtrTable t13, t2;
         for (int i = 0; i < MOE_MAX_GROUPS; ++i) {
@@ -895,8 +898,8 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     char* tbase = tile_part_bytes(cap_rows) > 0
                       ? (char*)part + align256((int64_t)PART_FACTOR * rmax * ncols * 4)
                       : nullptr;
-    float* tpart = tbase ? (float*)(tbase + 256) : nullptr;
-    int* tinfo = tbase ? (int*)tbase : nullptr;
+    float* tpart = tbase && !small ? (float*)(tbase + 256) : nullptr;
+    int* tinfo = tbase && !small ? (int*)tbase : nullptr;
     const int sgrid = ((cus * ST_WG_PER_CU) / NUM_XCD) * NUM_XCD;
     const int64_t red_items = rmax * ((f > d ? f : d) / 4);
     int rgrid = (int)ceil_div(red_items, ST_THREADS);
@@ -925,9 +928,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a1.split_units = grid < TILE_SPLIT_UNITS ? grid : TILE_SPLIT_UNITS;
     a1.a_rows = a_rows;
     a1.a_total = (int)a_total;
-    if (up && a_rows)
+    if (up && !small && a_rows)
         hipLaunchKernelGGL((grouped_gemm_kernel<true, true>), dim3(grid), dim3(GEMM_THREADS), 0, s, a1);
-    else if (up)
+    else if (up && !small)
         hipLaunchKernelGGL((grouped_gemm_kernel<true, false>), dim3(grid), dim3(GEMM_THREADS), 0, s, a1);
     StreamArgs s1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) s1.w[i] = a1.w[i];
@@ -967,7 +970,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a2.split_info = tinfo ? tinfo + 1 : nullptr;
     a2.product = 1;
     a2.a_rows = nullptr;
-    hipLaunchKernelGGL((grouped_gemm_kernel<false, false>), dim3(grid), dim3(GEMM_THREADS), 0, s, a2);
+    if (!small)
+        hipLaunchKernelGGL((grouped_gemm_kernel<false, false>), dim3(grid), dim3(GEMM_THREADS), 0, s,
+                           a2);
     StreamArgs s2 = s1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) s2.w[i] = a2.w[i];
     s2.a = h;

@@ -109,6 +109,11 @@ class LayerShare:
             self._fork = torch.cuda.Event(enable_timing=False)
             self._join = torch.cuda.Event(enable_timing=False)
         self.y = torch.empty((max(T, 1), d), dtype=dt, device=dv)
+        # a token reaches an expert at most once, so with at most 64 tokens no group
+        # exceeds the streaming kernels' limit and the tiled launches can be left out
+        self.ffn_products = moe.MOE_FFN_GATE_UP | moe.MOE_FFN_DOWN
+        if T <= 64:
+            self.ffn_products |= moe.MOE_FFN_SMALL_GROUPS
 
     def set_placement(self, placement: np.ndarray, w13: Sequence[torch.Tensor],
                       w2: Sequence[torch.Tensor]):
@@ -138,7 +143,8 @@ class LayerShare:
 
     def _shared_ffn(self, stream=None):
         moe.moe_grouped_ffn(self.X, self.shared_offsets, self.shared_weights, cap_rows=self.T,
-                            y_perm=self.y_shared, ws=self.ws_shared, stream=stream)
+                            y_perm=self.y_shared, ws=self.ws_shared, stream=stream,
+                            products=self.ffn_products)
 
     def run(self, logits_in: Optional[torch.Tensor] = None) -> torch.Tensor:
         """Enqueue the whole share after the current stream's earlier work; returns y
@@ -162,7 +168,8 @@ class LayerShare:
                                          ws=self.ws_ffn)
             else:
                 moe.moe_grouped_ffn(self.perm["x_perm"], self.perm["group_offsets"], self.weights,
-                                    cap_rows=self.cap_rows, y_perm=self.y_perm, ws=self.ws_ffn)
+                                    cap_rows=self.cap_rows, y_perm=self.y_perm, ws=self.ws_ffn,
+                                    products=self.ffn_products)
         if self._side is not None:
             main.wait_event(self._join)
         elif self.shared_weights is not None:

@@ -159,7 +159,8 @@ def test_grouped_ffn_products_validation(lib):
         return f(x, 1, FAKE, 2, w13, w2, d, f_, 16, y, ctypes.c_void_p(0x100000), ws_bytes,
                  products, None)
     assert call(products=0) == moe.MOE_ERR_ARG
-    assert call(products=4) == moe.MOE_ERR_ARG
+    assert call(products=4) == moe.MOE_ERR_ARG                    # a hint alone runs nothing
+    assert call(products=8) == moe.MOE_ERR_ARG
     assert call(products=1, x=None) == moe.MOE_ERR_ARG           # gate/up reads x_perm
     assert call(products=1, w13=None) == moe.MOE_ERR_ARG
     assert call(products=2, y=None) == moe.MOE_ERR_ARG           # down writes y_perm

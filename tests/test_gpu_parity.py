@@ -439,6 +439,29 @@ def test_ffn_products_one_at_a_time_equal_the_whole_call(name, regime):
     assert torch.equal(share.y_perm[:N], whole)
 
 
+@pytest.mark.parametrize("name,regime", [("mixtral_8x7b", "decode"), ("qwen3_30b_a3b", "decode")])
+def test_small_groups_hint_leaves_the_outputs_bitwise_unchanged(name, regime):
+    """At most 64 tokens: no group exceeds 64 rows, every group streams, and the call
+    with MOE_FFN_SMALL_GROUPS (no tiled launches) gives the bits of the call without."""
+    cfg = synth.CONFIGS[name]
+    T = cfg.T(regime)
+    assert T <= 64
+    say("[small groups]", name, regime, "T=%d" % T)
+    inp = synth.make_layer(cfg, T, seed=3, device="cuda")
+    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                       shared=inp.shared, coact=cfg.coact)
+    assert share.ffn_products & moe.MOE_FFN_SMALL_GROUPS
+    share.run()
+    torch.cuda.synchronize()
+    N = int(share.perm["group_offsets"][-1])
+    hinted = share.y_perm[:N].clone()
+    share.y_perm.zero_()
+    moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
+                        cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
+    torch.cuda.synchronize()
+    assert torch.equal(share.y_perm[:N], hinted)
+
+
 def test_very_long_batch_routing_and_packaging_every_element():
     """T = 100000 tokens at a small width: the long-batch paths of the gate (tiled
     scores), histogram (several workgroups), permute (count / scan / scatter over
