@@ -21,9 +21,12 @@ so they finish before the next exchange.  This module does the one-GPU part:
 * The bytes a window can hide are predicted from the last window: the copies
   compete with the FFN for memory bandwidth (the FFN slows down and the copy
   rate drops while both run), so the next window gets the bytes the last
-  window's copy rate moves in the last window's FFN time, times a margin.
-  The first window starts from the caller's estimate (f_comp of the step's
-  load at the uncontended copy rate).
+  window's copy rate moves in the window's target length, times a margin.
+  The target is the computation's length without copies (``window_ms``, set
+  by the caller from f_comp or a measurement): a window sized from the FFN
+  time with copies would grow with the slowdown it causes.  The first window
+  starts from the caller's estimate (f_comp of the step's load at the
+  uncontended copy rate).
 """
 from __future__ import annotations
 
@@ -95,6 +98,7 @@ class Migrator:
         self.incoming: Dict[int, int] = {}
         self.stats = MigrationStats()
         self.budget_bytes = self.chunk_bytes     # bytes the next window may take
+        self.window_ms: Optional[float] = None   # the computation's length without copies
         self._sent = 0
 
     # -- current weights -------------------------------------------------------
@@ -165,11 +169,13 @@ class Migrator:
 
     def observe(self, ffn_ms: float, copy_ms: float):
         """Size the next window from the last one: its copies moved `_sent` bytes in
-        `copy_ms` while the FFN, slowed by them, took `ffn_ms`."""
+        `copy_ms` while the FFN took `ffn_ms`; the next window gets what that rate
+        moves in the window's target length (`window_ms`, else `ffn_ms`)."""
         if self._sent <= 0 or copy_ms <= 0:
             return
         rate = self._sent / copy_ms                          # bytes per ms under contention
-        self.budget_bytes = max(self.chunk_bytes, int(WINDOW_MARGIN * rate * ffn_ms))
+        target = self.window_ms if self.window_ms else ffn_ms
+        self.budget_bytes = max(self.chunk_bytes, int(WINDOW_MARGIN * rate * target))
 
     @property
     def finished(self) -> bool:
@@ -220,13 +226,9 @@ def run_step(share, mig: Optional[Migrator], budget_bytes: Optional[int] = None,
                     share.dev, E=share.E, cap_rows=share.cap_rows, out=share.perm, ws=share.ws_perm)
     opened = torch.cuda.Event(enable_timing=True)
     opened.record(cur)
-    adaptive = budget_bytes is None and not empty
-    if mig is not None and adaptive:
-        budget_bytes = mig.budget_bytes
-    if mig is not None and empty:
-        done = mig.empty_window(opened)
-    else:
-        done = mig.window(opened, budget_bytes) if mig is not None else None
+    # the window's computation is enqueued first: the copies only wait for `opened`
+    # on the device, and issuing them (one host call per chunk) must not hold back
+    # the launch of the computation they hide behind
     if share.weights is not None:
         moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
                             cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
@@ -236,6 +238,13 @@ def run_step(share, mig: Optional[Migrator], budget_bytes: Optional[int] = None,
     stall = None
     ffn_end = torch.cuda.Event(enable_timing=True)
     ffn_end.record(cur)
+    adaptive = budget_bytes is None and not empty
+    if mig is not None and adaptive:
+        budget_bytes = mig.budget_bytes
+    if mig is not None and empty:
+        done = mig.empty_window(opened)
+    else:
+        done = mig.window(opened, budget_bytes) if mig is not None else None
     if done is not None:
         cur.wait_event(done)                 # the exchange after the FFN must not overlap copies
         after = torch.cuda.Event(enable_timing=True)

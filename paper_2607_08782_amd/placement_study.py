@@ -99,7 +99,7 @@ def migration_rows(cfg, G, T, weights, plans, f_comp, dev=0, reps=3):
         if not inc or x_new[:, dev].sum() != x_old[:, dev].sum():
             continue
         inp = synth.make_layer(cfg, T, seed=0, device="cuda", batch=b, experts="none")
-        mig = Migrator(store, x_old, dev, spare=len(inc), chunk_bytes=2 << 20)
+        mig = Migrator(store, x_old, dev, spare=len(inc), chunk_bytes=1 << 20)
         w13, w2 = mig.weights()
         share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, x_old, dev, w13, w2)
         base = {}
@@ -111,9 +111,10 @@ def migration_rows(cfg, G, T, weights, plans, f_comp, dev=0, reps=3):
         act = int((torch.diff(share.perm["group_offsets"]) > 0).sum())
         window_us = float(pl.comp_eval(f_comp, lam, act))
         moved = mig.plan(x_new)
-        # the first window from f_comp at the uncontended copy rate, the next ones from
-        # the last window's copy rate and FFN time with the copies in flight
-        mig.budget_bytes = int(window_us * rate)
+        # the first window from f_comp at half the uncontended copy rate (copies run
+        # slower beside the computation), the next ones from the last window's rate
+        mig.budget_bytes = int(WINDOW_MARGIN * window_us * rate / 2)
+        mig.window_ms = statistics.median(base["ffn"])      # the FFN without copies
         during, stalls, steps = {}, [], 0
         while not mig.finished:
             st = run_step(share, mig, None, during)
@@ -216,10 +217,12 @@ def main(argv=None):
               "Incoming experts are copied from pinned host memory (standing in for the peer",
               "GPUs; a host-to-device copy on the DMA engines) into spare buffers, chunk by chunk,",
               "inside the FFN window of the following steps, and the step waits for them where",
-              "the window closes (where the combine's all-to-all would start).  The first window",
-              "gets the bytes that f_comp(lambda of GPU 0) at the uncontended copy rate predicts",
-              "it can hide; every later window the bytes the last window's copies moved per ms,",
-              "times the last window's FFN time with copies in flight, times %.2f.  The batch"
+              "the window closes (where the combine's all-to-all would start); the computation is",
+              "enqueued before the copies, which wait for the window's opening on the device.",
+              "Chunks of 1 MB.  The first window gets %.2f x f_comp(lambda, a of GPU 0) x half the"
+              % WINDOW_MARGIN,
+              "uncontended copy rate; every later window the bytes the last window's copies moved per ms",
+              "(with the FFN running), times the FFN's time without copies, times %.2f.  The batch"
               % WINDOW_MARGIN,
               "keeps being served on the old placement meanwhile.  The wait at the window's",
               "close includes the stream join itself, measured with windows that copy nothing",
