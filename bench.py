@@ -101,8 +101,14 @@ def rotated_shares(cfg, inp, **kw):
 
 
 def ffn_call(share, products=None):
-    """The routed experts' moe_grouped_ffn call as LayerShare.run makes it (or the
-    given products of it)."""
+    """The routed experts' FFN call as LayerShare.run makes it: moe_grouped_ffn (or
+    the given products of it), or moe_grouped_ffn_combine when the share fuses the
+    combine into it."""
+    if products is None and share.fused_combine:
+        return lambda: moe.moe_grouped_ffn_combine(
+            share.perm["x_perm"], share.perm["group_offsets"], share.weights,
+            share.perm["token_row"], share.topk_gate, share.y_shared, cap_rows=share.cap_rows,
+            T=share.T, y=share.y, ws=share.ws_ffn)
     products = share.ffn_products if products is None else products
     return lambda: moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"],
                                        share.weights, cap_rows=share.cap_rows, y_perm=share.y_perm,
@@ -115,9 +121,12 @@ def ffn_work(share, cfg):
     N = int(go[-1])
     active = int((sizes > 0).sum())
     esz = 4 if cfg.dtype == "f32" else 2
+    # weights of the active experts once, the rows in, and the rows out (y_perm), or,
+    # when the call combines, the tokens' outputs y with their row maps and gates
+    out = (share.T * cfg.d * esz + share.T * cfg.k * 8.0) if share.fused_combine else N * cfg.d * esz
     return {"N": N, "active": active, "sizes": sizes.tolist(),
             "flops": 6.0 * cfg.d * cfg.f * N, "gate_up_flops": 4.0 * cfg.d * cfg.f * N,
-            "bytes": active * 3.0 * cfg.d * cfg.f * esz + 2.0 * N * cfg.d * esz}
+            "bytes": active * 3.0 * cfg.d * cfg.f * esz + N * cfg.d * esz + out}
 
 
 def phase_calls(share):
@@ -142,8 +151,9 @@ def phase_calls(share):
             share._shared_ffn()
 
     def combine():
-        moe.moe_combine(share.y_perm, share.perm["token_row"], share.topk_gate, share.y_shared,
-                        T=share.T, d=share.d, y=share.y)
+        if not share.fused_combine:        # else part of grouped_ffn
+            moe.moe_combine(share.y_perm, share.perm["token_row"], share.topk_gate,
+                            share.y_shared, T=share.T, d=share.d, y=share.y)
 
     return dict(route_topk=route, histogram=histogram, permute=permute, grouped_ffn=grouped_ffn,
                 shared_ffn=shared_ffn, combine=combine)
@@ -467,7 +477,10 @@ def main():
             "ms_per_step": dm["step_ms"], "eager_ms_per_step": dm["eager_ms"],
             "rows_here": dwork["N"], "active_experts": dwork["active"],
             "weight_copies": dm["weight_copies"],
-            "roofline": {"kernel": "moe_grouped_ffn call (weight-streaming launches)",
+            "roofline": {"kernel": "moe_grouped_ffn_combine call (weight-streaming launches, "
+                                   "the combine in the down product's chunk sum)"
+                                   if dshares[0].fused_combine else
+                                   "moe_grouped_ffn call (weight-streaming launches)",
                          "bound": "hbm", "achieved": dwork["bytes"] / dt / 1e9,
                          "peak": PEAK_HBM_BYTES / 1e9, "unit": "GB/s",
                          "frac": dwork["bytes"] / dt / PEAK_HBM_BYTES,

@@ -245,6 +245,31 @@ int moe_grouped_ffn_products(const void* x_perm, int dtype, const int32_t* group
                              int products, void* stream);
 
 /*
+ * moe_grouped_ffn_combine -- moe_grouped_ffn followed by moe_combine, for calls
+ * in which no group holds more than 64 rows (a batch of at most 64 tokens; the
+ * MOE_FFN_SMALL_GROUPS statement): the expert outputs are combined inside the
+ * down product's fixed-order sum of its K chunks (the gate-weighted sum of
+ * Sec. II-A, the return trip of Sec. II-B), so y_perm is neither written nor
+ * read back and the combine needs no launch of its own:
+ *
+ *   y[t] = sum_{r ascending, token_row[t][r] >= 0} topk_gate[t][r] * y_perm[token_row[t][r]]
+ *          + y_shared[t]
+ *
+ * with y_perm[p] the bf16 value moe_grouped_ffn would store, summed in fp32 in
+ * the order moe_combine uses: bitwise moe_grouped_ffn + moe_combine.
+ * x_perm, group_offsets, n_groups, w13, w2, d, f, cap_rows and ws as for
+ * moe_grouped_ffn; token_row, topk_gate, y_shared (nullable), T, k and y as for
+ * moe_combine.  MOE_BF16 only (MOE_ERR_ARG otherwise).  Rows of a group that
+ * holds more than 64 rows are left out of y.  If y_shared comes from another
+ * stream, that stream must be joined before this call.
+ */
+int moe_grouped_ffn_combine(const void* x_perm, int dtype, const int32_t* group_offsets,
+                            int n_groups, const void* const* w13, const void* const* w2, int d,
+                            int f, int64_t cap_rows, const int32_t* token_row,
+                            const float* topk_gate, const void* y_shared, int64_t T, int k,
+                            void* y, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * moe_grouped_ffn_rows -- moe_grouped_ffn whose first product reads row p of
  * its input straight from the token rows, x[row_token[p]], instead of from a
  * packaged copy: the row map of the packaging step (Sec. II-B) is kept and the

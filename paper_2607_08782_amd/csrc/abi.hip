@@ -217,6 +217,24 @@ int moe_grouped_ffn_products(const void* x_perm, int dtype, const int32_t* group
                               y_perm, ws, (hipStream_t)stream, nullptr, 0, products);
 }
 
+int moe_grouped_ffn_combine(const void* x_perm, int dtype, const int32_t* group_offsets,
+                            int n_groups, const void* const* w13, const void* const* w2, int d,
+                            int f, int64_t cap_rows, const int32_t* token_row,
+                            const float* topk_gate, const void* y_shared, int64_t T, int k,
+                            void* y, void* ws, size_t ws_bytes, void* stream) {
+    if (dtype != MOE_BF16) return MOE_ERR_ARG;
+    if (T < 0 || k < 1 || k > MOE_MAX_K) return MOE_ERR_ARG;
+    if (T > 0 && (!token_row || !topk_gate || !y)) return MOE_ERR_ARG;
+    if (T > 0 && (!aligned16(y) || (y_shared && !aligned16(y_shared)))) return MOE_ERR_ARG;
+    const int st = ffn_check(x_perm, dtype, group_offsets, n_groups, w13, w2, d, f, cap_rows,
+                             T > 0 ? y : nullptr, ws, ws_bytes,
+                             MOE_FFN_GATE_UP | MOE_FFN_DOWN | MOE_FFN_SMALL_GROUPS);
+    if (st != MOE_OK) return st;
+    return launch_grouped_ffn_combine(x_perm, group_offsets, n_groups, w13, w2, d, f, cap_rows,
+                                      token_row, topk_gate, y_shared, T, k, y, ws,
+                                      (hipStream_t)stream);
+}
+
 int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int dtype,
                          const int32_t* group_offsets, int n_groups, const void* const* w13,
                          const void* const* w2, int d, int f, int64_t cap_rows, void* y_perm,

@@ -137,7 +137,15 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
                        const void* const* w13, const void* const* w2, int d, int f,
                        int64_t cap_rows, void* y_perm, void* ws, hipStream_t s,
                        const int32_t* a_rows = nullptr, int64_t a_total = 0,
-                       int products = MOE_FFN_GATE_UP | MOE_FFN_DOWN);
+                       int products = MOE_FFN_GATE_UP | MOE_FFN_DOWN,
+                       const void* combine = nullptr);
+// moe_grouped_ffn with every group streamed and the down product's chunk sum
+// writing the gate-weighted combine (bf16)
+int launch_grouped_ffn_combine(const void* x_perm, const int32_t* offsets, int n_groups,
+                               const void* const* w13, const void* const* w2, int d, int f,
+                               int64_t cap_rows, const int32_t* token_row, const float* gate,
+                               const void* y_shared, int64_t T, int k, void* y, void* ws,
+                               hipStream_t s);
 size_t grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_groups);
 
 int launch_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* gate,

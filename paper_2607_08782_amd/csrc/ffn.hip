@@ -765,6 +765,112 @@ __device__ __forceinline__ void stream_reduce(const StreamArgs& args, const Stre
     }
 }
 
+// The down product's chunk sum fused with the gate-weighted combine, for calls
+// in which every group is streamed (no group above SMALL_ROWS rows): one
+// thread per token and 4 output columns.  For each assignment r of token t, in
+// ascending r, the row's output is summed over the K chunks in chunk order and
+// rounded to bf16 (the value the chunk sum would store in y_perm), then added
+// with its gate by fmaf; the shared experts' output is added last and the sum
+// stored in bf16 -- the arithmetic of split_reduce_kernel followed by the
+// combine, so the outputs are the same bits, without y_perm being written and
+// read back or the combine's launch.
+struct CombineArgs {
+    const int32_t* token_row;            // [T][k]
+    const float* gate;                   // [T][k]
+    const bf16_t* y_shared;              // [T][d], nullable
+    bf16_t* y;                           // [T][d]
+    int64_t T;
+    int k;
+};
+
+template <int KM>
+__global__ __launch_bounds__(ST_THREADS) void stream_reduce_combine_kernel(StreamArgs args,
+                                                                           CombineArgs cb) {
+    __shared__ StreamPlan P;
+    make_stream_plan(args, P, ST_THREADS);
+    const int lim = args.limits != nullptr ? args.limits[args.product] : SMALL_ROWS;
+    const int S = P.S;
+    const int d = args.N;
+    const int chunks = d / 4;
+    const int64_t cstride = (int64_t)P.n_small * d;
+    const int64_t total = cb.T * chunks;
+    // CB chunks of every assignment are loaded together, KM * CB loads in flight
+    constexpr int CB = 32 / KM > 0 ? 32 / KM : 1;
+    for (int64_t i = (int64_t)blockIdx.x * ST_THREADS + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * ST_THREADS) {
+        const int64_t t = i / chunks;
+        const int c4 = (int)(i - t * chunks) * 4;
+        // the partial row of each assignment here, or none
+        int64_t off[KM];
+        float g[KM];
+        bool ok[KM];
+        int64_t first = -1;
+#pragma unroll
+        for (int r = 0; r < KM; ++r) {
+            const int rr = r < cb.k ? r : cb.k - 1;
+            const int32_t p = r < cb.k ? cb.token_row[t * cb.k + rr] : -1;
+            g[r] = cb.gate[t * cb.k + rr];
+            ok[r] = false;
+            off[r] = 0;
+            if (p >= 0) {
+                const int grp = last_le(P.off, args.n_groups, p);
+                // a group above the streaming limit has no partial rows (outside the contract)
+                ok[r] = P.off[grp + 1] - P.off[grp] <= lim;
+                off[r] = (int64_t)(P.qbase[grp] + p - P.off[grp]) * d + c4;
+            }
+            if (ok[r] && first < 0) first = off[r];
+        }
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        if (first >= 0) {
+            float4 x[KM];
+#pragma unroll
+            for (int r = 0; r < KM; ++r) x[r] = make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int c = 0; c < S; c += CB) {
+                float4 v[KM][CB];
+                // every load issued before the first add: an assignment not here
+                // reads the first one's row and a chunk past S the last chunk,
+                // both dropped below
+#pragma unroll
+                for (int r = 0; r < KM; ++r)
+#pragma unroll
+                    for (int j = 0; j < CB; ++j) {
+                        const int cc = c + j < S ? c + j : S - 1;
+                        v[r][j] = *(const float4*)(args.part + (ok[r] ? off[r] : first) + cc * cstride);
+                    }
+#pragma unroll
+                for (int r = 0; r < KM; ++r)
+#pragma unroll
+                    for (int j = 0; j < CB; ++j)
+                        if (c + j < S) {
+                            x[r].x += v[r][j].x; x[r].y += v[r][j].y;
+                            x[r].z += v[r][j].z; x[r].w += v[r][j].w;
+                        }
+            }
+            // each row's bf16 value, as y_perm would hold it, added with its gate in
+            // ascending r
+#pragma unroll
+            for (int r = 0; r < KM; ++r) {
+                if (!ok[r]) continue;
+                acc[0] = fmaf(g[r], bf16_to_f32(f32_to_bf16(x[r].x)), acc[0]);
+                acc[1] = fmaf(g[r], bf16_to_f32(f32_to_bf16(x[r].y)), acc[1]);
+                acc[2] = fmaf(g[r], bf16_to_f32(f32_to_bf16(x[r].z)), acc[2]);
+                acc[3] = fmaf(g[r], bf16_to_f32(f32_to_bf16(x[r].w)), acc[3]);
+            }
+        }
+        if (cb.y_shared) {
+            const uint2 w = *(const uint2*)(cb.y_shared + t * d + c4);
+            acc[0] += __uint_as_float(w.x << 16);
+            acc[1] += __uint_as_float(w.x & 0xffff0000u);
+            acc[2] += __uint_as_float(w.y << 16);
+            acc[3] += __uint_as_float(w.y & 0xffff0000u);
+        }
+        uint2 pk;
+        pk.x = pack_bf16x2(acc[0], acc[1]);
+        pk.y = pack_bf16x2(acc[2], acc[3]);
+        *(uint2*)(cb.y + t * d + c4) = pk;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // fp32 path: plain FMA loops, one thread per output element.
 // ---------------------------------------------------------------------------
@@ -863,7 +969,8 @@ size_t grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_gro
 int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, int n_groups,
                        const void* const* w13, const void* const* w2, int d, int f,
                        int64_t cap_rows, void* y_perm, void* ws, hipStream_t s,
-                       const int32_t* a_rows, int64_t a_total, int products) {
+                       const int32_t* a_rows, int64_t a_total, int products,
+                       const void* combine) {
     if (cap_rows == 0) return MOE_OK;
     const bool up = (products & MOE_FFN_GATE_UP) != 0, down = (products & MOE_FFN_DOWN) != 0;
     // every group within the streaming kernel's own limit: no tile, no split tile and
@@ -983,8 +1090,46 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s2.a_rows = nullptr;
     s2.product = 1;
     hipLaunchKernelGGL(stream_gemm_kernel<false>, dim3(sgrid), dim3(ST_THREADS), 0, s, s2);
-    hipLaunchKernelGGL(split_reduce_kernel<false>, dim3(rgrid), dim3(ST_THREADS), 0, s, s2, a2);
+    if (combine == nullptr) {
+        hipLaunchKernelGGL(split_reduce_kernel<false>, dim3(rgrid), dim3(ST_THREADS), 0, s, s2, a2);
+        return launch_status();
+    }
+    // the down product's chunk sum writes the combined output (every group streamed)
+    const CombineArgs& cb = *(const CombineArgs*)combine;
+    int64_t cgrid = ceil_div(cb.T * (d / 4), ST_THREADS);
+    if (cgrid > 4096) cgrid = 4096;
+    if (cgrid < 1) cgrid = 1;
+#define MOE_RC(KM)                                                                               \
+    hipLaunchKernelGGL(stream_reduce_combine_kernel<KM>, dim3((unsigned)cgrid), dim3(ST_THREADS), \
+                       0, s, s2, cb)
+    if (cb.k <= 2) MOE_RC(2);
+    else if (cb.k <= 4) MOE_RC(4);
+    else if (cb.k <= 8) MOE_RC(8);
+    else MOE_RC(MOE_MAX_K);
+#undef MOE_RC
     return launch_status();
+}
+
+int launch_grouped_ffn_combine(const void* x_perm, const int32_t* offsets, int n_groups,
+                               const void* const* w13, const void* const* w2, int d, int f,
+                               int64_t cap_rows, const int32_t* token_row, const float* gate,
+                               const void* y_shared, int64_t T, int k, void* y, void* ws,
+                               hipStream_t s) {
+    if (T == 0) return MOE_OK;
+    CombineArgs cb;
+    cb.token_row = token_row;
+    cb.gate = gate;
+    cb.y_shared = (const bf16_t*)y_shared;
+    cb.y = (bf16_t*)y;
+    cb.T = T;
+    cb.k = k;
+    if (cap_rows == 0) {
+        // no local row: y is the shared experts' output (or zero), as the combine gives
+        return launch_combine(nullptr, MOE_BF16, token_row, gate, y_shared, T, d, k, y, s);
+    }
+    return launch_grouped_ffn(x_perm, MOE_BF16, offsets, n_groups, w13, w2, d, f, cap_rows,
+                              nullptr, ws, s, nullptr, 0,
+                              MOE_FFN_GATE_UP | MOE_FFN_DOWN | MOE_FFN_SMALL_GROUPS, &cb);
 }
 
 }  // namespace moe

@@ -4,7 +4,8 @@
 torch) and enqueues, on the current stream:
     moe_route_topk -> moe_expert_histogram -> moe_permute
     -> moe_grouped_ffn (routed experts) -> moe_combine
-with no host synchronisation in between.  The shared experts' FFN
+with no host synchronisation in between (for batches of at most 64 tokens the
+last two are one call, moe_grouped_ffn_combine).  The shared experts' FFN
 (moe_grouped_ffn over every token), which does not depend on the routing,
 runs on a second stream forked from the current one and joined back before
 the combine, so it overlaps the short routing and packaging launches; the
@@ -48,7 +49,8 @@ class LayerShare:
                  placement: np.ndarray, dev: int, w13: Sequence[torch.Tensor],
                  w2: Sequence[torch.Tensor], shared=(), renorm: bool = True,
                  coact: bool = False, want_logits: bool = True, cap_rows: Optional[int] = None,
-                 gather_in_ffn: bool = False, overlap_shared: bool = True):
+                 gather_in_ffn: bool = False, overlap_shared: bool = True,
+                 fuse_combine: bool = True):
         self.device = X.device
         self.X = X
         self.Wr = Wr
@@ -114,6 +116,10 @@ class LayerShare:
         self.ffn_products = moe.MOE_FFN_GATE_UP | moe.MOE_FFN_DOWN
         if T <= 64:
             self.ffn_products |= moe.MOE_FFN_SMALL_GROUPS
+        # ... and the combine can run inside the down product's chunk sum
+        # (moe_grouped_ffn_combine: y_perm is not written)
+        self.fused_combine = (fuse_combine and T <= 64 and dt == torch.bfloat16
+                              and not gather_in_ffn and self.weights is not None)
 
     def set_placement(self, placement: np.ndarray, w13: Sequence[torch.Tensor],
                       w2: Sequence[torch.Tensor]):
@@ -161,6 +167,16 @@ class LayerShare:
         moe.moe_permute(self.X, self.topk_idx, self.topk_gate, self.counts, self.placement,
                         self.dev, E=self.E, cap_rows=self.cap_rows, out=self.perm, ws=self.ws_perm,
                         copy_rows=not self.gather_in_ffn)
+        if self.fused_combine:
+            if self._side is not None:
+                main.wait_event(self._join)
+            elif self.shared_weights is not None:
+                self._shared_ffn()
+            moe.moe_grouped_ffn_combine(self.perm["x_perm"], self.perm["group_offsets"],
+                                        self.weights, self.perm["token_row"], self.topk_gate,
+                                        self.y_shared, cap_rows=self.cap_rows, T=self.T, y=self.y,
+                                        ws=self.ws_ffn)
+            return self.y
         if self.weights is not None:
             if self.gather_in_ffn:
                 moe.moe_grouped_ffn_rows(self.X, self.perm["row_token"], self.perm["group_offsets"],

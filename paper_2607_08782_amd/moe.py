@@ -28,7 +28,8 @@ MOE_PERMUTE_NOALLOC_MAX_WS = 4 << 20
 
 EXPORTS = ("moe_status_string", "moe_route_topk", "moe_route_topk_ws_bytes",
            "moe_expert_histogram", "moe_permute_ws_bytes",
-           "moe_permute", "moe_permute_noalloc", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_grouped_ffn_products", "moe_grouped_ffn_rows",
+           "moe_permute", "moe_permute_noalloc", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_grouped_ffn_products", "moe_grouped_ffn_combine",
+           "moe_grouped_ffn_rows",
            "moe_combine",
            "moe_quantize_e4m3", "moe_route_topk_e4m3")
 
@@ -71,6 +72,8 @@ def load_library(path: str = LIB_PATH):
     lib.moe_grouped_ffn.restype = I
     lib.moe_grouped_ffn_products.argtypes = [P, I, P, I, P, P, I, I, L, P, P, S, I, P]
     lib.moe_grouped_ffn_products.restype = I
+    lib.moe_grouped_ffn_combine.argtypes = [P, I, P, I, P, P, I, I, L, P, P, P, L, I, P, P, S, P]
+    lib.moe_grouped_ffn_combine.restype = I
     lib.moe_grouped_ffn_rows.argtypes = [P, L, P, I, P, I, P, P, I, I, L, P, P, S, P]
     lib.moe_grouped_ffn_rows.restype = I
     lib.moe_combine.argtypes = [P, I, P, P, P, L, I, I, P, P]
@@ -350,6 +353,34 @@ def moe_grouped_ffn(x_perm: torch.Tensor, group_offsets: torch.Tensor, weights: 
         _check("moe_grouped_ffn_products",
                lib.moe_grouped_ffn_products(*args, products, _stream(stream)))
     return y_perm
+
+
+def moe_grouped_ffn_combine(x_perm: torch.Tensor, group_offsets: torch.Tensor,
+                            weights: WeightTable, token_row: torch.Tensor, topk_gate: torch.Tensor,
+                            y_shared: Optional[torch.Tensor], *, cap_rows: int, T: int,
+                            y: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                            stream=None) -> torch.Tensor:
+    """Grouped FFN and weighted combine in one call (every group at most 64 rows).
+    Returns y [T, d]."""
+    lib = load_library()
+    d, f = weights.d, weights.f
+    dtype = _dtype_code(x_perm)
+    if x_perm.dtype != weights.dtype or x_perm.shape[1] != d:
+        raise ValueError("x_perm must be [rows, d] of the weights' dtype")
+    k = token_row.shape[1]
+    if y is None:
+        y = _empty((max(T, 1), d), x_perm.dtype, x_perm.device)
+    if ws is None:
+        ws = workspace(moe_grouped_ffn_ws_bytes(dtype, cap_rows, d, f, len(weights)), x_perm.device)
+    st = lib.moe_grouped_ffn_combine(
+        _dev(x_perm, "x_perm"), dtype, _dev(group_offsets, "group_offsets", torch.int32),
+        len(weights), ctypes.cast(weights.p13, ctypes.c_void_p),
+        ctypes.cast(weights.p2, ctypes.c_void_p), d, f, cap_rows,
+        _dev(token_row, "token_row", torch.int32), _dev(topk_gate, "topk_gate", torch.float32),
+        _dev(y_shared, "y_shared", x_perm.dtype), T, k, _dev(y, "y", x_perm.dtype),
+        _dev(ws, "ws"), ws.numel(), _stream(stream))
+    _check("moe_grouped_ffn_combine", st)
+    return y
 
 
 def moe_grouped_ffn_rows(x: torch.Tensor, row_token: torch.Tensor, group_offsets: torch.Tensor,

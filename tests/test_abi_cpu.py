@@ -169,6 +169,24 @@ def test_grouped_ffn_products_validation(lib):
     assert call(products=2, ws_bytes=10) == moe.MOE_ERR_SHAPE
 
 
+def test_grouped_ffn_combine_validation(lib):
+    f = lib.moe_grouped_ffn_combine
+    arr = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    P = ctypes.cast(arr, ctypes.c_void_p)
+
+    def call(dtype=1, T=8, k=2, y=FAKE, tr=FAKE, d=128, f_=64):
+        return f(FAKE, dtype, FAKE, 2, P, P, d, f_, 16, tr, FAKE, None, T, k, y,
+                 ctypes.c_void_p(0x100000), 1 << 30, None)
+    assert call(dtype=0) == moe.MOE_ERR_ARG                  # bf16 only
+    assert call(k=0) == moe.MOE_ERR_ARG
+    assert call(k=17) == moe.MOE_ERR_ARG
+    assert call(T=-1) == moe.MOE_ERR_ARG
+    assert call(y=None) == moe.MOE_ERR_ARG
+    assert call(tr=None) == moe.MOE_ERR_ARG
+    assert call(y=ctypes.c_void_p(0x1008)) == moe.MOE_ERR_ARG
+    assert call(d=100) == moe.MOE_ERR_SHAPE
+
+
 def test_grouped_ffn_validation(lib):
     f = lib.moe_grouped_ffn
     arr = (ctypes.c_void_p * 2)(0x1000, 0x2000)

@@ -212,7 +212,7 @@ def _share(cfg, T, logits=None, placement=None, dev=0):
     local = [int(e) for e in np.nonzero(pl[:, dev])[0]]
     ws = [synth.expert_weights(cfg, e, 1, "cuda") for e in local]
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, pl, dev, [a for a, _ in ws],
-                       [b for _, b in ws], shared=inp.shared)
+                       [b for _, b in ws], shared=inp.shared, fuse_combine=False)
     return inp, share
 
 
@@ -348,7 +348,8 @@ def _both_paths(cfg, T, logits=None, seed=1):
     outs = []
     for gather in (False, True):
         share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
-                           shared=inp.shared, coact=cfg.coact, gather_in_ffn=gather)
+                           shared=inp.shared, coact=cfg.coact, gather_in_ffn=gather,
+                           fuse_combine=False)
         share.run(logits_in=logits)
         torch.cuda.synchronize()
         N = int(share.perm["group_offsets"][-1])
@@ -425,7 +426,7 @@ def test_ffn_products_one_at_a_time_equal_the_whole_call(name, regime):
     say("[products]", name, regime, "T=%d" % T)
     inp = synth.make_layer(cfg, T, seed=2, device="cuda")
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
-                       shared=inp.shared, coact=cfg.coact)
+                       shared=inp.shared, coact=cfg.coact, fuse_combine=False)
     share.run()
     torch.cuda.synchronize()
     N = int(share.perm["group_offsets"][-1])
@@ -449,7 +450,7 @@ def test_small_groups_hint_leaves_the_outputs_bitwise_unchanged(name, regime):
     say("[small groups]", name, regime, "T=%d" % T)
     inp = synth.make_layer(cfg, T, seed=3, device="cuda")
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
-                       shared=inp.shared, coact=cfg.coact)
+                       shared=inp.shared, coact=cfg.coact, fuse_combine=False)
     assert share.ffn_products & moe.MOE_FFN_SMALL_GROUPS
     share.run()
     torch.cuda.synchronize()
@@ -460,6 +461,42 @@ def test_small_groups_hint_leaves_the_outputs_bitwise_unchanged(name, regime):
                         cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
     torch.cuda.synchronize()
     assert torch.equal(share.y_perm[:N], hinted)
+
+
+FUSED = [("mixtral_8x7b", "decode", None), ("qwen3_30b_a3b", "decode", None),
+         ("shared_T50", "batch", synth.custom_config(d=256, E=16, k=4, f=256, shared_f=(128, 64),
+                                                     G=3, replicas=2, zipf=1.2, T=50)),
+         ("T1", "batch", synth.custom_config(d=128, E=8, k=2, f=128, G=2, T=1)),
+         ("k16", "batch", synth.custom_config(d=128, E=64, k=16, f=64, G=3, replicas=2, zipf=1.1,
+                                              T=60))]
+
+
+@pytest.mark.parametrize("name,regime,custom", FUSED)
+def test_fused_ffn_combine_is_bitwise_the_ffn_then_the_combine(name, regime, custom):
+    """moe_grouped_ffn_combine (the down product's chunk sum writing the gate-weighted
+    combine, y_perm never written) gives the bits of moe_grouped_ffn + moe_combine,
+    with shared experts (joined from their stream), one token, and k = 16."""
+    cfg = custom if custom is not None else synth.CONFIGS[name]
+    T = cfg.T(regime)
+    say("[fused]", name, regime, "T=%d" % T)
+    inp = synth.make_layer(cfg, T, seed=5, device="cuda")
+    fused, plain = (LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                               shared=inp.shared, coact=cfg.coact, fuse_combine=fz)
+                    for fz in (True, False))
+    assert fused.fused_combine and not plain.fused_combine
+    fused.y.fill_(7.0)
+    fused.run()
+    plain.run()
+    torch.cuda.synchronize()
+    assert torch.equal(fused.y[:T], plain.y[:T])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fused.run()
+    for _ in range(3):
+        fused.y.fill_(7.0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(fused.y[:T], plain.y[:T])
 
 
 def test_very_long_batch_routing_and_packaging_every_element():
