@@ -101,18 +101,24 @@ def rotated_shares(cfg, inp, **kw):
 
 
 def ffn_call(share, products=None):
-    """The routed experts' FFN call as LayerShare.run makes it: moe_grouped_ffn (or
-    the given products of it), or moe_grouped_ffn_combine when the share fuses the
-    combine into it."""
-    if products is None and share.fused_combine:
-        return lambda: moe.moe_grouped_ffn_combine(
-            share.perm["x_perm"], share.perm["group_offsets"], share.weights,
-            share.perm["token_row"], share.topk_gate, share.y_shared, cap_rows=share.cap_rows,
-            T=share.T, y=share.y, ws=share.ws_ffn)
-    products = share.ffn_products if products is None else products
+    """The routed experts' FFN call as LayerShare.run makes it (LayerShare.routed_ffn:
+    moe_grouped_ffn, or moe_grouped_ffn_combine when the share fuses the combine), or
+    the given products of moe_grouped_ffn alone."""
+    if products is None:
+        return share.routed_ffn
     return lambda: moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"],
                                        share.weights, cap_rows=share.cap_rows, y_perm=share.y_perm,
                                        ws=share.ws_ffn, products=products)
+
+
+def ffn_label(share):
+    """What the routed experts' FFN call of `share` launches."""
+    if share.fused_combine:
+        return ("moe_grouped_ffn_combine call (weight-streaming launches, the combine in the "
+                "down product's chunk sum)")
+    if share.ffn_products & moe.MOE_FFN_SMALL_GROUPS:
+        return "moe_grouped_ffn call (weight-streaming launches, chunk sums)"
+    return "moe_grouped_ffn call (gate/up and down tiled GEMMs, streaming launches, chunk sums)"
 
 
 def ffn_work(share, cfg):
@@ -143,8 +149,7 @@ def phase_calls(share):
                         ws=share.ws_perm)
 
     def grouped_ffn():
-        if share.weights is not None:
-            ffn_call(share)()
+        share.routed_ffn()
 
     def shared_ffn():
         if share.shared_weights is not None:
@@ -409,8 +414,7 @@ def main():
     ms = m["step_ms"]
     t_call = m["ffn_ms"] * 1e-3
     workload = "%s:%s" % (name, regime)
-    call = {"kernel": "moe_grouped_ffn call (gate/up and down tiled GEMMs, streaming launches, "
-                      "chunk sums)", "avg_launch_us": t_call * 1e6}
+    call = {"kernel": ffn_label(shares[0]), "avg_launch_us": t_call * 1e6}
     if prefill:
         t_gu = m["gate_up_ms"] * 1e-3
         achieved = work["gate_up_flops"] / t_gu
@@ -427,7 +431,7 @@ def main():
                     algorithmic_flops_per_call=work["flops"])
     else:
         achieved = work["bytes"] / t_call
-        roofline = {"kernel": "moe_grouped_ffn call (weight-streaming launches)", "bound": "hbm",
+        roofline = {"kernel": ffn_label(shares[0]), "bound": "hbm",
                     "achieved": achieved / 1e9, "peak": PEAK_HBM_BYTES / 1e9, "unit": "GB/s",
                     "frac": achieved / PEAK_HBM_BYTES, "traffic": measured_traffic(workload),
                     "traffic_unit": "bytes per launch", "algorithmic_bytes_per_launch": work["bytes"],
@@ -477,10 +481,7 @@ def main():
             "ms_per_step": dm["step_ms"], "eager_ms_per_step": dm["eager_ms"],
             "rows_here": dwork["N"], "active_experts": dwork["active"],
             "weight_copies": dm["weight_copies"],
-            "roofline": {"kernel": "moe_grouped_ffn_combine call (weight-streaming launches, "
-                                   "the combine in the down product's chunk sum)"
-                                   if dshares[0].fused_combine else
-                                   "moe_grouped_ffn call (weight-streaming launches)",
+            "roofline": {"kernel": ffn_label(dshares[0]),
                          "bound": "hbm", "achieved": dwork["bytes"] / dt / 1e9,
                          "peak": PEAK_HBM_BYTES / 1e9, "unit": "GB/s",
                          "frac": dwork["bytes"] / dt / PEAK_HBM_BYTES,

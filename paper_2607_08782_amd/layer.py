@@ -152,6 +152,27 @@ class LayerShare:
                             y_perm=self.y_shared, ws=self.ws_shared, stream=stream,
                             products=self.ffn_products)
 
+    def routed_ffn(self):
+        """Enqueue the routed experts' FFN call as `run` makes it: moe_grouped_ffn (or
+        moe_grouped_ffn_rows) into y_perm, or, when the share fuses the combine,
+        moe_grouped_ffn_combine into y (which then reads y_shared: the shared experts'
+        call must have completed on this stream)."""
+        if self.weights is None:
+            return
+        if self.fused_combine:
+            moe.moe_grouped_ffn_combine(self.perm["x_perm"], self.perm["group_offsets"],
+                                        self.weights, self.perm["token_row"], self.topk_gate,
+                                        self.y_shared, cap_rows=self.cap_rows, T=self.T, y=self.y,
+                                        ws=self.ws_ffn)
+        elif self.gather_in_ffn:
+            moe.moe_grouped_ffn_rows(self.X, self.perm["row_token"], self.perm["group_offsets"],
+                                     self.weights, cap_rows=self.cap_rows, y_perm=self.y_perm,
+                                     ws=self.ws_ffn)
+        else:
+            moe.moe_grouped_ffn(self.perm["x_perm"], self.perm["group_offsets"], self.weights,
+                                cap_rows=self.cap_rows, y_perm=self.y_perm, ws=self.ws_ffn,
+                                products=self.ffn_products)
+
     def run(self, logits_in: Optional[torch.Tensor] = None) -> torch.Tensor:
         """Enqueue the whole share after the current stream's earlier work; returns y
         [T, d], complete on the current stream (the shared experts' branch, if
@@ -172,20 +193,9 @@ class LayerShare:
                 main.wait_event(self._join)
             elif self.shared_weights is not None:
                 self._shared_ffn()
-            moe.moe_grouped_ffn_combine(self.perm["x_perm"], self.perm["group_offsets"],
-                                        self.weights, self.perm["token_row"], self.topk_gate,
-                                        self.y_shared, cap_rows=self.cap_rows, T=self.T, y=self.y,
-                                        ws=self.ws_ffn)
+            self.routed_ffn()
             return self.y
-        if self.weights is not None:
-            if self.gather_in_ffn:
-                moe.moe_grouped_ffn_rows(self.X, self.perm["row_token"], self.perm["group_offsets"],
-                                         self.weights, cap_rows=self.cap_rows, y_perm=self.y_perm,
-                                         ws=self.ws_ffn)
-            else:
-                moe.moe_grouped_ffn(self.perm["x_perm"], self.perm["group_offsets"], self.weights,
-                                    cap_rows=self.cap_rows, y_perm=self.y_perm, ws=self.ws_ffn,
-                                    products=self.ffn_products)
+        self.routed_ffn()
         if self._side is not None:
             main.wait_event(self._join)
         elif self.shared_weights is not None:

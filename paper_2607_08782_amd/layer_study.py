@@ -5,10 +5,11 @@ Qwen3-30B-A3B-shaped shares; prefill and decode batches) and each seed 0-4:
 synthetic inputs of that shape (seeded normal hidden states and weights, Zipf
 popularity bias, the benchmark placement), the five calls captured in one HIP
 graph, and the step timed over graph replays (also with the row copy x_perm
-elided: the expert FFN reading token rows through the row map); the grouped
-FFN call is timed the same way on its own.  Reported: tokens/s, the FFN's rate against the bf16 MFMA
+elided: the expert FFN reading token rows through the row map); the routed
+experts' FFN call is timed the same way on its own (for batches of at most 64
+tokens that call also writes the combine).  Reported: tokens/s, the FFN's rate against the bf16 MFMA
 peak (6 d f N flop) and against HBM (weights of the active local experts read
-once plus x_perm in and y_perm out), mean and spread over the seeds.
+once plus x_perm in and y_perm, or the combined y, out), mean and spread over the seeds.
 
 Cache hygiene: when the local expert weights total less than 1 GB (they would
 otherwise stay in the 256 MB last-level cache between replays), the replays
@@ -87,15 +88,14 @@ def measure(name, regime, seed, steps):
     step_graphs = [_graph(s.run) for s in shares]
     gather_graphs = [_graph(s.run) for s in gshares]
 
-    def ffn(s):
-        return lambda: moe.moe_grouped_ffn(s.perm["x_perm"], s.perm["group_offsets"], s.weights,
-                                           cap_rows=s.cap_rows, y_perm=s.y_perm, ws=s.ws_ffn)
-    ffn_graphs = [_graph(ffn(s)) for s in shares]
+    ffn_graphs = [_graph(s.routed_ffn) for s in shares]
     step_us = _time(step_graphs, steps)
     gather_us = _time(gather_graphs, steps)
     ffn_us = _time(ffn_graphs, steps)
     flops = 6.0 * cfg.d * cfg.f * N
-    fbytes = active * 3.0 * cfg.d * cfg.f * 2 + 2.0 * N * cfg.d * 2
+    # out: y_perm, or, when the call combines, y with the row maps and gates it reads
+    out_bytes = (T * cfg.d * 2 + T * cfg.k * 8.0) if s0.fused_combine else N * cfg.d * 2
+    fbytes = active * 3.0 * cfg.d * cfg.f * 2 + N * cfg.d * 2 + out_bytes
     out = {"T": T, "N": N, "active": active, "slots": len(sizes), "copies": copies,
            "step_us": step_us, "tok_s": T / (step_us * 1e-6), "ffn_us": ffn_us,
            "gather_us": gather_us,
@@ -136,14 +136,16 @@ def main(argv=None):
     lines = ["# The layer share at every model shape and regime", "",
              "Synthetic seeded inputs of each shape (normal hidden states, N(0, 0.02) weights, Zipf",
              "popularity bias, the benchmark placement with this GPU = device 0).  Step = the five",
-             "calls as one HIP graph replay; FFN = the `moe_grouped_ffn` call of the routed experts",
-             "replayed on its own.  Mean (± population std) over seeds 0-%d; %d timed replays per"
+             "calls as one HIP graph replay; FFN = the routed experts' FFN call as the step makes it",
+             "(`moe_grouped_ffn`; `moe_grouped_ffn_combine` for batches of at most 64 tokens, which",
+             "also writes the combined output) replayed on its own.  Mean (± population std) over seeds 0-%d; %d timed replays per"
              % (args.seeds - 1, args.steps),
              "seed for prefill-sized batches, %d for decode.  FFN rate against the bf16 MFMA peak"
              % (args.steps * 10),
              "(2.5 PFLOP/s, algorithmic 6·d·f·N flop) and against HBM (8 TB/s, algorithmic bytes: the",
-             "active local experts' weights once, x_perm in, y_perm out).  Weight copies: replays",
-             "cycle through this many copies of the local expert weights (≥ 1 GB touched).",
+             "active local experts' weights once, x_perm in, y_perm or the combined y out).  Weight",
+             "copies: replays cycle through this many copies of the local expert weights (≥ 1 GB",
+             "touched).",
              "Gathered step: the same share with the row copy x_perm elided (moe_permute writes the",
              "row maps only and moe_grouped_ffn_rows reads the token rows through row_token;",
              "bitwise the same output).", "",

@@ -30,11 +30,20 @@ import json
 import os
 
 FFN_SOURCE = "paper_2607_08782_amd/csrc/ffn.hip"
-# kernels of one moe_grouped_ffn call and their launches per call (the streaming
-# kernel runs once per product)
+# kernels of one routed-expert FFN call and their launches per call (the streaming
+# kernel runs once per product; moe_grouped_ffn_combine ends with the combining
+# chunk sum in place of split_reduce_kernel<false>)
 FFN_CALL = {"grouped_gemm_kernel<true, false>": 1, "grouped_gemm_kernel<false, false>": 1,
             "stream_gemm_kernel<false>": 2, "split_reduce_kernel<true>": 1,
             "split_reduce_kernel<false>": 1}
+FFN_CALL_PREFIX = {"stream_reduce_combine_kernel<": 1}
+
+
+def per_call(kernel):
+    """Launches of `kernel` in one routed-expert FFN call (0: not one of its kernels)."""
+    if kernel in FFN_CALL:
+        return FFN_CALL[kernel]
+    return next((n for p, n in FFN_CALL_PREFIX.items() if kernel.startswith(p)), 0)
 COPY_KERNEL = "neg_kernel"     # torch.neg's elementwise kernel carries this in its name
 
 
@@ -107,9 +116,9 @@ def traffic(workload, fetch_csv, write_csv, copy_mib, out, repo="."):
         for n, v in disp:
             per[short(n)].append(v * 1024.0 * factor)
         for k, v in per.items():
-            if k in FFN_CALL:
+            if per_call(k):
                 w["kernels"].setdefault(k, {})[key] = _mean(v)
-                w["call"][key] += _mean(v) * FFN_CALL[k]
+                w["call"][key] += _mean(v) * per_call(k)
     res["workloads"][workload] = w
     res.setdefault("commands", {})[workload] = [
         "rocprofv3 --pmc %s --output-format csv -d gpurun_out/pmc -o %s -- python -u bench.py "
