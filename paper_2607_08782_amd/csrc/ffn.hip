@@ -11,9 +11,13 @@
 //
 // Kernel shape (gfx950, wave64):
 //   workgroup 512 threads = 8 waves (4 x 2, two per SIMD), macro tile 256 rows
-//   x 256 weight rows, K step 64, LDS double buffer (2 x 72 KiB), wave tile
-//   64 x 128 on v_mfma_f32_32x32x16_bf16 (2 x 4 accumulator tiles), fragment
-//   reads software-pipelined against the MFMAs.
+//   x 256 weight rows, K step 64, LDS double buffer (2 x 64 KiB, 128-byte rows
+//   with XOR-swizzled 16-byte chunks), wave tile 64 x 128 on
+//   v_mfma_f32_16x16x32_bf16 (4 x 8 accumulator tiles), fragment reads
+//   software-pipelined against the MFMAs.  Under sustained load the part runs
+//   at its board power limit, so the clock follows the energy spent per flop:
+//   16x16x32 moves half the accumulator bytes per flop of 32x32x16 and runs
+//   these loops at a higher clock.
 //   The grid is persistent (one workgroup per CU).  Tiles are ordered
 //   (group, n-tile, m-tile) and cut into eight contiguous chunks, one per XCD
 //   (workgroups are dispatched round-robin over the XCDs), so the workgroups
@@ -28,14 +32,18 @@ constexpr int BM = 256;          // rows per tile
 constexpr int BNW = 256;         // weight rows per tile
 constexpr int BK = 64;           // K per stage
 constexpr int LDK = BK + 8;      // LDS row stride in elements (144 B: conflict-free reads)
+constexpr int TLDK = BK;         // tiled kernel: 128-byte rows, 16-byte chunks XOR-swizzled
 constexpr int WAVES_M = 4, WAVES_N = 2;
 constexpr int GEMM_THREADS = WAVES_M * WAVES_N * 64;
-constexpr int MS = BM / WAVES_M / 32;              // 32-row accumulator tiles per wave
-constexpr int NS = BNW / WAVES_N / 32;             // 32-column accumulator tiles per wave
+constexpr int MS = BM / WAVES_M / 16;              // 16-row accumulator tiles per wave
+constexpr int NS = BNW / WAVES_N / 16;             // 16-column accumulator tiles per wave
+constexpr int NH = NS / 2;                         // column tiles per half sub-step
 constexpr int ROWS_PER_PASS = GEMM_THREADS / 8;    // rows one pass of 16-byte loads covers
 constexpr int A_PER = BM / ROWS_PER_PASS;          // 16-byte loads per thread per stage (A)
 constexpr int B_PER = BNW / ROWS_PER_PASS;         // (B)
 constexpr int NUM_XCD = 8;
+// instruction classes of __builtin_amdgcn_sched_group_barrier
+constexpr int SG_MFMA = 0x008, SG_VMEM_READ = 0x020, SG_DS_READ = 0x100, SG_DS_WRITE = 0x200;
 constexpr uint32_t RSRC_WORD3 = 0x00020000;        // raw buffer: 32-bit data format
 constexpr int A_OOB = 0x7fffff00;                  // offset past any descriptor: reads zero
 
@@ -119,9 +127,9 @@ template <bool SWIGLU>
 __device__ __forceinline__ int b_sub_row(int wn, int jj) {
     if (SWIGLU) {
         constexpr int HW = BNW / 2 / WAVES_N;
-        return jj < NS / 2 ? wn * HW + jj * 32 : BNW / 2 + wn * HW + (jj - NS / 2) * 32;
+        return jj < NS / 2 ? wn * HW + jj * 16 : BNW / 2 + wn * HW + (jj - NS / 2) * 16;
     }
-    return wn * (BNW / WAVES_N) + jj * 32;
+    return wn * (BNW / WAVES_N) + jj * 16;
 }
 
 __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
@@ -177,8 +185,8 @@ __device__ __forceinline__ void small_limits(const int* s_off, int n_groups, int
 // the packaged copy of them is never materialised).
 template <bool SWIGLU, bool GATHER = false>
 __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs args) {
-    __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LDK];
-    __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BNW * LDK];
+    __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * TLDK];
+    __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BNW * TLDK];
     __shared__ int s_off[MOE_MAX_GROUPS + 1];
     __shared__ int s_tstart[MOE_MAX_GROUPS + 1];
     __shared__ int s_cur[4];
@@ -227,8 +235,6 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
     const int kc = (tid & 7) * 8;
     const int voff = ((tid >> 3) * K + kc) * 2;
     const int vstep = ROWS_PER_PASS * K * 2;
-    const int frag_col = (lane >> 5) * 32;
-    const int frag_row = lane & 31;
 
     for (int i = widx; i < n_mine; i += nper) {
         // whole tile, or unit u = (split tile, K chunk)
@@ -295,78 +301,125 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
                     rb[i] = buffer_load16(brsrc_lo, voff + i * vstep, so);
             }
         };
+        // 16-byte chunk c of LDS row r sits at chunk c ^ (r & 7): conflict-free for the
+        // stage stores (8 lanes per row) and for the 16-row fragment reads
+        const int sc = ((tid & 7) ^ ((tid >> 3) & 7)) * 8;
         auto sstore = [&](int buf) {
 #pragma unroll
             for (int i = 0; i < A_PER; ++i)
-                *(uint4*)&As[buf][((tid >> 3) + ROWS_PER_PASS * i) * LDK + kc] = ra[i];
+                *(uint4*)&As[buf][((tid >> 3) + ROWS_PER_PASS * i) * TLDK + sc] = ra[i];
 #pragma unroll
             for (int i = 0; i < B_PER; ++i)
-                *(uint4*)&Bs[buf][((tid >> 3) + ROWS_PER_PASS * i) * LDK + kc] = rb[i];
+                *(uint4*)&Bs[buf][((tid >> 3) + ROWS_PER_PASS * i) * TLDK + sc] = rb[i];
         };
 
-        f32x16 acc[MS][NS];
+        f32x4 acc[MS][NS];
 #pragma unroll
         for (int mi = 0; mi < MS; ++mi)
 #pragma unroll
             for (int jj = 0; jj < NS; ++jj)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) acc[mi][jj][r] = 0.f;
+                for (int r = 0; r < 4; ++r) acc[mi][jj][r] = 0.f;
 
-        const bf16_t* a_lds0 = &As[0][(wm * (BM / WAVES_M) + frag_row) * LDK + frag_col];
-        const bf16_t* b_lds0 = &Bs[0][frag_row * LDK + frag_col];
-        bf16x8 fa0[MS], fb0[NS], fa1[MS], fb1[NS];
-        auto read = [&](int buf, int kk, bf16x8* fa, bf16x8* fb) {
+        // v_mfma_f32_16x16x32_bf16 fragments: lane l holds row l % 16 of a 16-row
+        // block and the 8 K elements 8 (l / 16) .. of a 32-wide sub-step, for A and
+        // B alike, so every product sums over the same K
+        const int frow = lane & 15;
+        const int fsw = lane & 7;                         // the swizzle of rows frow (+ 16 m)
+        const int fc0 = ((lane >> 4) ^ fsw) * 8, fc1 = ((4 + (lane >> 4)) ^ fsw) * 8;
+        const bf16_t* a_lds0 = &As[0][(wm * (BM / WAVES_M) + frow) * TLDK];
+        const bf16_t* b_lds0 = &Bs[0][frow * TLDK];
+        // a 32-wide sub-step q runs as two halves (column tiles 0..NH-1, NH..NS-1);
+        // the fragments of the next half are read while the current half multiplies
+        bf16x8 fa0[MS], fa1[MS], fb0[NH], fb1[NH];
+        auto read_a = [&](int buf, int q, bf16x8* fa) {
 #pragma unroll
             for (int mi = 0; mi < MS; ++mi)
-                fa[mi] = *(const bf16x8*)(a_lds0 + buf * BM * LDK + mi * 32 * LDK + kk * 8);
-#pragma unroll
-            for (int jj = 0; jj < NS; ++jj)
-                fb[jj] = *(const bf16x8*)(b_lds0 + buf * BNW * LDK + b_sub_row<SWIGLU>(wn, jj) * LDK +
-                                          kk * 8);
+                fa[mi] = *(const bf16x8*)(a_lds0 + buf * BM * TLDK + mi * 16 * TLDK + (q ? fc1 : fc0));
         };
-        auto mfma = [&](const bf16x8* fa, const bf16x8* fb) {
+        auto read_b = [&](int buf, int q, int h, bf16x8* fb) {
+#pragma unroll
+            for (int j = 0; j < NH; ++j)
+                fb[j] = *(const bf16x8*)(b_lds0 + buf * BNW * TLDK +
+                                         b_sub_row<SWIGLU>(wn, h * NH + j) * TLDK + (q ? fc1 : fc0));
+        };
+        auto mfma = [&](const bf16x8* fa, const bf16x8* fb, int h) {
 #pragma unroll
             for (int mi = 0; mi < MS; ++mi)
 #pragma unroll
-                for (int jj = 0; jj < NS; ++jj)
-                    acc[mi][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mi], fb[jj],
-                                                                          acc[mi][jj], 0, 0, 0);
+                for (int j = 0; j < NH; ++j)
+                    acc[mi][h * NH + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        fa[mi], fb[j], acc[mi][h * NH + j], 0, 0, 0);
         };
 
-        // The K permutation inside a stage (lane half h, sub-step kk -> K offset
-        // h*32 + kk*8) is the same for A and B, so the products sum over all K.
         gload(kt0);
         sstore(0);
         gload(kt0 + (nsteps > 1 ? 1 : 0));
         __syncthreads();
-        read(0, 0, fa0, fb0);
+        read_a(0, 0, fa0);
+        read_b(0, 0, 0, fb0);
         // Every step but the last runs one straight path, so the MFMAs after the
         // barrier (on fragments read before it) issue without waiting for the
         // next stage's reads; the last step is peeled off below.
         for (int t = 0; t + 1 < nsteps; ++t) {
             const int buf = t & 1;
-            __builtin_amdgcn_iglp_opt(1);
-            read(buf, 1, fa1, fb1);
-            mfma(fa0, fb0);
-            read(buf, 2, fa0, fb0);
-            mfma(fa1, fb1);
-            read(buf, 3, fa1, fb1);
-            mfma(fa0, fb0);
+            read_b(buf, 0, 1, fb1);
+            mfma(fa0, fb0, 0);
+            read_a(buf, 1, fa1);
+            read_b(buf, 1, 0, fb0);
+            mfma(fa0, fb1, 1);
+            read_b(buf, 1, 1, fb1);
+            mfma(fa1, fb0, 0);
             sstore(buf ^ 1);
+            // issue order up to the barrier: each half's fragment reads at the head of
+            // the MFMA batch before the one that uses them, then the stage stores
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(SG_MFMA, 12, 0);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(SG_MFMA, 8, 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(SG_MFMA, 12, 0);
+            __builtin_amdgcn_sched_group_barrier(SG_DS_WRITE, 8, 0);
             __syncthreads();
             gload(kt0 + (t + 2 < nsteps ? t + 2 : nsteps - 1));
-            read(buf ^ 1, 0, fa0, fb0);
-            mfma(fa1, fb1);
+            read_a(buf ^ 1, 0, fa0);
+            read_b(buf ^ 1, 0, 0, fb0);
+            mfma(fa1, fb1, 1);
+            // after the barrier: the next stage's first fragment reads, then its
+            // global loads, each between MFMAs of the last half
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+            }
         }
         {
             const int buf = (nsteps - 1) & 1;
-            read(buf, 1, fa1, fb1);
-            mfma(fa0, fb0);
-            read(buf, 2, fa0, fb0);
-            mfma(fa1, fb1);
-            read(buf, 3, fa1, fb1);
-            mfma(fa0, fb0);
-            mfma(fa1, fb1);
+            read_b(buf, 0, 1, fb1);
+            mfma(fa0, fb0, 0);
+            read_a(buf, 1, fa1);
+            read_b(buf, 1, 0, fb0);
+            mfma(fa0, fb1, 1);
+            read_b(buf, 1, 1, fb1);
+            mfma(fa1, fb0, 0);
+            mfma(fa1, fb1, 1);
         }
         __syncthreads();
 
@@ -375,45 +428,43 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
             // tile]; rows past the group fall outside the descriptor and are dropped
             const __amdgpu_buffer_rsrc_t prsrc = __builtin_amdgcn_make_buffer_rsrc(
                 (void*)(args.part + (int64_t)u * BM * BNW), (short)0, rows_valid * BNW * 4, RSRC_WORD3);
-            const int lbase = ((wm * (BM / WAVES_M) + (lane >> 5) * 4) * BNW +
-                               b_sub_row<SWIGLU>(wn, 0) + (lane & 31)) * 4;
+            const int lbase = ((wm * (BM / WAVES_M) + (lane >> 4) * 4) * BNW +
+                               b_sub_row<SWIGLU>(wn, 0) + (lane & 15)) * 4;
 #pragma unroll
             for (int mi = 0; mi < MS; ++mi)
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
+                for (int r = 0; r < 4; ++r)
 #pragma unroll
                     for (int jj = 0; jj < NS; ++jj) {
-                        const int off = ((mi * 32 + (r >> 2) * 8 + (r & 3)) * BNW +
-                                         b_sub_row<SWIGLU>(0, jj)) * 4;
+                        const int off = ((mi * 16 + r) * BNW + b_sub_row<SWIGLU>(0, jj)) * 4;
                         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[mi][jj][r]), prsrc,
                                                               lbase, off, 0);
                     }
             continue;
         }
 
-        // epilogue: accumulator element r of a 32x32 tile sits at
-        // row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
-        const int col_in = lane & 31;
+        // epilogue: accumulator element r of a 16x16 tile sits at
+        // row 4*(lane/16) + r, column lane%16
+        const int col_in = lane & 15;
 #pragma unroll
         for (int mi = 0; mi < MS; ++mi) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row_in = wm * (BM / WAVES_M) + mi * 32 + (r >> 2) * 8 + (lane >> 5) * 4 +
-                                   (r & 3);
+            for (int r = 0; r < 4; ++r) {
+                const int row_in = wm * (BM / WAVES_M) + mi * 16 + (lane >> 4) * 4 + r;
                 if (row_in >= rows_valid) continue;
                 bf16_t* orow = args.out + (int64_t)(row0 + row_in) * args.ldo;
                 if (SWIGLU) {
                     constexpr int HW = BNW / 2 / WAVES_N;
 #pragma unroll
                     for (int j = 0; j < NS / 2; ++j) {
-                        const int col = n0 + wn * HW + j * 32 + col_in;
+                        const int col = n0 + wn * HW + j * 16 + col_in;
                         if (col < args.N)
                             orow[col] = f32_to_bf16(silu(acc[mi][j][r]) * acc[mi][NS / 2 + j][r]);
                     }
                 } else {
 #pragma unroll
                     for (int jj = 0; jj < NS; ++jj) {
-                        const int col = n0 + wn * (BNW / WAVES_N) + jj * 32 + col_in;
+                        const int col = n0 + wn * (BNW / WAVES_N) + jj * 16 + col_in;
                         if (col < args.N) orow[col] = f32_to_bf16(acc[mi][jj][r]);
                     }
                 }
