@@ -372,7 +372,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
             mfma(fa1, fb0, 0);
             sstore(buf ^ 1);
             // issue order up to the barrier: each half's fragment reads at the head of
-            // the MFMA batch before the one that uses them, then the stage stores
+            // the MFMA batch before the one that uses them, the stage stores spread
+            // over the last batch
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
@@ -390,8 +391,12 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
                 __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
             }
-            __builtin_amdgcn_sched_group_barrier(SG_MFMA, 12, 0);
-            __builtin_amdgcn_sched_group_barrier(SG_DS_WRITE, 8, 0);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                __builtin_amdgcn_sched_group_barrier(SG_DS_WRITE, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(SG_MFMA, 4, 0);
             __syncthreads();
             gload(kt0 + (t + 2 < nsteps ? t + 2 : nsteps - 1));
             read_a(buf ^ 1, 0, fa0);
