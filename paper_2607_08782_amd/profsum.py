@@ -12,7 +12,7 @@ Each profiled run measures one layer shape and regime alone
     python -m paper_2607_08782_amd.profsum traffic NAME:REGIME <FETCH csv> <WRITE csv>
     # tiled-GEMM utilisation from a GRBM_GUI_ACTIVE / SQ_* counter run
     python -m paper_2607_08782_amd.profsum mfma <counter csv>
-    # where one step's time goes, per kernel (kernel traces of --steps S runs)
+    # where one step's time goes, per kernel (kernel traces of layer_trace runs)
     python -m paper_2607_08782_amd.profsum breakdown --steps N LABEL=<kernel_trace.csv> ...
 
 Counter calibration: the run's first kernel is a plain elementwise copy of
@@ -163,11 +163,15 @@ def mfma(counter_csv, cus=256, simds=1024, xcds=8):
 
 def breakdown(runs, steps):
     """Markdown table per run: each kernel's launches per step, mean duration and
-    time per step (every dispatch of a run belongs to one of its `steps` steps)."""
+    time per step.  The dispatches counted are those after the last marker kernel
+    (layer_trace launches one right before its `steps` steps), else all of them."""
     lines = []
     for label, path in runs:
         with open(path) as fh:
             rows = sorted(csv.DictReader(fh), key=lambda r: int(r["Start_Timestamp"]))
+        marks = [i for i, r in enumerate(rows) if COPY_KERNEL in r["Kernel_Name"]]
+        if marks:
+            rows = rows[marks[-1] + 1:]
         per, order = collections.defaultdict(list), []
         for r in rows:
             k = short(r["Kernel_Name"])
