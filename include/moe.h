@@ -53,7 +53,7 @@ extern "C" {
 /* products of moe_grouped_ffn_products */
 #define MOE_FFN_GATE_UP 1   /* h = SiLU(W1 x) * (W3 x), kept in the workspace */
 #define MOE_FFN_DOWN    2   /* y = W2 h, from the workspace */
-#define MOE_FFN_SMALL_GROUPS 4   /* hint: no group has more than 64 rows */
+#define MOE_FFN_SMALL_GROUPS 4   /* hint: no group has more than 256 rows; all are streamed */
 
 /* flags of moe_route_topk */
 #define MOE_RENORM    1   /* gates = softmax over the k selected logits (else: full softmax, restricted) */
@@ -232,12 +232,15 @@ int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets,
  * MOE_FFN_DOWN.  Other arguments, requirements and errors as for
  * moe_grouped_ffn; products outside {1, 2, 3} give MOE_ERR_ARG.
  * Adding MOE_FFN_SMALL_GROUPS to products states that no group holds more
- * than 64 rows (true of the routed experts of a batch of at most 64 tokens:
- * a token reaches an expert at most once).  Such groups always take the
- * weight-streaming kernels, so the call skips the launches of the tiled
- * kernels and gives bitwise the outputs it gives without the flag; rows of a
- * group that breaks the statement are left unwritten.  It must be passed the
- * same way to the MOE_FFN_GATE_UP and the MOE_FFN_DOWN call of one pair.
+ * than 256 rows (true of a batch of at most 256 tokens: a token reaches an
+ * expert at most once).  Every group then takes the weight-streaming kernels
+ * and the call skips the launches of the tiled kernels.  Groups of at most 64
+ * rows are streamed with or without the flag, so a call whose groups all hold
+ * at most 64 rows gives bitwise the outputs it gives without it; a group of 65
+ * to 256 rows that the call without the flag would give to the tiled kernel
+ * sums its products in another order (same tolerance).  Rows of a group that
+ * breaks the statement are left unwritten.  It must be passed the same way to
+ * the MOE_FFN_GATE_UP and the MOE_FFN_DOWN call of one pair.
  */
 int moe_grouped_ffn_products(const void* x_perm, int dtype, const int32_t* group_offsets,
                              int n_groups, const void* const* w13, const void* const* w2, int d,
@@ -246,8 +249,8 @@ int moe_grouped_ffn_products(const void* x_perm, int dtype, const int32_t* group
 
 /*
  * moe_grouped_ffn_combine -- moe_grouped_ffn followed by moe_combine, for calls
- * in which no group holds more than 64 rows (a batch of at most 64 tokens; the
- * MOE_FFN_SMALL_GROUPS statement): the expert outputs are combined inside the
+ * in which no group holds more than 256 rows (a batch of at most 256 tokens;
+ * the MOE_FFN_SMALL_GROUPS statement): the expert outputs are combined inside the
  * down product's fixed-order sum of its K chunks (the gate-weighted sum of
  * Sec. II-A, the return trip of Sec. II-B), so y_perm is neither written nor
  * read back and the combine needs no launch of its own:
@@ -255,12 +258,13 @@ int moe_grouped_ffn_products(const void* x_perm, int dtype, const int32_t* group
  *   y[t] = sum_{r ascending, token_row[t][r] >= 0} topk_gate[t][r] * y_perm[token_row[t][r]]
  *          + y_shared[t]
  *
- * with y_perm[p] the bf16 value moe_grouped_ffn would store, summed in fp32 in
- * the order moe_combine uses: bitwise moe_grouped_ffn + moe_combine.
+ * with y_perm[p] the bf16 value moe_grouped_ffn with MOE_FFN_SMALL_GROUPS would
+ * store, summed in fp32 in the order moe_combine uses: bitwise that call
+ * followed by moe_combine.
  * x_perm, group_offsets, n_groups, w13, w2, d, f, cap_rows and ws as for
  * moe_grouped_ffn; token_row, topk_gate, y_shared (nullable), T, k and y as for
  * moe_combine.  MOE_BF16 only (MOE_ERR_ARG otherwise).  Rows of a group that
- * holds more than 64 rows are left out of y.  If y_shared comes from another
+ * holds more than 256 rows are left out of y.  If y_shared comes from another
  * stream, that stream must be joined before this call.
  */
 int moe_grouped_ffn_combine(const void* x_perm, int dtype, const int32_t* group_offsets,

@@ -60,9 +60,10 @@ struct GemmArgs {
     int n_tiles;                       // output-column tiles per group
     int* limits;                       // [2] row limits of the streamed groups of the gate/up and
                                        // the down product (small_limits): the gate/up launch
-                                       // writes both, later launches read theirs; nullptr: no
-                                       // group exceeds SMALL_ROWS
+                                       // writes both, later launches read theirs; nullptr: the
+                                       // limit is lim0
     int product;                       // 0 gate/up, 1 down
+    int lim0;                          // row limit of streamed groups when limits is nullptr
     int down_tiles;                    // gate/up launch: the down product's column tiles
     float* part;                       // fp32 partial tiles for split K (nullptr: never split)
     int* split_info;                   // the kernel records its split factor here for the reduce
@@ -199,7 +200,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 
     // the down launch reads its row limit from the gate/up launch (no group can
     // exceed SMALL_ROWS when there is nowhere to keep it)
-    int lim = args.limits != nullptr && args.product == 1 ? args.limits[1] : SMALL_ROWS;
+    int lim = args.limits != nullptr && args.product == 1 ? args.limits[1] : args.lim0;
     for (int s = tid; s <= n_groups; s += GEMM_THREADS) s_off[s] = args.offsets[s];
     __syncthreads();
     if (wave == 0) {
@@ -521,7 +522,8 @@ struct StreamArgs {
     const int32_t* a_rows;               // gather: row p of A is a[a_rows[p]] (a holds a_total rows)
     int a_total;
     const int* limits;                   // row limits written by the gate/up tiled launch (nullptr:
-    int product;                         // SMALL_ROWS); this product's index, 0 gate/up, 1 down
+    int product;                         // lim0); this product's index, 0 gate/up, 1 down
+    int lim0;                            // row limit of streamed groups when limits is nullptr
 };
 
 struct StreamPlan {
@@ -532,7 +534,7 @@ struct StreamPlan {
 };
 
 __device__ void make_stream_plan(const StreamArgs& a, StreamPlan& P, int nthreads) {
-    const int lim = a.limits != nullptr ? a.limits[a.product] : SMALL_ROWS;
+    const int lim = a.limits != nullptr ? a.limits[a.product] : a.lim0;
     for (int g = threadIdx.x; g <= a.n_groups; g += nthreads) P.off[g] = a.offsets[g];
     __syncthreads();
     if (threadIdx.x < 64) {                          // one wave: prefix sums over the groups
@@ -709,7 +711,7 @@ __device__ void tile_split_reduce(const GemmArgs& t, int* s_off, int* s_tstart) 
     const int n_groups = t.n_groups;
     for (int g = threadIdx.x; g <= n_groups; g += ST_THREADS) s_off[g] = t.offsets[g];
     __syncthreads();
-    const int lim = t.limits != nullptr ? t.limits[t.product] : SMALL_ROWS;
+    const int lim = t.limits != nullptr ? t.limits[t.product] : t.lim0;
     if (threadIdx.x < 64) tile_starts(s_off, n_groups, lim, t.n_tiles, s_tstart, threadIdx.x);
     __syncthreads();
     const SplitPlan plan = split_plan(s_tstart[n_groups], t.K / BK, t.split_units);
@@ -844,7 +846,7 @@ __global__ __launch_bounds__(ST_THREADS) void stream_reduce_combine_kernel(Strea
                                                                            CombineArgs cb) {
     __shared__ StreamPlan P;
     make_stream_plan(args, P, ST_THREADS);
-    const int lim = args.limits != nullptr ? args.limits[args.product] : SMALL_ROWS;
+    const int lim = args.limits != nullptr ? args.limits[args.product] : args.lim0;
     const int S = P.S;
     const int d = args.N;
     const int chunks = d / 4;
@@ -1029,8 +1031,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
                        const void* combine) {
     if (cap_rows == 0) return MOE_OK;
     const bool up = (products & MOE_FFN_GATE_UP) != 0, down = (products & MOE_FFN_DOWN) != 0;
-    // every group within the streaming kernel's own limit: no tile, no split tile and
-    // no row limit to pass on, so the tiled launches are left out
+    // every group within SMALL_ROWS_MAX rows (the caller's statement): all of them are
+    // streamed, so no tile, no split tile and no row limit to pass on, and the tiled
+    // launches are left out
     const bool small = (products & MOE_FFN_SMALL_GROUPS) != 0;
     if (dtype == MOE_F32) {
         PtrTable t13, t2;
@@ -1085,6 +1088,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a1.n_tiles = (int)ceil_div(f, BNW / 2);
     a1.limits = tinfo ? tinfo + 2 : nullptr;
     a1.product = 0;
+    a1.lim0 = small ? SMALL_ROWS_MAX : SMALL_ROWS;
     a1.down_tiles = (int)ceil_div(d, BNW);
     a1.part = tpart;
     a1.split_info = tinfo;
@@ -1111,6 +1115,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s1.a_total = (int)a_total;
     s1.limits = a1.limits;
     s1.product = 0;
+    s1.lim0 = a1.lim0;
     if (up) {
         if (a_rows)
             hipLaunchKernelGGL(stream_gemm_kernel<true>, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);

@@ -4,8 +4,9 @@
 torch) and enqueues, on the current stream:
     moe_route_topk -> moe_expert_histogram -> moe_permute
     -> moe_grouped_ffn (routed experts) -> moe_combine
-with no host synchronisation in between (for batches of at most 64 tokens the
-last two are one call, moe_grouped_ffn_combine).  The shared experts' FFN
+with no host synchronisation in between (decode-sized batches stream every
+expert group and skip the tiled GEMM launches; at most 64 tokens with k <= 2 the
+last two calls are one, moe_grouped_ffn_combine).  The shared experts' FFN
 (moe_grouped_ffn over every token), which does not depend on the routing,
 runs on a second stream forked from the current one and joined back before
 the combine, so it overlaps the short routing and packaging launches; the
@@ -50,7 +51,7 @@ class LayerShare:
                  w2: Sequence[torch.Tensor], shared=(), renorm: bool = True,
                  coact: bool = False, want_logits: bool = True, cap_rows: Optional[int] = None,
                  gather_in_ffn: bool = False, overlap_shared: bool = True,
-                 fuse_combine: bool = True):
+                 fuse_combine: Optional[bool] = None):
         self.device = X.device
         self.X = X
         self.Wr = Wr
@@ -111,15 +112,24 @@ class LayerShare:
             self._fork = torch.cuda.Event(enable_timing=False)
             self._join = torch.cuda.Event(enable_timing=False)
         self.y = torch.empty((max(T, 1), d), dtype=dt, device=dv)
-        # a token reaches an expert at most once, so with at most 64 tokens no group
-        # exceeds the streaming kernels' limit and the tiled launches can be left out
+        # a token reaches an expert at most once, so with at most 256 tokens no group
+        # exceeds the streaming kernels' limit; when the mean group is decode-sized
+        # (T k / E <= 64 rows) every group is streamed and the tiled launches are
+        # left out (the shared experts' call, one group of T rows, likewise)
         self.ffn_products = moe.MOE_FFN_GATE_UP | moe.MOE_FFN_DOWN
-        if T <= 64:
+        if T <= 64 or (T <= 256 and T * k <= 64 * self.E):
             self.ffn_products |= moe.MOE_FFN_SMALL_GROUPS
-        # ... and the combine can run inside the down product's chunk sum
-        # (moe_grouped_ffn_combine: y_perm is not written)
-        self.fused_combine = (fuse_combine and T <= 64 and dt == torch.bfloat16
-                              and not gather_in_ffn and self.weights is not None)
+        # ... and then the combine can run inside the down product's chunk sum
+        # (moe_grouped_ffn_combine: y_perm is not written).  fuse_combine None: where
+        # it measured faster, batches of at most 64 tokens with k <= 2 (at k = 6 or 8
+        # the fused chunk sum, k x S partial loads per output element, is slower than
+        # the chunk sum plus the combine launch); True: whenever the call streams
+        # every group; False: never
+        can_fuse = (bool(self.ffn_products & moe.MOE_FFN_SMALL_GROUPS) and dt == torch.bfloat16
+                    and not gather_in_ffn and self.weights is not None)
+        if fuse_combine is None:
+            fuse_combine = T <= 64 and k <= 2
+        self.fused_combine = bool(fuse_combine) and can_fuse
 
     def set_placement(self, placement: np.ndarray, w13: Sequence[torch.Tensor],
                       w2: Sequence[torch.Tensor]):

@@ -360,7 +360,7 @@ def moe_grouped_ffn_combine(x_perm: torch.Tensor, group_offsets: torch.Tensor,
                             y_shared: Optional[torch.Tensor], *, cap_rows: int, T: int,
                             y: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
                             stream=None) -> torch.Tensor:
-    """Grouped FFN and weighted combine in one call (every group at most 64 rows).
+    """Grouped FFN and weighted combine in one call (every group at most 256 rows).
     Returns y [T, d]."""
     lib = load_library()
     d, f = weights.d, weights.f
