@@ -106,6 +106,9 @@ def ffn_call(share, products=None):
     the given products of moe_grouped_ffn alone."""
     if products is None:
         return share.routed_ffn
+    if share.gather_in_ffn:
+        raise ValueError("a share that gathers its rows in the FFN has no x_perm to run "
+                         "single products on")
     return lambda: moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"],
                                        share.weights, cap_rows=share.cap_rows, y_perm=share.y_perm,
                                        ws=share.ws_ffn, products=products)
@@ -144,9 +147,7 @@ def phase_calls(share):
         moe.moe_expert_histogram(share.topk_idx, share.E, counts=share.counts, coact=share.coact)
 
     def permute():
-        moe.moe_permute(share.X, share.topk_idx, share.topk_gate, share.counts, share.placement,
-                        share.dev, E=share.E, cap_rows=share.cap_rows, out=share.perm,
-                        ws=share.ws_perm)
+        share.package()
 
     def grouped_ffn():
         share.routed_ffn()
@@ -223,9 +224,15 @@ def measure(name, regime, steps, warmup, seed=0, dominant=False, eager=False):
         out["ffn_ms"] = time_replays([capture(ffn_call(s)) for s in shares], steps, warmup)
         if dominant:
             # the gate/up product alone: the tiled GEMM plus its (empty at this size)
-            # streaming launch and chunk sum
-            gu = [capture(ffn_call(s, moe.MOE_FFN_GATE_UP)) for s in shares]
+            # streaming launch and chunk sum, on the packaged rows
+            pshares = shares
+            if s0.gather_in_ffn:
+                pshares = rotated_shares(cfg, inp, gather_in_ffn=False)
+                for s in pshares:
+                    s.run()
+            gu = [capture(ffn_call(s, moe.MOE_FFN_GATE_UP)) for s in pshares]
             out["gate_up_ms"] = time_replays(gu, steps, warmup)
+            del pshares
     if eager:
         out["phases_us"], out["eager_ms"] = eager_phases(s0, max(steps // 2, 3), warmup)
     return cfg, inp, shares, work, out
@@ -291,21 +298,25 @@ def shape_entry(name, regime, steps, warmup):
 
 
 def gathered_variant(cfg, inp, shares, steps, warmup):
-    """The headline share with the row copy x_perm elided (moe_permute writes the row
-    maps only, moe_grouped_ffn_rows reads the token rows through row_token): step time
-    from graph replays over the same weight copies, and whether its output equals the
-    packaged path's bit for bit."""
+    """The headline share on its other packaging path (with the row copy x_perm
+    elided -- moe_permute writes the row maps only and moe_grouped_ffn_rows reads the
+    token rows through row_token -- or with it, whichever the share does not use):
+    step time from graph replays over the same weight copies, and whether its output
+    equals the share's bit for bit."""
+    gather = not shares[0].gather_in_ffn
     gs = [LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, s.weights.w13,
-                     s.weights.w2, shared=inp.shared, coact=cfg.coact, gather_in_ffn=True)
+                     s.weights.w2, shared=inp.shared, coact=cfg.coact, gather_in_ffn=gather)
           for s in shares]
     shares[0].run()
     gs[0].run()
     torch.cuda.synchronize()
     equal = bool(torch.equal(shares[0].y, gs[0].y))
     ms = time_replays([capture(g.run) for g in gs], steps, warmup)
-    return {"ms_per_step": ms, "tokens_per_s": inp.T / (ms * 1e-3), "bitwise_equal_output": equal,
-            "what": "row copy x_perm elided: moe_permute writes the row maps only and "
-                    "moe_grouped_ffn_rows reads the token rows through row_token"}
+    what = ("row copy x_perm elided: moe_permute writes the row maps only and "
+            "moe_grouped_ffn_rows reads the token rows through row_token") if gather else \
+           "rows copied to x_perm by moe_permute and read from there by moe_grouped_ffn"
+    return {"gather_in_ffn": gather, "ms_per_step": ms, "tokens_per_s": inp.T / (ms * 1e-3),
+            "bitwise_equal_output": equal, "what": what}
 
 
 # ---------------------------------------------------------------------------

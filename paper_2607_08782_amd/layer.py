@@ -50,7 +50,7 @@ class LayerShare:
                  placement: np.ndarray, dev: int, w13: Sequence[torch.Tensor],
                  w2: Sequence[torch.Tensor], shared=(), renorm: bool = True,
                  coact: bool = False, want_logits: bool = True, cap_rows: Optional[int] = None,
-                 gather_in_ffn: bool = False, overlap_shared: bool = True,
+                 gather_in_ffn: Optional[bool] = None, overlap_shared: bool = True,
                  fuse_combine: Optional[bool] = None):
         self.device = X.device
         self.X = X
@@ -63,8 +63,13 @@ class LayerShare:
         self.renorm = renorm
         self.want_coact = coact
         # gather_in_ffn: the permute step writes only the row maps and the expert
-        # FFN reads its rows from X through row_token (moe_grouped_ffn_rows)
-        self.gather_in_ffn = gather_in_ffn
+        # FFN reads its rows from X through row_token (moe_grouped_ffn_rows).  None:
+        # for bf16 batches of at least 16384 token-expert assignments, where the row
+        # copy it saves is large (measured faster at the DeepSeek-V2-Lite and Qwen3
+        # prefill shapes, even at Mixtral's, slower at Qwen1.5's 8192)
+        if gather_in_ffn is None:
+            gather_in_ffn = X.dtype == torch.bfloat16 and X.shape[0] * k >= 16384
+        self.gather_in_ffn = bool(gather_in_ffn)
         self.placement = np.ascontiguousarray(placement, dtype=np.uint8)
         self.G = self.placement.shape[1]
         self.n_local = int(self.placement[:, dev].sum())
@@ -162,14 +167,21 @@ class LayerShare:
                             y_perm=self.y_shared, ws=self.ws_shared, stream=stream,
                             products=self.ffn_products)
 
-    def routed_ffn(self):
+    def package(self):
+        """Enqueue the packaging step as `run` makes it (moe_permute; the row copy
+        x_perm only when the FFN does not gather the rows itself)."""
+        moe.moe_permute(self.X, self.topk_idx, self.topk_gate, self.counts, self.placement,
+                        self.dev, E=self.E, cap_rows=self.cap_rows, out=self.perm, ws=self.ws_perm,
+                        copy_rows=not self.gather_in_ffn)
+
+    def routed_ffn(self, fused: Optional[bool] = None):
         """Enqueue the routed experts' FFN call as `run` makes it: moe_grouped_ffn (or
-        moe_grouped_ffn_rows) into y_perm, or, when the share fuses the combine,
-        moe_grouped_ffn_combine into y (which then reads y_shared: the shared experts'
-        call must have completed on this stream)."""
+        moe_grouped_ffn_rows) into y_perm, or, when the share fuses the combine (fused
+        None: as `run` does), moe_grouped_ffn_combine into y (which then reads y_shared:
+        the shared experts' call must have completed on this stream)."""
         if self.weights is None:
             return
-        if self.fused_combine:
+        if self.fused_combine if fused is None else (fused and self.fused_combine):
             moe.moe_grouped_ffn_combine(self.perm["x_perm"], self.perm["group_offsets"],
                                         self.weights, self.perm["token_row"], self.topk_gate,
                                         self.y_shared, cap_rows=self.cap_rows, T=self.T, y=self.y,
@@ -195,9 +207,7 @@ class LayerShare:
             self._join.record(self._side)
         self.route(logits_in)
         moe.moe_expert_histogram(self.topk_idx, self.E, counts=self.counts, coact=self.coact)
-        moe.moe_permute(self.X, self.topk_idx, self.topk_gate, self.counts, self.placement,
-                        self.dev, E=self.E, cap_rows=self.cap_rows, out=self.perm, ws=self.ws_perm,
-                        copy_rows=not self.gather_in_ffn)
+        self.package()
         if self.fused_combine:
             if self._side is not None:
                 main.wait_event(self._join)

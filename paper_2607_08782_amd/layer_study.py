@@ -4,10 +4,12 @@ For each shape (Mixtral-8x7B, DeepSeek-V2-Lite, Qwen1.5-MoE-A2.7B and
 Qwen3-30B-A3B-shaped shares; prefill and decode batches) and each seed 0-4:
 synthetic inputs of that shape (seeded normal hidden states and weights, Zipf
 popularity bias, the benchmark placement), the five calls captured in one HIP
-graph, and the step timed over graph replays (also with the row copy x_perm
-elided: the expert FFN reading token rows through the row map); the routed
-experts' FFN call is timed the same way on its own (for batches of at most 64
-tokens that call also writes the combine).  Reported: tokens/s, the FFN's rate against the bf16 MFMA
+graph, and the step timed over graph replays, with the packaged row copy x_perm
+and with it elided (the expert FFN reading token rows through the row map, which
+LayerShare picks by itself for bf16 batches of at least 16384 token-expert
+assignments); the routed experts' FFN call of the packaged share is timed the
+same way on its own (for batches of at most 64 tokens with k <= 2 that call also
+writes the combine).  Reported: tokens/s, the FFN's rate against the bf16 MFMA
 peak (6 d f N flop) and against HBM (weights of the active local experts read
 once plus x_perm in and y_perm, or the combined y, out), mean and spread over the seeds.
 
@@ -75,7 +77,7 @@ def measure(name, regime, seed, steps):
         w13 = inp.w13 if c == 0 else [w.clone() for w in inp.w13]
         w2 = inp.w2 if c == 0 else [w.clone() for w in inp.w2]
         shares.append(LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, w13, w2,
-                                 shared=inp.shared, coact=cfg.coact))
+                                 shared=inp.shared, coact=cfg.coact, gather_in_ffn=False))
         gshares.append(LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, w13, w2,
                                   shared=inp.shared, coact=cfg.coact, gather_in_ffn=True))
     for s in shares + gshares:
@@ -137,8 +139,8 @@ def main(argv=None):
              "Synthetic seeded inputs of each shape (normal hidden states, N(0, 0.02) weights, Zipf",
              "popularity bias, the benchmark placement with this GPU = device 0).  Step = the five",
              "calls as one HIP graph replay; FFN = the routed experts' FFN call as the step makes it",
-             "(`moe_grouped_ffn`; `moe_grouped_ffn_combine` for batches of at most 64 tokens, which",
-             "also writes the combined output) replayed on its own.  Mean (± population std) over seeds 0-%d; %d timed replays per"
+             "(`moe_grouped_ffn`; `moe_grouped_ffn_combine` for batches of at most 64 tokens with",
+             "k <= 2, which also writes the combined output) replayed on its own.  Mean (± population std) over seeds 0-%d; %d timed replays per"
              % (args.seeds - 1, args.steps),
              "seed for prefill-sized batches, %d for decode.  FFN rate against the bf16 MFMA peak"
              % (args.steps * 10),
@@ -146,9 +148,10 @@ def main(argv=None):
              "active local experts' weights once, x_perm in, y_perm or the combined y out).  Weight",
              "copies: replays cycle through this many copies of the local expert weights (≥ 1 GB",
              "touched).",
-             "Gathered step: the same share with the row copy x_perm elided (moe_permute writes the",
-             "row maps only and moe_grouped_ffn_rows reads the token rows through row_token;",
-             "bitwise the same output).", "",
+             "Step: the share with the packaged row copy x_perm.  Gathered step: the same share with",
+             "the row copy elided (moe_permute writes the row maps only and moe_grouped_ffn_rows",
+             "reads the token rows through row_token; bitwise the same output), the path LayerShare",
+             "takes by itself for bf16 batches of at least 16384 token-expert assignments.", "",
              "Command: `python -m paper_2607_08782_amd.layer_study --seeds %d --steps %d --out %s`"
              % (args.seeds, args.steps, args.out), "",
              "| shape / regime | T | rows here N | active / local experts | weight copies | step us | tokens/s | gathered step us | FFN us | FFN TFLOP/s (% bf16 peak) | FFN GB/s (% HBM peak) |",

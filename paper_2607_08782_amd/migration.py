@@ -222,16 +222,13 @@ def run_step(share, mig: Optional[Migrator], budget_bytes: Optional[int] = None,
     cur = torch.cuda.current_stream()
     share.route()
     moe.moe_expert_histogram(share.topk_idx, share.E, counts=share.counts, coact=share.coact)
-    moe.moe_permute(share.X, share.topk_idx, share.topk_gate, share.counts, share.placement,
-                    share.dev, E=share.E, cap_rows=share.cap_rows, out=share.perm, ws=share.ws_perm)
+    share.package()
     opened = torch.cuda.Event(enable_timing=True)
     opened.record(cur)
     # the window's computation is enqueued first: the copies only wait for `opened`
     # on the device, and issuing them (one host call per chunk) must not hold back
     # the launch of the computation they hide behind
-    if share.weights is not None:
-        moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
-                            cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
+    share.routed_ffn(fused=False)
     if share.shared_weights is not None:
         moe.moe_grouped_ffn(share.X, share.shared_offsets, share.shared_weights, cap_rows=share.T,
                             y_perm=share.y_shared, ws=share.ws_shared)

@@ -73,8 +73,7 @@ def straggler_ffn_us(inp, cfg, x_map, weights, reps=5):
         for _ in range(reps):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
-            moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
-                                cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
+            share.routed_ffn(fused=False)
             b.record()
             b.synchronize()
             times.append(a.elapsed_time(b) * 1e3)

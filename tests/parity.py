@@ -60,13 +60,14 @@ class Case:
     """One layer share on the GPU plus its CPU copies for the oracle."""
 
     def __init__(self, cfg: synth.LayerConfig, T: int, seed: int = 0, batch: int = 0,
-                 dev: int = 0):
+                 dev: int = 0, gather_in_ffn=None):
         self.cfg = cfg
         self.T = T
         self.inp = synth.make_layer(cfg, T, seed=seed, device="cuda", batch=batch, dev=dev)
         i = self.inp
         self.share = LayerShare(i.X, i.Wr, i.bias, cfg.k, i.placement, dev, i.w13, i.w2,
-                                shared=i.shared, renorm=True, coact=cfg.coact)
+                                shared=i.shared, renorm=True, coact=cfg.coact,
+                                gather_in_ffn=gather_in_ffn)
         self.X = np32(i.X)
         self.Wr = np32(i.Wr)
         self.b = np32(i.bias)

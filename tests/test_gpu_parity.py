@@ -211,8 +211,10 @@ def _share(cfg, T, logits=None, placement=None, dev=0):
     pl = inp.placement if placement is None else placement
     local = [int(e) for e in np.nonzero(pl[:, dev])[0]]
     ws = [synth.expert_weights(cfg, e, 1, "cuda") for e in local]
+    # the packaging checks read the row copy x_perm, so the share keeps it
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, pl, dev, [a for a, _ in ws],
-                       [b for _, b in ws], shared=inp.shared, fuse_combine=False)
+                       [b for _, b in ws], shared=inp.shared, fuse_combine=False,
+                       gather_in_ffn=False)
     return inp, share
 
 
@@ -516,7 +518,7 @@ def test_very_long_batch_routing_and_packaging_every_element():
     sampled tokens within the bf16 tolerance."""
     cfg = synth.custom_config(d=64, E=48, k=4, f=64, G=2, replicas=1, zipf=1.2, coact=True)
     say("[long]", "T=100000")
-    case = Case(cfg, 100000)
+    case = Case(cfg, 100000, gather_in_ffn=False)       # the row copy is checked too
     ref_logits, _ = check_logits(case)
     idx, gate, pm = check_routing(case, ref_logits)
     check_ffn_and_combine(case, idx, gate, pm, sample=64)
