@@ -109,14 +109,114 @@ __global__ __launch_bounds__(COMBINE_THREADS) void combine_kernel(
     Vec<Elem, V>::store(y + t * d + col, acc);
 }
 
+// Rows that are a whole number of wave widths (every lane of a wave serves the
+// same token): the token's local rows are compacted in registers (ascending r,
+// by selects, no indexed registers), their count is uniform across the wave,
+// and one of KM + 1 straight paths issues exactly that many row loads at once.
+// At k = 8 with about two local rows per token this issues a quarter of the
+// loads of the kernel above; the sum is the same, in the same order.
+template <typename Elem, int V, int N, int KM>
+__device__ __forceinline__ void combine_rows(const Elem* __restrict__ y_perm, const int32_t* q,
+                                             const float* h, int d, int col, float* acc) {
+    if constexpr (N > 0) {
+        float v[N][V];
+#pragma unroll
+        for (int j = 0; j < N; ++j) Vec<Elem, V>::load(y_perm + (int64_t)q[j] * d + col, v[j]);
+#pragma unroll
+        for (int j = 0; j < N; ++j)
+#pragma unroll
+            for (int i = 0; i < V; ++i) acc[i] = fmaf(h[j], v[j][i], acc[i]);
+    }
+}
+
+template <typename Elem, int V, int KM>
+__global__ __launch_bounds__(COMBINE_THREADS) void combine_compact_kernel(
+    const Elem* __restrict__ y_perm, const int32_t* __restrict__ token_row,
+    const float* __restrict__ gate, const Elem* __restrict__ y_shared, int64_t T, int d, int k,
+    int chunks_per_row, Elem* __restrict__ y) {
+    const int64_t gid = (int64_t)blockIdx.x * COMBINE_THREADS + threadIdx.x;
+    const int64_t t = gid / chunks_per_row;
+    const int c = (int)(gid - t * chunks_per_row);
+    if (t >= T) return;                      // whole waves: T * chunks_per_row is a multiple of 64
+    const int col = c * V;
+    int32_t p[KM];
+    float g[KM];
+#pragma unroll
+    for (int r = 0; r < KM; ++r) {
+        const int rr = r < k ? r : k - 1;
+        p[r] = r < k ? token_row[t * k + rr] : -1;
+        g[r] = gate[t * k + rr];
+    }
+    // slot j of the compacted list takes the r with p[r] >= 0 and j local rows before it
+    int32_t q[KM];
+    float h[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        q[j] = 0;
+        h[j] = 0.f;
+    }
+    int n = 0;
+#pragma unroll
+    for (int r = 0; r < KM; ++r) {
+        const bool here = p[r] >= 0;
+#pragma unroll
+        for (int j = 0; j <= r; ++j) {
+            const bool take = here && n == j;
+            q[j] = take ? p[r] : q[j];
+            h[j] = take ? g[r] : h[j];
+        }
+        n += here ? 1 : 0;
+    }
+    n = __builtin_amdgcn_readfirstlane(n);
+    float acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = 0.f;
+    switch (n) {
+        case 0: break;
+        case 1: combine_rows<Elem, V, 1, KM>(y_perm, q, h, d, col, acc); break;
+        case 2: combine_rows<Elem, V, (2 <= KM ? 2 : 1), KM>(y_perm, q, h, d, col, acc); break;
+        case 3: combine_rows<Elem, V, (3 <= KM ? 3 : 1), KM>(y_perm, q, h, d, col, acc); break;
+        case 4: combine_rows<Elem, V, (4 <= KM ? 4 : 1), KM>(y_perm, q, h, d, col, acc); break;
+        default:
+#pragma unroll
+            for (int j0 = 0; j0 < KM; j0 += 4) {
+                // more than four rows: four at a time, in order
+                if (j0 < n) {
+                    float v[4][V];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        Vec<Elem, V>::load(y_perm + (int64_t)q[j0 + j < KM ? j0 + j : 0] * d + col, v[j]);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+#pragma unroll
+                        for (int i = 0; i < V; ++i)
+                            acc[i] = j0 + j < n ? fmaf(h[j0 + j < KM ? j0 + j : 0], v[j][i], acc[i]) : acc[i];
+                }
+            }
+            break;
+    }
+    if (y_shared) {
+        float w[V];
+        Vec<Elem, V>::load(y_shared + t * d + col, w);
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] += w[i];
+    }
+    Vec<Elem, V>::store(y + t * d + col, acc);
+}
+
 template <typename Elem, int V, int KM>
 int launch_k(const void* y_perm, const int32_t* token_row, const float* gate, const void* y_shared,
              int64_t T, int d, int k, void* y, hipStream_t s) {
     const int chunks = d / V;
     const int64_t blocks = ceil_div(T * chunks, COMBINE_THREADS);
-    hipLaunchKernelGGL((combine_kernel<Elem, V, KM>), dim3((unsigned)blocks), dim3(COMBINE_THREADS),
-                       0, s, (const Elem*)y_perm, token_row, gate, (const Elem*)y_shared, T, d, k,
-                       chunks, (Elem*)y);
+    if (chunks % 64 == 0 && KM > 2)
+        hipLaunchKernelGGL((combine_compact_kernel<Elem, V, KM>), dim3((unsigned)blocks),
+                           dim3(COMBINE_THREADS), 0, s, (const Elem*)y_perm, token_row, gate,
+                           (const Elem*)y_shared, T, d, k, chunks, (Elem*)y);
+    else
+        hipLaunchKernelGGL((combine_kernel<Elem, V, KM>), dim3((unsigned)blocks),
+                           dim3(COMBINE_THREADS), 0, s, (const Elem*)y_perm, token_row, gate,
+                           (const Elem*)y_shared, T, d, k, chunks, (Elem*)y);
     return launch_status();
 }
 
