@@ -733,3 +733,36 @@ def test_graph_replays_match_eager_runs():
         ref = snap()
         for a, b in zip(got, ref):
             assert torch.equal(a, b), "replay %d differs from the eager run" % i
+
+
+@pytest.mark.parametrize("k,d", [(3, 512), (8, 512), (16, 1024), (8, 2048)])
+def test_combine_with_compacted_rows_is_exact_on_exact_values(k, d):
+    """Rows of whole wave widths at k > 2 take the combine that compacts each token's
+    local rows: tokens with none, some and all of their k rows here, in every order.
+    Values are small integers and the gates powers of two, so every sum is exact in
+    fp32 and bf16 and the output must equal the oracle's bit for bit."""
+    say("[combine compact]", "k=%d d=%d" % (k, d))
+    rng = np.random.default_rng(k * 1000 + d)
+    T = 301
+    local = rng.integers(0, k + 1, size=T)
+    local[:3] = (0, k, 1)
+    N = int(local.sum())
+    rows = rng.permutation(N)
+    token_row = np.full((T, k), -1, np.int32)
+    p = 0
+    for t in range(T):
+        slots = rng.choice(k, size=int(local[t]), replace=False)
+        for r in slots:
+            token_row[t, r] = rows[p]
+            p += 1
+    gate = rng.choice(np.array([0.25, 0.5, 1.0], np.float32), size=(T, k)).astype(np.float32)
+    y_perm = rng.integers(-2, 3, size=(max(N, 1), d)).astype(np.float32)
+    y_shared = rng.integers(-2, 3, size=(T, d)).astype(np.float32)
+    for ys in (None, y_shared):
+        got = moe.moe_combine(torch.from_numpy(y_perm).bfloat16().cuda(),
+                              torch.from_numpy(token_row).cuda(), torch.from_numpy(gate).cuda(),
+                              None if ys is None else torch.from_numpy(ys).bfloat16().cuda(),
+                              T=T, d=d)
+        torch.cuda.synchronize()
+        ref = oracle.combine(y_perm, token_row, gate, ys, T, d, k)
+        np.testing.assert_array_equal(np32(got[:T]), ref.astype(np.float32))
