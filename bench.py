@@ -227,7 +227,10 @@ def measure(name, regime, steps, warmup, seed=0, dominant=False, eager=False):
             # streaming launch and chunk sum, on the packaged rows
             pshares = shares
             if s0.gather_in_ffn:
-                pshares = rotated_shares(cfg, inp, gather_in_ffn=False)
+                # the same weight copies, packaged
+                pshares = [LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0,
+                                      s.weights.w13, s.weights.w2, shared=inp.shared,
+                                      coact=cfg.coact, gather_in_ffn=False) for s in shares]
                 for s in pshares:
                     s.run()
             gu = [capture(ffn_call(s, moe.MOE_FFN_GATE_UP)) for s in pshares]

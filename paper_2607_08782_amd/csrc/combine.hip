@@ -115,7 +115,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void combine_kernel(
 // and one of KM + 1 straight paths issues exactly that many row loads at once.
 // At k = 8 with about two local rows per token this issues a quarter of the
 // loads of the kernel above; the sum is the same, in the same order.
-template <typename Elem, int V, int N, int KM>
+template <typename Elem, int V, int N>
 __device__ __forceinline__ void combine_rows(const Elem* __restrict__ y_perm, const int32_t* q,
                                              const float* h, int d, int col, float* acc) {
     if constexpr (N > 0) {
@@ -171,26 +171,28 @@ __global__ __launch_bounds__(COMBINE_THREADS) void combine_compact_kernel(
     float acc[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) acc[i] = 0.f;
+    static_assert(KM > 2, "the compacting combine serves k > 2");
     switch (n) {
         case 0: break;
-        case 1: combine_rows<Elem, V, 1, KM>(y_perm, q, h, d, col, acc); break;
-        case 2: combine_rows<Elem, V, (2 <= KM ? 2 : 1), KM>(y_perm, q, h, d, col, acc); break;
-        case 3: combine_rows<Elem, V, (3 <= KM ? 3 : 1), KM>(y_perm, q, h, d, col, acc); break;
-        case 4: combine_rows<Elem, V, (4 <= KM ? 4 : 1), KM>(y_perm, q, h, d, col, acc); break;
+        case 1: combine_rows<Elem, V, 1>(y_perm, q, h, d, col, acc); break;
+        case 2: combine_rows<Elem, V, 2>(y_perm, q, h, d, col, acc); break;
+        case 3: combine_rows<Elem, V, 3>(y_perm, q, h, d, col, acc); break;
+        case 4: combine_rows<Elem, V, 4>(y_perm, q, h, d, col, acc); break;
         default:
+            // more than four rows: four at a time, in order (slots past n hold row
+            // 0, which is loaded and dropped)
 #pragma unroll
             for (int j0 = 0; j0 < KM; j0 += 4) {
-                // more than four rows: four at a time, in order
                 if (j0 < n) {
                     float v[4][V];
 #pragma unroll
                     for (int j = 0; j < 4; ++j)
-                        Vec<Elem, V>::load(y_perm + (int64_t)q[j0 + j < KM ? j0 + j : 0] * d + col, v[j]);
+                        Vec<Elem, V>::load(y_perm + (int64_t)q[j0 + j] * d + col, v[j]);
 #pragma unroll
                     for (int j = 0; j < 4; ++j)
 #pragma unroll
                         for (int i = 0; i < V; ++i)
-                            acc[i] = j0 + j < n ? fmaf(h[j0 + j < KM ? j0 + j : 0], v[j][i], acc[i]) : acc[i];
+                            acc[i] = j0 + j < n ? fmaf(h[j0 + j], v[j][i], acc[i]) : acc[i];
                 }
             }
             break;
@@ -209,14 +211,17 @@ int launch_k(const void* y_perm, const int32_t* token_row, const float* gate, co
              int64_t T, int d, int k, void* y, hipStream_t s) {
     const int chunks = d / V;
     const int64_t blocks = ceil_div(T * chunks, COMBINE_THREADS);
-    if (chunks % 64 == 0 && KM > 2)
-        hipLaunchKernelGGL((combine_compact_kernel<Elem, V, KM>), dim3((unsigned)blocks),
-                           dim3(COMBINE_THREADS), 0, s, (const Elem*)y_perm, token_row, gate,
-                           (const Elem*)y_shared, T, d, k, chunks, (Elem*)y);
-    else
-        hipLaunchKernelGGL((combine_kernel<Elem, V, KM>), dim3((unsigned)blocks),
-                           dim3(COMBINE_THREADS), 0, s, (const Elem*)y_perm, token_row, gate,
-                           (const Elem*)y_shared, T, d, k, chunks, (Elem*)y);
+    if constexpr (KM > 2) {
+        if (chunks % 64 == 0) {
+            hipLaunchKernelGGL((combine_compact_kernel<Elem, V, KM>), dim3((unsigned)blocks),
+                               dim3(COMBINE_THREADS), 0, s, (const Elem*)y_perm, token_row, gate,
+                               (const Elem*)y_shared, T, d, k, chunks, (Elem*)y);
+            return launch_status();
+        }
+    }
+    hipLaunchKernelGGL((combine_kernel<Elem, V, KM>), dim3((unsigned)blocks), dim3(COMBINE_THREADS),
+                       0, s, (const Elem*)y_perm, token_row, gate, (const Elem*)y_shared, T, d, k,
+                       chunks, (Elem*)y);
     return launch_status();
 }
 
