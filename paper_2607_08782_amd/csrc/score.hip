@@ -198,15 +198,17 @@ int launch_tiles(const uint8_t* x, const uint8_t* w, const float* sx, const floa
 
 // K chunks for the tiled score kernel, or 0 when the shape does not suit it:
 // E > 32 (smaller E is cheap for the K-split kernel), whole 128-byte stages,
-// and at least 192 token tiles (about one per CU).  One chunk: summing K-chunk
-// partials in a second pass cost more than the parallelism it bought, and with
-// fewer tiles the K-split kernel, which spreads a batch over more workgroups,
-// measured faster (Mixtral-, DeepSeek- and Qwen1.5-shaped batches).
+// and at least 128 token tiles (half a tile per CU or more; the DeepSeek-V2-Lite
+// prefill batch of 8192 tokens: 22.1 -> 20.2 us against the block kernel).  One
+// chunk: summing K-chunk partials in a second pass cost more than the
+// parallelism it bought (that batch split in two: 27.1 us), and with fewer tiles
+// the K-split kernel, which spreads a batch over more workgroups, measured faster
+// (Qwen1.5-shaped batches).
 int score_tiles_split(int64_t T, int rowbytes, int E, bool allow_split) {
     (void)allow_split;
     if (E <= 32 || E > MOE_MAX_E || rowbytes % SC_BKB != 0 || T <= 0) return 0;
     if ((int64_t)MOE_MAX_E * rowbytes >= ((int64_t)1 << 31)) return 0;   // 32-bit buffer offsets
-    return ceil_div(T, SC_BM) >= 192 ? 1 : 0;
+    return ceil_div(T, SC_BM) >= 128 ? 1 : 0;
 }
 
 // Ring depth by tile width: one workgroup per CU, as many stages in flight as
