@@ -133,6 +133,31 @@ __device__ __forceinline__ int b_sub_row(int wn, int jj) {
     return wn * (BNW / WAVES_N) + jj * 16;
 }
 
+// 4 x 4 transpose inside each aligned quad of lanes: on entry lane 4 q + e holds
+// v[r] = M[r][e] of its quad's block, on exit v[c] = M[e][c].  Two exchange
+// stages (lane distance 1, then 2) with DPP quad permutations.
+__device__ __forceinline__ float dpp_quad(float x, int ctrl_sel) {
+    const int i = __float_as_int(x);
+    return __int_as_float(ctrl_sel == 1 ? __builtin_amdgcn_mov_dpp(i, 0xB1, 0xF, 0xF, true)
+                                        : __builtin_amdgcn_mov_dpp(i, 0x4E, 0xF, 0xF, true));
+}
+
+__device__ __forceinline__ void quad_transpose(float* v, int lane) {
+    const bool o1 = (lane & 1) != 0, o2 = (lane & 2) != 0;
+#pragma unroll
+    for (int r = 0; r < 4; r += 2) {          // lanes e, e ^ 1 swap elements r ^ 1
+        const float recv = dpp_quad(o1 ? v[r] : v[r + 1], 1);
+        v[r] = o1 ? recv : v[r];
+        v[r + 1] = o1 ? v[r + 1] : recv;
+    }
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {             // lanes e, e ^ 2 swap elements r ^ 2
+        const float recv = dpp_quad(o2 ? v[r] : v[r + 2], 2);
+        v[r] = o2 ? recv : v[r];
+        v[r + 2] = o2 ? v[r + 2] : recv;
+    }
+}
+
 __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
@@ -190,7 +215,6 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
     __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BNW * TLDK];
     __shared__ int s_off[MOE_MAX_GROUPS + 1];
     __shared__ int s_tstart[MOE_MAX_GROUPS + 1];
-    __shared__ int s_cur[4];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -237,84 +261,155 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
     const int voff = ((tid >> 3) * K + kc) * 2;
     const int vstep = ROWS_PER_PASS * K * 2;
 
-    for (int i = widx; i < n_mine; i += nper) {
-        // whole tile, or unit u = (split tile, K chunk)
+    if (widx >= n_mine) return;
+
+    // Tile coordinates, uniform across the workgroup: every thread derives them
+    // from the plan in LDS, kept in scalar registers.  Whole tile, or unit
+    // u = (split tile, K chunk).
+    struct Tile {
+        int g, row0, rows_valid, n0, kt0, nsteps, u, split;
+    };
+    auto tile_at = [&](int i) {
+        Tile c;
         const bool split = i >= n_head;
         const int u = split ? s_begin + (i - n_head) : 0;
         const int L = split ? plan.head + u / plan.S : h_begin + i;
         const int S = split ? plan.S : 1;
         const int kchunk = split ? u - (u / plan.S) * plan.S : 0;
         const int kt0 = (int)((int64_t)kchunk * KT / S);
-        const int nsteps = (int)((int64_t)(kchunk + 1) * KT / S) - kt0;
-        if (tid == 0) {
-            const int s = last_le(s_tstart, n_groups, L);
-            const int rows = s_off[s + 1] - s_off[s];
-            const int mt = (int)ceil_div(rows, BM);
-            const int local = L - s_tstart[s];
-            const int nt = local / mt;
-            s_cur[0] = s;
-            s_cur[1] = (local - nt * mt) * BM;
-            s_cur[2] = nt;
-        }
-        __syncthreads();
-        // tile coordinates are uniform across the workgroup: keep them (and the
-        // buffer descriptors built from them) in scalar registers
-        const int g = __builtin_amdgcn_readfirstlane(s_cur[0]);
-        const int m0 = __builtin_amdgcn_readfirstlane(s_cur[1]);
-        const int n0 = __builtin_amdgcn_readfirstlane(s_cur[2]) * BN_OUT;
-        const int row0 = __builtin_amdgcn_readfirstlane(s_off[g] + m0);
-        const int rows_valid = __builtin_amdgcn_readfirstlane(min(BM, s_off[g + 1] - row0));
-        const bf16_t* __restrict__ W = args.w[g];
-
-        const __amdgpu_buffer_rsrc_t arsrc =
-            GATHER ? __builtin_amdgcn_make_buffer_rsrc((void*)args.a, (short)0, args.a_total * K * 2,
-                                                      RSRC_WORD3)
-                   : __builtin_amdgcn_make_buffer_rsrc((void*)(args.a + (int64_t)row0 * K), (short)0,
-                                                      rows_valid * K * 2, RSRC_WORD3);
-        // per-thread A row offsets; rows past the group fall outside the descriptor
-        int avoff[A_PER];
+        const int s = last_le(s_tstart, n_groups, L);
+        const int rows = s_off[s + 1] - s_off[s];
+        const int mt = (int)ceil_div(rows, BM);
+        const int local = L - s_tstart[s];
+        const int nt = local / mt;
+        const int row0 = s_off[s] + (local - nt * mt) * BM;
+        c.g = __builtin_amdgcn_readfirstlane(s);
+        c.row0 = __builtin_amdgcn_readfirstlane(row0);
+        c.rows_valid = __builtin_amdgcn_readfirstlane(min(BM, s_off[s + 1] - row0));
+        c.n0 = __builtin_amdgcn_readfirstlane(nt) * BN_OUT;
+        c.kt0 = __builtin_amdgcn_readfirstlane(kt0);
+        c.nsteps = __builtin_amdgcn_readfirstlane((int)((int64_t)(kchunk + 1) * KT / S) - kt0);
+        c.u = __builtin_amdgcn_readfirstlane(u);
+        c.split = __builtin_amdgcn_readfirstlane(split ? 1 : 0);
+        return c;
+    };
+    // operand descriptors of a tile: rows past the group's end fall outside the
+    // A descriptor and read as zero; gate and up halves of a SwiGLU weight tile
+    struct Rsrc {
+        __amdgpu_buffer_rsrc_t a, lo, hi;
+    };
+    auto rsrc_of = [&](const Tile& c) {
+        Rsrc r;
+        r.a = GATHER ? __builtin_amdgcn_make_buffer_rsrc((void*)args.a, (short)0, args.a_total * K * 2,
+                                                         RSRC_WORD3)
+                     : __builtin_amdgcn_make_buffer_rsrc((void*)(args.a + (int64_t)c.row0 * K), (short)0,
+                                                         c.rows_valid * K * 2, RSRC_WORD3);
+        const bf16_t* __restrict__ W = args.w[c.g];
+        const int bvalid = min(BN_OUT, args.N - c.n0);
+        const int bup = SWIGLU ? args.up_row + c.n0 : c.n0;
+        r.lo = __builtin_amdgcn_make_buffer_rsrc((void*)(W + (int64_t)c.n0 * K), (short)0,
+                                                 bvalid * K * 2, RSRC_WORD3);
+        r.hi = __builtin_amdgcn_make_buffer_rsrc((void*)(W + (int64_t)bup * K), (short)0,
+                                                 bvalid * K * 2, RSRC_WORD3);
+        return r;
+    };
+    // per-thread A row offsets (GATHER: the token rows of the tile)
+    auto a_offsets = [&](const Tile& c, int* av) {
 #pragma unroll
         for (int i = 0; i < A_PER; ++i) {
             if constexpr (GATHER) {
                 const int rin = (tid >> 3) + ROWS_PER_PASS * i;
-                avoff[i] = rin < rows_valid ? (args.a_rows[row0 + rin] * K + kc) * 2 : A_OOB;
+                av[i] = rin < c.rows_valid ? (args.a_rows[c.row0 + rin] * K + kc) * 2 : A_OOB;
             } else {
-                avoff[i] = voff + i * vstep;
+                av[i] = voff + i * vstep;
             }
         }
-        const int bvalid = min(BN_OUT, args.N - n0);
-        const int bup = SWIGLU ? args.up_row + n0 : n0;
-        const __amdgpu_buffer_rsrc_t brsrc_lo = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)(W + (int64_t)n0 * K), (short)0, bvalid * K * 2, RSRC_WORD3);
-        const __amdgpu_buffer_rsrc_t brsrc_hi = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)(W + (int64_t)bup * K), (short)0, bvalid * K * 2, RSRC_WORD3);
+    };
 
-        uint4 ra[A_PER], rb[B_PER];
-        auto gload = [&](int kt) {
-            const int so = kt * BK * 2;
+    uint4 ra[A_PER], rb[B_PER];
+    auto gload = [&](const Rsrc& r, const int* av, int kt) {
+        const int so = kt * BK * 2;
 #pragma unroll
-            for (int i = 0; i < A_PER; ++i) ra[i] = buffer_load16(arsrc, avoff[i], so);
+        for (int i = 0; i < A_PER; ++i) ra[i] = buffer_load16(r.a, av[i], so);
 #pragma unroll
-            for (int i = 0; i < B_PER; ++i) {
-                if (SWIGLU && i >= B_PER / 2)
-                    rb[i] = buffer_load16(brsrc_hi, voff + (i - B_PER / 2) * vstep, so);
-                else
-                    rb[i] = buffer_load16(brsrc_lo, voff + i * vstep, so);
-            }
-        };
-        // 16-byte chunk c of LDS row r sits at chunk c ^ (r & 7): conflict-free for the
-        // stage stores (8 lanes per row) and for the 16-row fragment reads
-        const int sc = ((tid & 7) ^ ((tid >> 3) & 7)) * 8;
-        auto sstore = [&](int buf) {
+        for (int i = 0; i < B_PER; ++i) {
+            if (SWIGLU && i >= B_PER / 2)
+                rb[i] = buffer_load16(r.hi, voff + (i - B_PER / 2) * vstep, so);
+            else
+                rb[i] = buffer_load16(r.lo, voff + i * vstep, so);
+        }
+    };
+    // 16-byte chunk c of LDS row r sits at chunk c ^ (r & 7): conflict-free for the
+    // stage stores (8 lanes per row) and for the 16-row fragment reads
+    const int sc = ((tid & 7) ^ ((tid >> 3) & 7)) * 8;
+    auto sstore = [&](int buf) {
 #pragma unroll
-            for (int i = 0; i < A_PER; ++i)
-                *(uint4*)&As[buf][((tid >> 3) + ROWS_PER_PASS * i) * TLDK + sc] = ra[i];
+        for (int i = 0; i < A_PER; ++i)
+            *(uint4*)&As[buf][((tid >> 3) + ROWS_PER_PASS * i) * TLDK + sc] = ra[i];
 #pragma unroll
-            for (int i = 0; i < B_PER; ++i)
-                *(uint4*)&Bs[buf][((tid >> 3) + ROWS_PER_PASS * i) * TLDK + sc] = rb[i];
-        };
+        for (int i = 0; i < B_PER; ++i)
+            *(uint4*)&Bs[buf][((tid >> 3) + ROWS_PER_PASS * i) * TLDK + sc] = rb[i];
+    };
 
-        f32x4 acc[MS][NS];
+    f32x4 acc[MS][NS];
+    // v_mfma_f32_16x16x32_bf16 fragments: lane l holds row l % 16 of a 16-row
+    // block and the 8 K elements 8 (l / 16) .. of a 32-wide sub-step, for A and
+    // B alike, so every product sums over the same K
+    const int frow = lane & 15;
+    const int fsw = lane & 7;                         // the swizzle of rows frow (+ 16 m)
+    const int fc0 = ((lane >> 4) ^ fsw) * 8, fc1 = ((4 + (lane >> 4)) ^ fsw) * 8;
+    const bf16_t* a_lds0 = &As[0][(wm * (BM / WAVES_M) + frow) * TLDK];
+    const bf16_t* b_lds0 = &Bs[0][frow * TLDK];
+    // a 32-wide sub-step q runs as two halves (column tiles 0..NH-1, NH..NS-1);
+    // the fragments of the next half are read while the current half multiplies
+    bf16x8 fa0[MS], fa1[MS], fb0[NH], fb1[NH];
+    auto read_a = [&](int buf, int q, bf16x8* fa) {
+#pragma unroll
+        for (int mi = 0; mi < MS; ++mi)
+            fa[mi] = *(const bf16x8*)(a_lds0 + buf * BM * TLDK + mi * 16 * TLDK + (q ? fc1 : fc0));
+    };
+    auto read_b = [&](int buf, int q, int h, bf16x8* fb) {
+#pragma unroll
+        for (int j = 0; j < NH; ++j)
+            fb[j] = *(const bf16x8*)(b_lds0 + buf * BNW * TLDK +
+                                     b_sub_row<SWIGLU>(wn, h * NH + j) * TLDK + (q ? fc1 : fc0));
+    };
+    auto mfma = [&](const bf16x8* fa, const bf16x8* fb, int h) {
+#pragma unroll
+        for (int mi = 0; mi < MS; ++mi)
+#pragma unroll
+            for (int j = 0; j < NH; ++j)
+                acc[mi][h * NH + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    fa[mi], fb[j], acc[mi][h * NH + j], 0, 0, 0);
+    };
+
+    // The workgroup's tiles form one pipeline: while a tile's last K steps run,
+    // the next tile's first stage is loaded (in place of a repeat of the last
+    // stage) and stored to the free LDS buffer, and its second stage is in flight
+    // during the epilogue, so a tile starts without waiting for its operands.
+    // pb: the LDS buffer that holds the current tile's first stage.
+    int i = widx;
+    Tile cur = tile_at(i);
+    Rsrc rc = rsrc_of(cur);
+    int avc[A_PER];
+    a_offsets(cur, avc);
+    int pb = 0;
+    gload(rc, avc, cur.kt0);
+    sstore(0);
+    gload(rc, avc, cur.kt0 + (cur.nsteps > 1 ? 1 : 0));
+    __syncthreads();
+    for (;;) {
+        const int inext = i + nper;
+        const bool has_next = inext < n_mine;
+        const Tile nxt = tile_at(has_next ? inext : i);
+        const Rsrc rn = rsrc_of(nxt);
+        int avn[A_PER];
+        a_offsets(nxt, avn);
+        // what the load after this tile's last stage fetches: the next tile's
+        // first stage, or (last tile) this tile's last stage again (cached)
+        const int kt_after = has_next ? nxt.kt0 : cur.kt0 + cur.nsteps - 1;
+        const int nsteps = cur.nsteps;
+
 #pragma unroll
         for (int mi = 0; mi < MS; ++mi)
 #pragma unroll
@@ -322,48 +417,13 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 #pragma unroll
                 for (int r = 0; r < 4; ++r) acc[mi][jj][r] = 0.f;
 
-        // v_mfma_f32_16x16x32_bf16 fragments: lane l holds row l % 16 of a 16-row
-        // block and the 8 K elements 8 (l / 16) .. of a 32-wide sub-step, for A and
-        // B alike, so every product sums over the same K
-        const int frow = lane & 15;
-        const int fsw = lane & 7;                         // the swizzle of rows frow (+ 16 m)
-        const int fc0 = ((lane >> 4) ^ fsw) * 8, fc1 = ((4 + (lane >> 4)) ^ fsw) * 8;
-        const bf16_t* a_lds0 = &As[0][(wm * (BM / WAVES_M) + frow) * TLDK];
-        const bf16_t* b_lds0 = &Bs[0][frow * TLDK];
-        // a 32-wide sub-step q runs as two halves (column tiles 0..NH-1, NH..NS-1);
-        // the fragments of the next half are read while the current half multiplies
-        bf16x8 fa0[MS], fa1[MS], fb0[NH], fb1[NH];
-        auto read_a = [&](int buf, int q, bf16x8* fa) {
-#pragma unroll
-            for (int mi = 0; mi < MS; ++mi)
-                fa[mi] = *(const bf16x8*)(a_lds0 + buf * BM * TLDK + mi * 16 * TLDK + (q ? fc1 : fc0));
-        };
-        auto read_b = [&](int buf, int q, int h, bf16x8* fb) {
-#pragma unroll
-            for (int j = 0; j < NH; ++j)
-                fb[j] = *(const bf16x8*)(b_lds0 + buf * BNW * TLDK +
-                                         b_sub_row<SWIGLU>(wn, h * NH + j) * TLDK + (q ? fc1 : fc0));
-        };
-        auto mfma = [&](const bf16x8* fa, const bf16x8* fb, int h) {
-#pragma unroll
-            for (int mi = 0; mi < MS; ++mi)
-#pragma unroll
-                for (int j = 0; j < NH; ++j)
-                    acc[mi][h * NH + j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        fa[mi], fb[j], acc[mi][h * NH + j], 0, 0, 0);
-        };
-
-        gload(kt0);
-        sstore(0);
-        gload(kt0 + (nsteps > 1 ? 1 : 0));
-        __syncthreads();
-        read_a(0, 0, fa0);
-        read_b(0, 0, 0, fb0);
+        read_a(pb, 0, fa0);
+        read_b(pb, 0, 0, fb0);
         // Every step but the last runs one straight path, so the MFMAs after the
         // barrier (on fragments read before it) issue without waiting for the
         // next stage's reads; the last step is peeled off below.
         for (int t = 0; t + 1 < nsteps; ++t) {
-            const int buf = t & 1;
+            const int buf = pb ^ (t & 1);
             read_b(buf, 0, 1, fb1);
             mfma(fa0, fb0, 0);
             read_a(buf, 1, fa1);
@@ -399,7 +459,18 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
             }
             __builtin_amdgcn_sched_group_barrier(SG_MFMA, 4, 0);
             __syncthreads();
-            gload(kt0 + (t + 2 < nsteps ? t + 2 : nsteps - 1));
+            {
+                // stage t + 2 of this tile, or what follows its last stage
+                const bool own = t + 2 < nsteps;
+                Rsrc rl;
+                rl.a = own ? rc.a : rn.a;
+                rl.lo = own ? rc.lo : rn.lo;
+                rl.hi = own ? rc.hi : rn.hi;
+                int avl[A_PER];
+#pragma unroll
+                for (int q = 0; q < A_PER; ++q) avl[q] = own ? avc[q] : avn[q];
+                gload(rl, avl, own ? cur.kt0 + t + 2 : kt_after);
+            }
             read_a(buf ^ 1, 0, fa0);
             read_b(buf ^ 1, 0, 0, fb0);
             mfma(fa1, fb1, 1);
@@ -416,24 +487,33 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
                 __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
             }
         }
+        const int lbuf = pb ^ ((nsteps - 1) & 1);
         {
-            const int buf = (nsteps - 1) & 1;
-            read_b(buf, 0, 1, fb1);
+            read_b(lbuf, 0, 1, fb1);
             mfma(fa0, fb0, 0);
-            read_a(buf, 1, fa1);
-            read_b(buf, 1, 0, fb0);
+            read_a(lbuf, 1, fa1);
+            read_b(lbuf, 1, 0, fb0);
             mfma(fa0, fb1, 1);
-            read_b(buf, 1, 1, fb1);
+            read_b(lbuf, 1, 1, fb1);
             mfma(fa1, fb0, 0);
             mfma(fa1, fb1, 1);
         }
+        if (has_next) {
+            // the next tile's first stage into the LDS buffer this tile no longer
+            // reads (with a one-stage tile the registers hold this tile's stage
+            // again: load it first), its second stage into the registers
+            if (nsteps == 1) gload(rn, avn, nxt.kt0);
+            sstore(lbuf ^ 1);
+            gload(rn, avn, nxt.kt0 + (nxt.nsteps > 1 ? 1 : 0));
+        }
         __syncthreads();
 
-        if (split) {
+        if (cur.split) {
             // fp32 partial tile of this K chunk, laid out [row][weight row of the
             // tile]; rows past the group fall outside the descriptor and are dropped
             const __amdgpu_buffer_rsrc_t prsrc = __builtin_amdgcn_make_buffer_rsrc(
-                (void*)(args.part + (int64_t)u * BM * BNW), (short)0, rows_valid * BNW * 4, RSRC_WORD3);
+                (void*)(args.part + (int64_t)cur.u * BM * BNW), (short)0, cur.rows_valid * BNW * 4,
+                RSRC_WORD3);
             const int lbase = ((wm * (BM / WAVES_M) + (lane >> 4) * 4) * BNW +
                                b_sub_row<SWIGLU>(wn, 0) + (lane & 15)) * 4;
 #pragma unroll
@@ -446,36 +526,51 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
                         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[mi][jj][r]), prsrc,
                                                               lbase, off, 0);
                     }
-            continue;
-        }
-
-        // epilogue: accumulator element r of a 16x16 tile sits at
-        // row 4*(lane/16) + r, column lane%16
-        const int col_in = lane & 15;
+        } else {
+            // epilogue: accumulator element r of a 16x16 tile sits at row 4 (lane / 16)
+            // + r, column lane % 16; a 4 x 4 transpose inside each lane quad gives
+            // lane 4 b + e of row group a the row 4 a + e, columns 4 b .. 4 b + 3,
+            // stored as one 8-byte vector (a quarter of the store instructions of
+            // 2-byte stores, whole 32-byte row segments per lane quad)
+            const int qa = lane >> 4, qb = (lane >> 2) & 3, qe = lane & 3;
 #pragma unroll
-        for (int mi = 0; mi < MS; ++mi) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row_in = wm * (BM / WAVES_M) + mi * 16 + (lane >> 4) * 4 + r;
-                if (row_in >= rows_valid) continue;
-                bf16_t* orow = args.out + (int64_t)(row0 + row_in) * args.ldo;
+            for (int mi = 0; mi < MS; ++mi) {
+                const int row_in = wm * (BM / WAVES_M) + mi * 16 + qa * 4 + qe;
+                const bool row_ok = row_in < cur.rows_valid;
+                bf16_t* orow = args.out + (int64_t)(cur.row0 + row_in) * args.ldo;
                 if (SWIGLU) {
                     constexpr int HW = BNW / 2 / WAVES_N;
 #pragma unroll
                     for (int j = 0; j < NS / 2; ++j) {
-                        const int col = n0 + wn * HW + j * 16 + col_in;
-                        if (col < args.N)
-                            orow[col] = f32_to_bf16(silu(acc[mi][j][r]) * acc[mi][NS / 2 + j][r]);
+                        float v[4];
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) v[r] = silu(acc[mi][j][r]) * acc[mi][NS / 2 + j][r];
+                        quad_transpose(v, lane);
+                        const int col = cur.n0 + wn * HW + j * 16 + qb * 4;
+                        if (row_ok && col < args.N)
+                            *(uint2*)(orow + col) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
                     }
                 } else {
 #pragma unroll
                     for (int jj = 0; jj < NS; ++jj) {
-                        const int col = n0 + wn * (BNW / WAVES_N) + jj * 16 + col_in;
-                        if (col < args.N) orow[col] = f32_to_bf16(acc[mi][jj][r]);
+                        float v[4];
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) v[r] = acc[mi][jj][r];
+                        quad_transpose(v, lane);
+                        const int col = cur.n0 + wn * (BNW / WAVES_N) + jj * 16 + qb * 4;
+                        if (row_ok && col < args.N)
+                            *(uint2*)(orow + col) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
                     }
                 }
             }
         }
+        if (!has_next) break;
+        i = inext;
+        cur = nxt;
+        rc = rn;
+#pragma unroll
+        for (int q = 0; q < A_PER; ++q) avc[q] = avn[q];
+        pb = lbuf ^ 1;
     }
 }
 
