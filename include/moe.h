@@ -54,6 +54,7 @@ extern "C" {
 #define MOE_FFN_GATE_UP 1   /* h = SiLU(W1 x) * (W3 x), kept in the workspace */
 #define MOE_FFN_DOWN    2   /* y = W2 h, from the workspace */
 #define MOE_FFN_SMALL_GROUPS 4   /* hint: no group has more than 256 rows; all are streamed */
+#define MOE_FFN_LARGE_GROUPS 8   /* hint: every non-empty group has more than 256 rows; none is streamed */
 
 /* flags of moe_route_topk */
 #define MOE_RENORM    1   /* gates = softmax over the k selected logits (else: full softmax, restricted) */
@@ -241,6 +242,14 @@ int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets,
  * sums its products in another order (same tolerance).  Rows of a group that
  * breaks the statement are left unwritten.  It must be passed the same way to
  * the MOE_FFN_GATE_UP and the MOE_FFN_DOWN call of one pair.
+ * Adding MOE_FFN_LARGE_GROUPS instead states that every non-empty group holds
+ * more than 256 rows (true of a shared expert's call over more than 256
+ * tokens): every group then takes the tiled kernels and the call skips the
+ * weight-streaming launches.  Such a call gives bitwise the outputs it gives
+ * without the flag; a group that breaks the statement is still computed in
+ * full, by the tiled kernels (its products summed in another order, same
+ * tolerance).  It must be passed the same way to both calls of a pair; the
+ * two hints together give MOE_ERR_ARG.
  */
 int moe_grouped_ffn_products(const void* x_perm, int dtype, const int32_t* group_offsets,
                              int n_groups, const void* const* w13, const void* const* w2, int d,

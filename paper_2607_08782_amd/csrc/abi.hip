@@ -168,7 +168,9 @@ int ffn_check(const void* x_perm, int dtype, const int32_t* group_offsets, int n
               const void* const* w13, const void* const* w2, int d, int f, int64_t cap_rows,
               const void* y_perm, const void* ws, size_t ws_bytes, int products) {
     if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
-    if (products & ~(MOE_FFN_GATE_UP | MOE_FFN_DOWN | MOE_FFN_SMALL_GROUPS)) return MOE_ERR_ARG;
+    if (products & ~(MOE_FFN_GATE_UP | MOE_FFN_DOWN | MOE_FFN_SMALL_GROUPS | MOE_FFN_LARGE_GROUPS))
+        return MOE_ERR_ARG;
+    if ((products & MOE_FFN_SMALL_GROUPS) && (products & MOE_FFN_LARGE_GROUPS)) return MOE_ERR_ARG;
     const bool up = products & MOE_FFN_GATE_UP, down = products & MOE_FFN_DOWN;
     if (!up && !down) return MOE_ERR_ARG;
     if (n_groups < 1 || n_groups > MOE_MAX_GROUPS || d < 1 || f < 1 || cap_rows < 0)

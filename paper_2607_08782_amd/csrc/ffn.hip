@@ -1130,6 +1130,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     // streamed, so no tile, no split tile and no row limit to pass on, and the tiled
     // launches are left out
     const bool small = (products & MOE_FFN_SMALL_GROUPS) != 0;
+    // every non-empty group above SMALL_ROWS_MAX rows (the caller's statement): none is
+    // streamed, every group is tiled (row limit 0) and the streaming launches are left out
+    const bool large = (products & MOE_FFN_LARGE_GROUPS) != 0;
     if (dtype == MOE_F32) {
         PtrTable t13, t2;
         for (int i = 0; i < MOE_MAX_GROUPS; ++i) {
@@ -1181,9 +1184,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     a1.ldo = f;
     a1.up_row = f;
     a1.n_tiles = (int)ceil_div(f, BNW / 2);
-    a1.limits = tinfo ? tinfo + 2 : nullptr;
+    a1.limits = tinfo && !large ? tinfo + 2 : nullptr;
     a1.product = 0;
-    a1.lim0 = small ? SMALL_ROWS_MAX : SMALL_ROWS;
+    a1.lim0 = small ? SMALL_ROWS_MAX : large ? 0 : SMALL_ROWS;
     a1.down_tiles = (int)ceil_div(d, BNW);
     a1.part = tpart;
     a1.split_info = tinfo;
@@ -1212,9 +1215,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s1.product = 0;
     s1.lim0 = a1.lim0;
     if (up) {
-        if (a_rows)
+        if (!large && a_rows)
             hipLaunchKernelGGL(stream_gemm_kernel<true>, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
-        else
+        else if (!large)
             hipLaunchKernelGGL(stream_gemm_kernel<false>, dim3(sgrid), dim3(ST_THREADS), 0, s, s1);
         hipLaunchKernelGGL(split_reduce_kernel<true>, dim3(rgrid), dim3(ST_THREADS), 0, s, s1, a1);
     }
@@ -1245,7 +1248,8 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     s2.ldo = d;
     s2.a_rows = nullptr;
     s2.product = 1;
-    hipLaunchKernelGGL(stream_gemm_kernel<false>, dim3(sgrid), dim3(ST_THREADS), 0, s, s2);
+    if (!large)
+        hipLaunchKernelGGL(stream_gemm_kernel<false>, dim3(sgrid), dim3(ST_THREADS), 0, s, s2);
     if (combine == nullptr) {
         hipLaunchKernelGGL(split_reduce_kernel<false>, dim3(rgrid), dim3(ST_THREADS), 0, s, s2, a2);
         return launch_status();

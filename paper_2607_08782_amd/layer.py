@@ -130,6 +130,11 @@ class LayerShare:
         # the fused chunk sum, k x S partial loads per output element, is slower than
         # the chunk sum plus the combine launch); True: whenever the call streams
         # every group; False: never
+        # the shared experts' call is one group of T rows: above 256 rows it is tiled
+        # whole and its streaming launches are left out (MOE_FFN_LARGE_GROUPS)
+        self.shared_products = self.ffn_products
+        if T > 256:
+            self.shared_products |= moe.MOE_FFN_LARGE_GROUPS
         can_fuse = (bool(self.ffn_products & moe.MOE_FFN_SMALL_GROUPS) and dt == torch.bfloat16
                     and not gather_in_ffn and self.weights is not None)
         if fuse_combine is None:
@@ -165,7 +170,7 @@ class LayerShare:
     def _shared_ffn(self, stream=None):
         moe.moe_grouped_ffn(self.X, self.shared_offsets, self.shared_weights, cap_rows=self.T,
                             y_perm=self.y_shared, ws=self.ws_shared, stream=stream,
-                            products=self.ffn_products)
+                            products=self.shared_products)
 
     def package(self):
         """Enqueue the packaging step as `run` makes it (moe_permute; the row copy

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libmoe.so")
 MOE_F32, MOE_BF16 = 0, 1
 MOE_OK, MOE_ERR_ARG, MOE_ERR_PLACEMENT, MOE_ERR_SHAPE, MOE_ERR_DEVICE = 0, 1, 2, 3, 4
 MOE_RENORM, MOE_LOGITS_IN = 1, 2
-MOE_FFN_GATE_UP, MOE_FFN_DOWN, MOE_FFN_SMALL_GROUPS = 1, 2, 4
+MOE_FFN_GATE_UP, MOE_FFN_DOWN, MOE_FFN_SMALL_GROUPS, MOE_FFN_LARGE_GROUPS = 1, 2, 4, 8
 MOE_MAX_E, MOE_MAX_K, MOE_MAX_G, MOE_MAX_GROUPS = 256, 16, 64, 128
 MOE_PERMUTE_NOALLOC_MAX_WS = 4 << 20
 

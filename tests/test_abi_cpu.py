@@ -161,6 +161,8 @@ def test_grouped_ffn_products_validation(lib):
     assert call(products=0) == moe.MOE_ERR_ARG
     assert call(products=4) == moe.MOE_ERR_ARG                    # a hint alone runs nothing
     assert call(products=8) == moe.MOE_ERR_ARG
+    assert call(products=3 | 4 | 8) == moe.MOE_ERR_ARG            # the two hints contradict
+    assert call(products=1 | 16) == moe.MOE_ERR_ARG               # no such flag
     assert call(products=1, x=None) == moe.MOE_ERR_ARG           # gate/up reads x_perm
     assert call(products=1, w13=None) == moe.MOE_ERR_ARG
     assert call(products=2, y=None) == moe.MOE_ERR_ARG           # down writes y_perm

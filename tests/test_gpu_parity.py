@@ -475,6 +475,64 @@ def test_small_groups_hint_leaves_the_outputs_bitwise_unchanged(name, regime):
         assert torch.equal(plain[:T], share.y_shared[:T])
 
 
+@pytest.mark.parametrize("name,regime", [("deepseek_v2_lite", "prefill"), ("qwen15_moe_a27b", "batch")])
+def test_large_groups_hint_leaves_the_shared_call_bitwise_unchanged(name, regime):
+    """The shared experts' call over T > 256 tokens (one group of T rows) takes
+    MOE_FFN_LARGE_GROUPS in LayerShare.run: no streaming launches, bitwise the call
+    without the hint."""
+    cfg = synth.CONFIGS[name]
+    T = cfg.T(regime)
+    say("[large groups]", name, regime, "T=%d" % T)
+    inp = synth.make_layer(cfg, T, seed=4, device="cuda")
+    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                       shared=inp.shared, coact=cfg.coact)
+    assert share.shared_products & moe.MOE_FFN_LARGE_GROUPS
+    share.run()
+    torch.cuda.synchronize()
+    plain = torch.empty_like(share.y_shared)
+    moe.moe_grouped_ffn(share.X, share.shared_offsets, share.shared_weights, cap_rows=share.T,
+                        y_perm=plain, ws=share.ws_shared)
+    torch.cuda.synchronize()
+    assert torch.equal(plain[:T], share.y_shared[:T])
+
+
+def test_large_groups_hint_broken_still_computes_every_group():
+    """MOE_FFN_LARGE_GROUPS on groups that break it (empty, 1, 40, 64, 65, 200 and
+    700 rows): every group goes to the tiled kernel instead of streaming and must
+    still match the oracle; two runs agree bit for bit."""
+    sizes = [0, 1, 40, 64, 65, 200, 700]
+    E = len(sizes)
+    cfg = synth.custom_config(d=256, E=E, k=1, f=192, G=1)
+    T = sum(sizes)
+    owner = np.repeat(np.arange(E), sizes)
+    np.random.default_rng(11).shuffle(owner)
+    L = np.zeros((T, E), np.float32)
+    L[np.arange(T), owner] = 1.0
+    inp, share = _share(cfg, T)
+    share.run(logits_in=torch.from_numpy(L).cuda())
+    torch.cuda.synchronize()
+    go = share.perm["group_offsets"].cpu().numpy()
+    assert np.diff(go).tolist() == sizes
+    hinted = moe.MOE_FFN_GATE_UP | moe.MOE_FFN_DOWN | moe.MOE_FFN_LARGE_GROUPS
+    outs = []
+    for _ in range(2):
+        share.y_perm.fill_(7.0)
+        moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
+                            cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn,
+                            products=hinted)
+        torch.cuda.synchronize()
+        outs.append(share.y_perm[:T].clone())
+    assert torch.equal(outs[0], outs[1])
+    X = np32(inp.X)
+    idx, gate = oracle.topk(L, 1)
+    pm = oracle.permute(X, idx, gate, E, inp.placement, 0)
+    for s in range(E):
+        if sizes[s]:
+            ref = oracle.expert_ffn(pm["x_perm"][go[s]:go[s + 1]], np32(share.weights.w13[s]),
+                                    np32(share.weights.w2[s]))
+            close(np32(outs[0][go[s]:go[s + 1]]), ref, OUT_TOL["bf16"], "group %d" % s)
+
+
 FUSED = [("mixtral_8x7b", "decode", None), ("qwen3_30b_a3b", "decode", None),
          ("shared_T50", "batch", synth.custom_config(d=256, E=16, k=4, f=256, shared_f=(128, 64),
                                                      G=3, replicas=2, zipf=1.2, T=50)),
