@@ -28,6 +28,8 @@
 namespace moe {
 namespace {
 
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
 constexpr int BM = 256;          // rows per tile
 constexpr int BNW = 256;         // weight rows per tile
 constexpr int BK = 64;           // K per stage
@@ -531,13 +533,20 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
             // + r, column lane % 16; a 4 x 4 transpose inside each lane quad gives
             // lane 4 b + e of row group a the row 4 a + e, columns 4 b .. 4 b + 3,
             // stored as one 8-byte vector (a quarter of the store instructions of
-            // 2-byte stores, whole 32-byte row segments per lane quad)
+            // 2-byte stores, whole 32-byte row segments per lane quad) through a
+            // descriptor over the tile's rows (rows past the group are dropped)
             const int qa = lane >> 4, qb = (lane >> 2) & 3, qe = lane & 3;
+            const __amdgpu_buffer_rsrc_t orsrc = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(args.out + (int64_t)cur.row0 * args.ldo), (short)0,
+                cur.rows_valid * args.ldo * 2, RSRC_WORD3);
+            auto store4 = [&](const float* v, int row_in, int col) {
+                const uint2 w = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, w), orsrc,
+                                                      (row_in * args.ldo + col) * 2, 0, 0);
+            };
 #pragma unroll
             for (int mi = 0; mi < MS; ++mi) {
                 const int row_in = wm * (BM / WAVES_M) + mi * 16 + qa * 4 + qe;
-                const bool row_ok = row_in < cur.rows_valid;
-                bf16_t* orow = args.out + (int64_t)(cur.row0 + row_in) * args.ldo;
                 if (SWIGLU) {
                     constexpr int HW = BNW / 2 / WAVES_N;
 #pragma unroll
@@ -547,8 +556,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
                         for (int r = 0; r < 4; ++r) v[r] = silu(acc[mi][j][r]) * acc[mi][NS / 2 + j][r];
                         quad_transpose(v, lane);
                         const int col = cur.n0 + wn * HW + j * 16 + qb * 4;
-                        if (row_ok && col < args.N)
-                            *(uint2*)(orow + col) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+                        if (col < args.N) store4(v, row_in, col);
                     }
                 } else {
 #pragma unroll
@@ -558,8 +566,7 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
                         for (int r = 0; r < 4; ++r) v[r] = acc[mi][jj][r];
                         quad_transpose(v, lane);
                         const int col = cur.n0 + wn * (BNW / WAVES_N) + jj * 16 + qb * 4;
-                        if (row_ok && col < args.N)
-                            *(uint2*)(orow + col) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+                        if (col < args.N) store4(v, row_in, col);
                     }
                 }
             }
