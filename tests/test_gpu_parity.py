@@ -49,6 +49,10 @@ SMALL = {
                                          coact=True), 150),
     "bf16_k12": (synth.custom_config(d=64, E=40, k=12, f=64, shared_f=(64,), G=2, replicas=1,
                                      zipf=1.0), 300),
+    # the largest expert count, k and local group count the boundary takes (MOE_MAX_E = 256,
+    # MOE_MAX_K = 16, 128 local slots = MOE_MAX_GROUPS), co-activation past the LDS bins
+    "bf16_E256_k16_128_groups": (synth.custom_config(d=128, E=256, k=16, f=64, G=2, zipf=1.1,
+                                                     coact=True), 300),
 }
 
 
