@@ -537,6 +537,33 @@ def test_large_groups_hint_broken_still_computes_every_group():
             close(np32(outs[0][go[s]:go[s + 1]]), ref, OUT_TOL["bf16"], "group %d" % s)
 
 
+@pytest.mark.parametrize("d,f,group_rows", [(64, 64, 5000), (128, 64, 6000), (64, 128, 5000)])
+def test_many_short_k_tiles_per_workgroup(d, f, group_rows):
+    """One and two K stages per tile (K = 64 or 128) with more tiles than workgroups:
+    each workgroup runs several tiles back to back, so the next tile's first stages
+    are loaded during the last step of the one before (and with one stage per tile,
+    in the peeled step).  Every group against the oracle, two runs bit for bit."""
+    n = 16
+    sizes = [group_rows + 37 * s for s in range(n)]          # ragged last m-tiles
+    N = sum(sizes)
+    say("[short-K tiles]", "d", d, "f", f, "rows", N)
+    cfg = synth.custom_config(d=d, E=n, k=1, f=f, G=1)
+    x = synth.normal((N, d), 21, "x", 0, 1.0, "cuda", torch.bfloat16)
+    ws = [synth.expert_weights(cfg, s, 21, "cuda") for s in range(n)]
+    table = moe.WeightTable([a for a, _ in ws], [b for _, b in ws])
+    offs = torch.tensor(np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32), device="cuda")
+    outs = []
+    for _ in range(2):
+        outs.append(moe.moe_grouped_ffn(x, offs, table, cap_rows=N).clone())
+        torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])
+    X = np32(x)
+    go = offs.cpu().numpy()
+    for s in range(n):
+        ref = oracle.expert_ffn(X[go[s]:go[s + 1]], np32(ws[s][0]), np32(ws[s][1]))
+        close(np32(outs[0][go[s]:go[s + 1]]), ref, OUT_TOL["bf16"], "group %d" % s)
+
+
 FUSED = [("mixtral_8x7b", "decode", None), ("qwen3_30b_a3b", "decode", None),
          ("shared_T50", "batch", synth.custom_config(d=256, E=16, k=4, f=256, shared_f=(128, 64),
                                                      G=3, replicas=2, zipf=1.2, T=50)),
