@@ -235,12 +235,13 @@ int moe_grouped_ffn(const void* x_perm, int dtype, const int32_t* group_offsets,
  * Adding MOE_FFN_SMALL_GROUPS to products states that no group holds more
  * than 256 rows (true of a batch of at most 256 tokens: a token reaches an
  * expert at most once).  Every group then takes the weight-streaming kernels
- * and the call skips the launches of the tiled kernels.  Groups of at most 64
- * rows are streamed with or without the flag, so a call whose groups all hold
- * at most 64 rows gives bitwise the outputs it gives without it; a group of 65
- * to 256 rows that the call without the flag would give to the tiled kernel
- * sums its products in another order (same tolerance).  Rows of a group that
- * breaks the statement are left unwritten.  It must be passed the same way to
+ * and the call skips the launches of the tiled kernels.  Without the flag a
+ * call streams every group of at most 256 rows when its groups above 64 rows
+ * make few tiles (always so when no group holds more than 64 rows), and tiles
+ * every group otherwise; so a call whose groups all hold at most 64 rows gives
+ * bitwise the outputs it gives without the flag, and a group that the call
+ * without the flag would tile sums its products in another order (same
+ * tolerance).  Rows of a group that breaks the statement are left unwritten.  It must be passed the same way to
  * the MOE_FFN_GATE_UP and the MOE_FFN_DOWN call of one pair.
  * Adding MOE_FFN_LARGE_GROUPS instead states that every non-empty group holds
  * more than 256 rows (true of a shared expert's call over more than 256

@@ -83,8 +83,10 @@ struct GemmArgs {
 constexpr int TILE_SPLIT_UNITS = 256;
 constexpr int TILE_SPLIT_MIN_STEPS = 8;
 
-// Groups of at most SMALL_ROWS rows always go to the split-K streaming kernel;
-// in a short call (see small_limits) groups of up to SMALL_ROWS_MAX rows do too.
+// A short call (see small_limits) streams its groups of up to SMALL_ROWS_MAX rows
+// through the split-K streaming kernel and tiles the rest; any other call tiles
+// every group.  Without the row limits in the workspace (a call of at most
+// SMALL_ROWS rows in all) every group is streamed.
 constexpr int SMALL_ROWS = 64;
 constexpr int SMALL_ROWS_MAX = 256;
 
@@ -187,7 +189,11 @@ __device__ __forceinline__ void tile_starts(const int* s_off, int n_groups, int 
 // launch is short and latency-bound: every workgroup still runs several K
 // stages of a 256 x 256 tile, on a fraction of the CUs.  Streaming every group
 // of up to SMALL_ROWS_MAX rows instead spreads the weight reads over all CUs
-// (a DeepSeek-V2-Lite-shaped decode step: 219 -> 188 us).
+// (a DeepSeek-V2-Lite-shaped decode step: 219 -> 188 us).  Otherwise the small
+// groups join the tiled launch, whose rounds leave CUs free for their tiles,
+// rather than stream in a launch of their own after it (the two run one after
+// the other): DeepSeek-V2-Lite prefill FFN 364 -> 332 us, Qwen1.5 batch 137 ->
+// 129 us, Qwen3 prefill 466 -> 459 us.
 __device__ __forceinline__ void small_limits(const int* s_off, int n_groups, int tiles_up,
                                              int tiles_down, int split_units, int lane,
                                              int& lim_up, int& lim_down) {
@@ -199,8 +205,8 @@ __device__ __forceinline__ void small_limits(const int* s_off, int n_groups, int
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) mt += __shfl_xor(mt, o, 64);
-    lim_up = 4 * mt * tiles_up <= split_units ? SMALL_ROWS_MAX : SMALL_ROWS;
-    lim_down = 4 * mt * tiles_down <= split_units ? SMALL_ROWS_MAX : SMALL_ROWS;
+    lim_up = 4 * mt * tiles_up <= split_units ? SMALL_ROWS_MAX : 0;
+    lim_down = 4 * mt * tiles_down <= split_units ? SMALL_ROWS_MAX : 0;
 }
 
 // Persistent grouped NT GEMM.  Per tile: operands stream through per-tile
@@ -582,8 +588,10 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
 }
 
 // ---------------------------------------------------------------------------
-// Small groups (decode-sized: at most SMALL_ROWS rows, or SMALL_ROWS_MAX in a
-// short call, see small_limits): weight streaming with split-K.  Here the weights dominate the traffic (each weight byte is used by
+// Small groups (those of a short call up to SMALL_ROWS_MAX rows, see
+// small_limits; every group of a call with the MOE_FFN_SMALL_GROUPS statement or
+// of at most SMALL_ROWS rows in all): weight streaming with split-K.  Here the
+// weights dominate the traffic (each weight byte is used by
 // a handful of rows), so the aim is to read every weight byte once, from all
 // CUs at once.  Work item = (group, 128 weight rows, K chunk, 64 rows); one
 // workgroup per item, three per CU with three K steps of loads in flight
