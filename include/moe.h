@@ -209,7 +209,7 @@ size_t moe_grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n
  *                256-byte aligned
  * For MOE_BF16 the products accumulate in fp32 and h is rounded to bf16
  * before the second product.  Requires 1 <= n_groups <= MOE_MAX_GROUPS and
- * for MOE_BF16 d % 64 == 0 and f % 64 == 0.
+ * for MOE_BF16 d % 64 == 0, f % 64 == 0 and d, f < 2^22 (else MOE_ERR_SHAPE).
  * A shared (always-on) expert is the call with x_perm = x, one group and
  * group_offsets = {0, T}.
  */

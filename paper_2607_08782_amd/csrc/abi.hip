@@ -182,6 +182,9 @@ int ffn_check(const void* x_perm, int dtype, const int32_t* group_offsets, int n
     if (cap_rows > 0 && ((up && !x_perm) || (down && !y_perm))) return MOE_ERR_ARG;
     if (dtype == MOE_BF16) {
         if (d % 64 || f % 64) return MOE_ERR_SHAPE;
+        // a 256-row tile of either product spans 256 rows of d or f elements in 32-bit
+        // byte offsets
+        if ((int64_t)d * 512 > 0x7fffffffLL || (int64_t)f * 512 > 0x7fffffffLL) return MOE_ERR_SHAPE;
         if ((x_perm && !aligned16(x_perm)) || (y_perm && !aligned16(y_perm))) return MOE_ERR_ARG;
         for (int s = 0; s < n_groups; ++s)
             if ((up && !aligned16(w13[s])) || (down && !aligned16(w2[s]))) return MOE_ERR_ARG;

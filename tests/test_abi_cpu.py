@@ -168,6 +168,8 @@ def test_grouped_ffn_products_validation(lib):
     assert call(products=2, y=None) == moe.MOE_ERR_ARG           # down writes y_perm
     assert call(products=2, w2=None) == moe.MOE_ERR_ARG
     assert call(products=3, d=100) == moe.MOE_ERR_SHAPE
+    assert call(products=3, d=1 << 22) == moe.MOE_ERR_SHAPE          # tile offsets past 32 bits
+    assert call(products=3, f_=1 << 22) == moe.MOE_ERR_SHAPE
     assert call(products=2, ws_bytes=10) == moe.MOE_ERR_SHAPE
 
 
