@@ -254,8 +254,10 @@ int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int
     if (cap_rows > 0 && (!x || !row_token || !y_perm || T < 1)) return MOE_ERR_ARG;
     if (dtype == MOE_BF16) {
         if (d % 64 || f % 64) return MOE_ERR_SHAPE;
-        // token rows are addressed through 32-bit buffer offsets
+        // token rows are addressed through 32-bit buffer offsets, and so is a
+        // 256-row tile of either product
         if (T * (int64_t)d * 2 > 0x7fffffffLL) return MOE_ERR_SHAPE;
+        if ((int64_t)d * 512 > 0x7fffffffLL || (int64_t)f * 512 > 0x7fffffffLL) return MOE_ERR_SHAPE;
         if (!aligned16(x) || !aligned16(y_perm)) return MOE_ERR_ARG;
         for (int s = 0; s < n_groups; ++s)
             if (!aligned16(w13[s]) || !aligned16(w2[s])) return MOE_ERR_ARG;

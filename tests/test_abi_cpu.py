@@ -223,6 +223,7 @@ def test_grouped_ffn_rows_validation(lib):
     assert call(T=0) == moe.MOE_ERR_ARG                     # rows to compute but no token rows
     assert call(T=1 << 24, d=128) == moe.MOE_ERR_SHAPE      # T*d*2 past 32-bit row offsets
     assert call(d=100) == moe.MOE_ERR_SHAPE
+    assert call(T=1, f_=1 << 22) == moe.MOE_ERR_SHAPE        # a tile's offsets past 32 bits
     assert call(x=FAKE.value + 8) == moe.MOE_ERR_ARG        # bf16 rows not 16-byte aligned
     assert call(ws_bytes=10) == moe.MOE_ERR_SHAPE
     assert call(dtype=3) == moe.MOE_ERR_ARG
