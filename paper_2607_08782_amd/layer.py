@@ -8,10 +8,11 @@ with no host synchronisation in between (decode-sized batches stream every
 expert group and skip the tiled GEMM launches; at most 64 tokens with k <= 2 the
 last two calls are one, moe_grouped_ffn_combine).  The shared experts' FFN
 (moe_grouped_ffn over every token), which does not depend on the routing,
-runs on a second stream forked from the current one and joined back before
-the combine, so it overlaps the short routing and packaging launches; the
-fork and join are stream events, so a graph capture of `run` holds both
-branches.  The expert placement can be
+runs on a second stream forked from the current one after the packaging step
+and joined back before the combine, so it overlaps the routed experts' FFN
+(whose launches leave CUs idle) without holding CUs the routing launches wait
+for; the fork and join are stream events, so a graph capture of `run` holds
+both branches.  The expert placement can be
 swapped between batches (`set_placement`) by re-pointing the weight table;
 nothing is reallocated.
 """
@@ -205,21 +206,34 @@ class LayerShare:
         [T, d], complete on the current stream (the shared experts' branch, if
         any, is joined back before the combine)."""
         main = torch.cuda.current_stream(self.device)
-        if self._side is not None:
+
+        def fork_shared():
             self._fork.record(main)
             self._side.wait_event(self._fork)
             self._shared_ffn(self._side)
             self._join.record(self._side)
-        self.route(logits_in)
-        moe.moe_expert_histogram(self.topk_idx, self.E, counts=self.counts, coact=self.coact)
-        self.package()
+
         if self.fused_combine:
+            # the fused call reads y_shared: the shared branch overlaps the routing
+            if self._side is not None:
+                fork_shared()
+            self.route(logits_in)
+            moe.moe_expert_histogram(self.topk_idx, self.E, counts=self.counts, coact=self.coact)
+            self.package()
             if self._side is not None:
                 main.wait_event(self._join)
             elif self.shared_weights is not None:
                 self._shared_ffn()
             self.routed_ffn()
             return self.y
+        self.route(logits_in)
+        moe.moe_expert_histogram(self.topk_idx, self.E, counts=self.counts, coact=self.coact)
+        self.package()
+        # the shared branch forks after the routing launches, which would otherwise
+        # wait for CUs held by its GEMMs, and overlaps the routed experts' FFN, whose
+        # launches leave CUs idle
+        if self._side is not None:
+            fork_shared()
         self.routed_ffn()
         if self._side is not None:
             main.wait_event(self._join)
