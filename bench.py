@@ -109,6 +109,8 @@ def ffn_call(share, products=None):
     if share.gather_in_ffn:
         raise ValueError("a share that gathers its rows in the FFN has no x_perm to run "
                          "single products on")
+    # with the share's own hints, as its step passes them to the whole call
+    products |= share.ffn_products & (moe.MOE_FFN_SMALL_GROUPS | moe.MOE_FFN_LARGE_GROUPS)
     return lambda: moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"],
                                        share.weights, cap_rows=share.cap_rows, y_perm=share.y_perm,
                                        ws=share.ws_ffn, products=products)
@@ -121,6 +123,8 @@ def ffn_label(share):
                 "down product's chunk sum)")
     if share.ffn_products & moe.MOE_FFN_SMALL_GROUPS:
         return "moe_grouped_ffn call (weight-streaming launches, chunk sums)"
+    if share.ffn_products & moe.MOE_FFN_LARGE_GROUPS:
+        return "moe_grouped_ffn call (gate/up and down tiled GEMMs, chunk sums; every group tiled)"
     return "moe_grouped_ffn call (gate/up and down tiled GEMMs, streaming launches, chunk sums)"
 
 
@@ -223,8 +227,9 @@ def measure(name, regime, steps, warmup, seed=0, dominant=False, eager=False):
         out.update(rows_here=work["N"], active_experts=work["active"], group_rows=work["sizes"])
         out["ffn_ms"] = time_replays([capture(ffn_call(s)) for s in shares], steps, warmup)
         if dominant:
-            # the gate/up product alone: the tiled GEMM plus its (empty at this size)
-            # streaming launch and chunk sum, on the packaged rows
+            # the gate/up product alone: the tiled GEMM and its chunk sum (the share's
+            # hint leaves out the streaming launch when every group is tiled), on the
+            # packaged rows
             pshares = shares
             if s0.gather_in_ffn:
                 # the same weight copies, packaged

@@ -125,6 +125,13 @@ class LayerShare:
         self.ffn_products = moe.MOE_FFN_GATE_UP | moe.MOE_FFN_DOWN
         if T <= 64 or (T <= 256 and T * k <= 64 * self.E):
             self.ffn_products |= moe.MOE_FFN_SMALL_GROUPS
+        # when the mean group is at least 512 rows, a call short enough to stream its
+        # groups (at most a quarter of the CUs' worth of tiles in its groups above 64
+        # rows) would need this GPU's experts to get a small fraction of their share:
+        # every group is tiled and the streaming launches, which would find nothing to
+        # do, are left out (a hint only: any group sizes give correct results)
+        elif T * k >= 512 * self.E:
+            self.ffn_products |= moe.MOE_FFN_LARGE_GROUPS
         # ... and then the combine can run inside the down product's chunk sum
         # (moe_grouped_ffn_combine: y_perm is not written).  fuse_combine None: where
         # it measured faster, batches of at most 64 tokens with k <= 2 (at k = 6 or 8
@@ -133,7 +140,7 @@ class LayerShare:
         # every group; False: never
         # the shared experts' call is one group of T rows: above 256 rows it is tiled
         # whole and its streaming launches are left out (MOE_FFN_LARGE_GROUPS)
-        self.shared_products = self.ffn_products
+        self.shared_products = self.ffn_products & ~moe.MOE_FFN_LARGE_GROUPS
         if T > 256:
             self.shared_products |= moe.MOE_FFN_LARGE_GROUPS
         can_fuse = (bool(self.ffn_products & moe.MOE_FFN_SMALL_GROUPS) and dt == torch.bfloat16
