@@ -21,7 +21,11 @@
 //   The grid is persistent (one workgroup per CU).  Tiles are ordered
 //   (group, n-tile, m-tile) and cut into eight contiguous chunks, one per XCD
 //   (workgroups are dispatched round-robin over the XCDs), so the workgroups
-//   sharing an L2 also share weight tiles.  Group sizes are read on the
+//   sharing an L2 also share weight tiles.  A workgroup's tiles form one load
+//   pipeline: the next tile's first stages are loaded during the current
+//   tile's last step, so a tile starts without waiting for its operands.  The
+//   epilogue stores 8 bytes per lane (four columns of one row, gathered by a
+//   4 x 4 transpose inside each lane quad).  Group sizes are read on the
 //   device; empty groups produce no tiles, so their weights are never read.
 #include "common.h"
 
