@@ -305,6 +305,21 @@ int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int
                          void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * moe_grouped_ffn_rows_products -- moe_grouped_ffn_rows with the products mask of
+ * moe_grouped_ffn_products (one product at a time, and the MOE_FFN_SMALL_GROUPS
+ * or MOE_FFN_LARGE_GROUPS statement, with the same meaning and the same
+ * outputs): x and row_token are read only with MOE_FFN_GATE_UP (may be NULL
+ * otherwise), y_perm and w2 only with MOE_FFN_DOWN.  Other arguments,
+ * requirements and errors as for moe_grouped_ffn_rows; MOE_FFN_GATE_UP |
+ * MOE_FFN_DOWN is exactly moe_grouped_ffn_rows.
+ */
+int moe_grouped_ffn_rows_products(const void* x, int64_t T, const int32_t* row_token, int dtype,
+                                  const int32_t* group_offsets, int n_groups,
+                                  const void* const* w13, const void* const* w2, int d, int f,
+                                  int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes,
+                                  int products, void* stream);
+
+/*
  * moe_combine -- gate-weighted sum of the experts' outputs (Sec. II-A) back
  * in token order (the return trip of Sec. II-B), plus shared experts with
  * weight 1:

@@ -240,34 +240,50 @@ int moe_grouped_ffn_combine(const void* x_perm, int dtype, const int32_t* group_
                                       (hipStream_t)stream);
 }
 
-int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int dtype,
-                         const int32_t* group_offsets, int n_groups, const void* const* w13,
-                         const void* const* w2, int d, int f, int64_t cap_rows, void* y_perm,
-                         void* ws, size_t ws_bytes, void* stream) {
+int moe_grouped_ffn_rows_products(const void* x, int64_t T, const int32_t* row_token, int dtype,
+                                  const int32_t* group_offsets, int n_groups,
+                                  const void* const* w13, const void* const* w2, int d, int f,
+                                  int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes,
+                                  int products, void* stream) {
     if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
+    if (products & ~(MOE_FFN_GATE_UP | MOE_FFN_DOWN | MOE_FFN_SMALL_GROUPS | MOE_FFN_LARGE_GROUPS))
+        return MOE_ERR_ARG;
+    if ((products & MOE_FFN_SMALL_GROUPS) && (products & MOE_FFN_LARGE_GROUPS)) return MOE_ERR_ARG;
+    const bool up = products & MOE_FFN_GATE_UP, down = products & MOE_FFN_DOWN;
+    if (!up && !down) return MOE_ERR_ARG;
     if (T < 0 || n_groups < 1 || n_groups > MOE_MAX_GROUPS || d < 1 || f < 1 || cap_rows < 0)
         return MOE_ERR_ARG;
     if (cap_rows > 0x7fffffff) return MOE_ERR_ARG;
-    if (!group_offsets || !w13 || !w2) return MOE_ERR_ARG;
+    if (!group_offsets || (up && !w13) || (down && !w2)) return MOE_ERR_ARG;
     for (int s = 0; s < n_groups; ++s)
-        if (!w13[s] || !w2[s]) return MOE_ERR_ARG;
-    if (cap_rows > 0 && (!x || !row_token || !y_perm || T < 1)) return MOE_ERR_ARG;
+        if ((up && !w13[s]) || (down && !w2[s])) return MOE_ERR_ARG;
+    if (cap_rows > 0 && ((up && (!x || !row_token || T < 1)) || (down && !y_perm)))
+        return MOE_ERR_ARG;
     if (dtype == MOE_BF16) {
         if (d % 64 || f % 64) return MOE_ERR_SHAPE;
         // token rows are addressed through 32-bit buffer offsets, and so is a
         // 256-row tile of either product
         if (T * (int64_t)d * 2 > 0x7fffffffLL) return MOE_ERR_SHAPE;
         if ((int64_t)d * 512 > 0x7fffffffLL || (int64_t)f * 512 > 0x7fffffffLL) return MOE_ERR_SHAPE;
-        if (!aligned16(x) || !aligned16(y_perm)) return MOE_ERR_ARG;
+        if ((x && !aligned16(x)) || (y_perm && !aligned16(y_perm))) return MOE_ERR_ARG;
         for (int s = 0; s < n_groups; ++s)
-            if (!aligned16(w13[s]) || !aligned16(w2[s])) return MOE_ERR_ARG;
+            if ((up && !aligned16(w13[s])) || (down && !aligned16(w2[s]))) return MOE_ERR_ARG;
     }
     if (cap_rows > 0 &&
         (!ws || ws_bytes < grouped_ffn_ws_bytes(dtype, cap_rows, d, f, n_groups) ||
          ((uintptr_t)ws & 255u)))
         return MOE_ERR_SHAPE;
     return launch_grouped_ffn(x, dtype, group_offsets, n_groups, w13, w2, d, f, cap_rows, y_perm,
-                              ws, (hipStream_t)stream, row_token, T);
+                              ws, (hipStream_t)stream, row_token, T, products);
+}
+
+int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int dtype,
+                         const int32_t* group_offsets, int n_groups, const void* const* w13,
+                         const void* const* w2, int d, int f, int64_t cap_rows, void* y_perm,
+                         void* ws, size_t ws_bytes, void* stream) {
+    return moe_grouped_ffn_rows_products(x, T, row_token, dtype, group_offsets, n_groups, w13, w2,
+                                         d, f, cap_rows, y_perm, ws, ws_bytes,
+                                         MOE_FFN_GATE_UP | MOE_FFN_DOWN, stream);
 }
 
 int moe_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* topk_gate,

@@ -202,7 +202,7 @@ class LayerShare:
         elif self.gather_in_ffn:
             moe.moe_grouped_ffn_rows(self.X, self.perm["row_token"], self.perm["group_offsets"],
                                      self.weights, cap_rows=self.cap_rows, y_perm=self.y_perm,
-                                     ws=self.ws_ffn)
+                                     ws=self.ws_ffn, products=self.ffn_products)
         else:
             moe.moe_grouped_ffn(self.perm["x_perm"], self.perm["group_offsets"], self.weights,
                                 cap_rows=self.cap_rows, y_perm=self.y_perm, ws=self.ws_ffn,

@@ -29,7 +29,7 @@ MOE_PERMUTE_NOALLOC_MAX_WS = 4 << 20
 EXPORTS = ("moe_status_string", "moe_route_topk", "moe_route_topk_ws_bytes",
            "moe_expert_histogram", "moe_permute_ws_bytes",
            "moe_permute", "moe_permute_noalloc", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_grouped_ffn_products", "moe_grouped_ffn_combine",
-           "moe_grouped_ffn_rows",
+           "moe_grouped_ffn_rows", "moe_grouped_ffn_rows_products",
            "moe_combine",
            "moe_quantize_e4m3", "moe_route_topk_e4m3")
 
@@ -76,6 +76,8 @@ def load_library(path: str = LIB_PATH):
     lib.moe_grouped_ffn_combine.restype = I
     lib.moe_grouped_ffn_rows.argtypes = [P, L, P, I, P, I, P, P, I, I, L, P, P, S, P]
     lib.moe_grouped_ffn_rows.restype = I
+    lib.moe_grouped_ffn_rows_products.argtypes = [P, L, P, I, P, I, P, P, I, I, L, P, P, S, I, P]
+    lib.moe_grouped_ffn_rows_products.restype = I
     lib.moe_combine.argtypes = [P, I, P, P, P, L, I, I, P, P]
     lib.moe_combine.restype = I
     lib.moe_quantize_e4m3.argtypes = [P, I, L, I, P, P, P]
@@ -386,8 +388,9 @@ def moe_grouped_ffn_combine(x_perm: torch.Tensor, group_offsets: torch.Tensor,
 def moe_grouped_ffn_rows(x: torch.Tensor, row_token: torch.Tensor, group_offsets: torch.Tensor,
                          weights: WeightTable, *, cap_rows: int,
                          y_perm: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-                         stream=None) -> torch.Tensor:
-    """moe_grouped_ffn reading row p from x[row_token[p]] (no x_perm).  Returns y_perm."""
+                         stream=None, products: int = 3) -> torch.Tensor:
+    """moe_grouped_ffn reading row p from x[row_token[p]] (no x_perm).  Returns y_perm.
+    products other than 3 (single products, hints) call moe_grouped_ffn_rows_products."""
     lib = load_library()
     T = x.shape[0]
     d, f = weights.d, weights.f
@@ -400,13 +403,15 @@ def moe_grouped_ffn_rows(x: torch.Tensor, row_token: torch.Tensor, group_offsets
         y_perm = _empty((max(cap_rows, 1), d), x.dtype, x.device)
     if ws is None:
         ws = workspace(moe_grouped_ffn_ws_bytes(dtype, cap_rows, d, f, len(weights)), x.device)
-    st = lib.moe_grouped_ffn_rows(_dev(x, "x"), T, _dev(row_token, "row_token", torch.int32),
-                                  dtype, _dev(group_offsets, "group_offsets", torch.int32),
-                                  len(weights), ctypes.cast(weights.p13, ctypes.c_void_p),
-                                  ctypes.cast(weights.p2, ctypes.c_void_p), d, f, cap_rows,
-                                  _dev(y_perm, "y_perm", x.dtype), _dev(ws, "ws"), ws.numel(),
-                                  _stream(stream))
-    _check("moe_grouped_ffn_rows", st)
+    args = [_dev(x, "x"), T, _dev(row_token, "row_token", torch.int32), dtype,
+            _dev(group_offsets, "group_offsets", torch.int32), len(weights),
+            ctypes.cast(weights.p13, ctypes.c_void_p), ctypes.cast(weights.p2, ctypes.c_void_p), d, f,
+            cap_rows, _dev(y_perm, "y_perm", x.dtype), _dev(ws, "ws"), ws.numel()]
+    if products == MOE_FFN_GATE_UP | MOE_FFN_DOWN:
+        _check("moe_grouped_ffn_rows", lib.moe_grouped_ffn_rows(*args, _stream(stream)))
+    else:
+        _check("moe_grouped_ffn_rows_products",
+               lib.moe_grouped_ffn_rows_products(*args, products, _stream(stream)))
     return y_perm
 
 

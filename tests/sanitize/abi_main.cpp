@@ -92,6 +92,10 @@ int main() {
                                 1 << 30, nullptr), MOE_ERR_ARG);
     EXPECT(moe_grouped_ffn_rows(F, 20000000, (int32_t*)F, 1, (int32_t*)F, 2, wp, wp, 128, 64, 16,
                                 F, W, 1 << 30, nullptr), MOE_ERR_SHAPE);
+    EXPECT(moe_grouped_ffn_rows_products(F, 64, (int32_t*)F, 1, (int32_t*)F, 2, wp, wp, 128, 64,
+                                         16, F, W, 1 << 30, 3 | 4 | 8, nullptr), MOE_ERR_ARG);
+    EXPECT(moe_grouped_ffn_rows_products(F, 64, nullptr, 1, (int32_t*)F, 2, wp, wp, 128, 64, 16,
+                                         F, W, 1 << 30, 1, nullptr), MOE_ERR_ARG);
     // moe_combine
     EXPECT(moe_combine(nullptr, 1, (int32_t*)F, (float*)F, nullptr, 4, 64, 2, F, nullptr),
            MOE_ERR_ARG);

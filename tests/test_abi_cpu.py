@@ -229,6 +229,25 @@ def test_grouped_ffn_rows_validation(lib):
     assert call(dtype=3) == moe.MOE_ERR_ARG
 
 
+def test_grouped_ffn_rows_products_validation(lib):
+    f = lib.moe_grouped_ffn_rows_products
+    arr = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    P = ctypes.cast(arr, ctypes.c_void_p)
+
+    def call(products=3, rows=FAKE, x=FAKE, y=FAKE, d=128, ws_bytes=1 << 30):
+        return f(x, 64, rows, 1, FAKE, 2, P, P, d, 64, 16, y, ctypes.c_void_p(0x100000), ws_bytes,
+                 products, None)
+    assert call(products=0) == moe.MOE_ERR_ARG
+    assert call(products=8) == moe.MOE_ERR_ARG                     # a hint alone runs nothing
+    assert call(products=3 | 4 | 8) == moe.MOE_ERR_ARG             # the two hints contradict
+    assert call(products=1 | 16) == moe.MOE_ERR_ARG
+    assert call(products=1, rows=None) == moe.MOE_ERR_ARG          # gate/up reads the row map
+    assert call(products=1, x=None) == moe.MOE_ERR_ARG
+    assert call(products=2, y=None) == moe.MOE_ERR_ARG             # down writes y_perm
+    assert call(products=3 | 8, d=100) == moe.MOE_ERR_SHAPE
+    assert call(products=3 | 8, ws_bytes=10) == moe.MOE_ERR_SHAPE
+
+
 def test_combine_validation(lib):
     f = lib.moe_combine
     assert f(FAKE, 1, FAKE, FAKE, None, 4, 64, 0, FAKE, None) == moe.MOE_ERR_ARG

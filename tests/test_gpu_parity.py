@@ -500,6 +500,37 @@ def test_large_groups_hint_leaves_the_shared_call_bitwise_unchanged(name, regime
     assert torch.equal(plain[:T], share.y_shared[:T])
 
 
+@pytest.mark.parametrize("name,regime", [("mixtral_8x7b", "prefill"), ("deepseek_v2_lite", "prefill"),
+                                         ("qwen3_30b_a3b", "prefill")])
+def test_large_groups_hint_leaves_the_routed_call_bitwise_unchanged(name, regime):
+    """Prefill batches whose mean group holds at least 512 rows: LayerShare passes
+    MOE_FFN_LARGE_GROUPS to the routed call (packaged rows at the Mixtral shape,
+    rows gathered through row_token at the others), which leaves out the streaming
+    launches; such a call tiles every group either way, so its outputs are the bits
+    of the call without the hint."""
+    cfg = synth.CONFIGS[name]
+    T = cfg.T(regime)
+    say("[large groups, routed]", name, regime, "T=%d" % T)
+    inp = synth.make_layer(cfg, T, seed=6, device="cuda")
+    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                       shared=inp.shared, coact=cfg.coact)
+    assert share.ffn_products & moe.MOE_FFN_LARGE_GROUPS
+    share.run()
+    torch.cuda.synchronize()
+    N = int(share.perm["group_offsets"][-1])
+    hinted = share.y_perm[:N].clone()
+    share.y_perm.zero_()
+    if share.gather_in_ffn:
+        moe.moe_grouped_ffn_rows(share.X, share.perm["row_token"], share.perm["group_offsets"],
+                                 share.weights, cap_rows=share.cap_rows, y_perm=share.y_perm,
+                                 ws=share.ws_ffn)
+    else:
+        moe.moe_grouped_ffn(share.perm["x_perm"], share.perm["group_offsets"], share.weights,
+                            cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
+    torch.cuda.synchronize()
+    assert torch.equal(share.y_perm[:N], hinted)
+
+
 def test_large_groups_hint_broken_still_computes_every_group():
     """MOE_FFN_LARGE_GROUPS on groups that break it (empty, 1, 40, 64, 65, 200 and
     700 rows): every group goes to the tiled kernel instead of streaming and must
