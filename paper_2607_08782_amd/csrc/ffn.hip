@@ -1050,10 +1050,25 @@ struct PtrTable {
     const float* p[MOE_MAX_GROUPS];
 };
 
-__device__ __forceinline__ int find_group(const int* off, int n_groups, int p) {
-    int s = 0;
-    while (s + 1 < n_groups && off[s + 1] <= p) ++s;
-    return s;
+// fp32 path (small layers): 16 x 16 output tiles within one group, operands
+// staged through LDS in 32-wide K slices (coalesced loads); every output is still
+// one fmaf chain over K in ascending order, as a thread per output would sum it.
+constexpr int F32_T = 16, F32_K = 32;
+
+__device__ __forceinline__ void f32_tile_plan(const int32_t* offsets, int n_groups, int ncols,
+                                              int* s_off, int* s_tstart) {
+    for (int s = threadIdx.x; s <= n_groups; s += blockDim.x) s_off[s] = offsets[s];
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int nt = (ncols + F32_T - 1) / F32_T;
+        int t = 0;
+        for (int g = 0; g < n_groups; ++g) {
+            s_tstart[g] = t;
+            t += (s_off[g + 1] - s_off[g] + F32_T - 1) / F32_T * nt;
+        }
+        s_tstart[n_groups] = t;
+    }
+    __syncthreads();
 }
 
 __global__ __launch_bounds__(256) void ffn1_f32_kernel(const float* __restrict__ x,
@@ -1061,22 +1076,37 @@ __global__ __launch_bounds__(256) void ffn1_f32_kernel(const float* __restrict__
                                                        const int32_t* __restrict__ offsets,
                                                        int n_groups, PtrTable w13, int d, int f,
                                                        float* __restrict__ h) {
-    __shared__ int s_off[MOE_MAX_GROUPS + 1];
-    for (int s = threadIdx.x; s <= n_groups; s += blockDim.x) s_off[s] = offsets[s];
-    __syncthreads();
-    const int64_t N = s_off[n_groups];
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N * f;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        const int p = (int)(i / f), j = (int)(i % f);
-        const int s = find_group(s_off, n_groups, p);
-        const float* W = w13.p[s];
-        const float* xr = x + (int64_t)(a_rows ? a_rows[p] : p) * d;
+    __shared__ int s_off[MOE_MAX_GROUPS + 1], s_tstart[MOE_MAX_GROUPS + 1];
+    __shared__ float xs[F32_T][F32_K + 1], gs[F32_T][F32_K + 1], us[F32_T][F32_K + 1];
+    f32_tile_plan(offsets, n_groups, f, s_off, s_tstart);
+    const int tid = threadIdx.x, tr = tid / F32_T, tc = tid % F32_T;
+    const int nt = (f + F32_T - 1) / F32_T;
+    for (int tile = blockIdx.x; tile < s_tstart[n_groups]; tile += gridDim.x) {
+        const int g = last_le(s_tstart, n_groups, tile);
+        const int local = tile - s_tstart[g];
+        const int row0 = s_off[g] + (local / nt) * F32_T, col0 = (local % nt) * F32_T;
+        const int rows = min(F32_T, s_off[g + 1] - row0);
+        const float* __restrict__ W = w13.p[g];
         float a = 0.f, b = 0.f;
-        for (int q = 0; q < d; ++q) {
-            a = fmaf(W[(int64_t)j * d + q], xr[q], a);
-            b = fmaf(W[(int64_t)(f + j) * d + q], xr[q], b);
+        for (int q0 = 0; q0 < d; q0 += F32_K) {
+            for (int e = tid; e < F32_T * F32_K; e += 256) {
+                const int r = e / F32_K, q = e % F32_K;
+                const bool kin = q0 + q < d;
+                const int p = row0 + r;
+                xs[r][q] = r < rows && kin ? x[(int64_t)(a_rows ? a_rows[p] : p) * d + q0 + q] : 0.f;
+                gs[r][q] = col0 + r < f && kin ? W[(int64_t)(col0 + r) * d + q0 + q] : 0.f;
+                us[r][q] = col0 + r < f && kin ? W[(int64_t)(f + col0 + r) * d + q0 + q] : 0.f;
+            }
+            __syncthreads();
+            const int qn = min(F32_K, d - q0);
+            for (int q = 0; q < qn; ++q) {
+                a = fmaf(gs[tc][q], xs[tr][q], a);
+                b = fmaf(us[tc][q], xs[tr][q], b);
+            }
+            __syncthreads();
         }
-        h[i] = a / (1.0f + expf(-a)) * b;
+        if (tr < rows && col0 + tc < f)
+            h[(int64_t)(row0 + tr) * f + col0 + tc] = a / (1.0f + expf(-a)) * b;
     }
 }
 
@@ -1084,19 +1114,31 @@ __global__ __launch_bounds__(256) void ffn2_f32_kernel(const float* __restrict__
                                                        const int32_t* __restrict__ offsets,
                                                        int n_groups, PtrTable w2, int d, int f,
                                                        float* __restrict__ y) {
-    __shared__ int s_off[MOE_MAX_GROUPS + 1];
-    for (int s = threadIdx.x; s <= n_groups; s += blockDim.x) s_off[s] = offsets[s];
-    __syncthreads();
-    const int64_t N = s_off[n_groups];
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N * d;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        const int p = (int)(i / d), o = (int)(i % d);
-        const int s = find_group(s_off, n_groups, p);
-        const float* W = w2.p[s] + (int64_t)o * f;
-        const float* hr = h + (int64_t)p * f;
+    __shared__ int s_off[MOE_MAX_GROUPS + 1], s_tstart[MOE_MAX_GROUPS + 1];
+    __shared__ float hs[F32_T][F32_K + 1], ws[F32_T][F32_K + 1];
+    f32_tile_plan(offsets, n_groups, d, s_off, s_tstart);
+    const int tid = threadIdx.x, tr = tid / F32_T, tc = tid % F32_T;
+    const int nt = (d + F32_T - 1) / F32_T;
+    for (int tile = blockIdx.x; tile < s_tstart[n_groups]; tile += gridDim.x) {
+        const int g = last_le(s_tstart, n_groups, tile);
+        const int local = tile - s_tstart[g];
+        const int row0 = s_off[g] + (local / nt) * F32_T, col0 = (local % nt) * F32_T;
+        const int rows = min(F32_T, s_off[g + 1] - row0);
+        const float* __restrict__ W = w2.p[g];
         float acc = 0.f;
-        for (int j = 0; j < f; ++j) acc = fmaf(W[j], hr[j], acc);
-        y[i] = acc;
+        for (int j0 = 0; j0 < f; j0 += F32_K) {
+            for (int e = tid; e < F32_T * F32_K; e += 256) {
+                const int r = e / F32_K, j = e % F32_K;
+                const bool kin = j0 + j < f;
+                hs[r][j] = r < rows && kin ? h[(int64_t)(row0 + r) * f + j0 + j] : 0.f;
+                ws[r][j] = col0 + r < d && kin ? W[(int64_t)(col0 + r) * f + j0 + j] : 0.f;
+            }
+            __syncthreads();
+            const int jn = min(F32_K, f - j0);
+            for (int j = 0; j < jn; ++j) acc = fmaf(ws[tc][j], hs[tr][j], acc);
+            __syncthreads();
+        }
+        if (tr < rows && col0 + tc < d) y[(int64_t)(row0 + tr) * d + col0 + tc] = acc;
     }
 }
 
@@ -1159,7 +1201,9 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
             t2.p[i] = i < n_groups ? (const float*)w2[i] : nullptr;
         }
         float* h = (float*)ws;
-        int64_t b1 = ceil_div(cap_rows * (int64_t)f, 256), b2 = ceil_div(cap_rows * (int64_t)d, 256);
+        // tiles of 16 rows within a group: at most cap_rows / 16 + n_groups row tiles
+        const int64_t mt = cap_rows / 16 + n_groups;
+        int64_t b1 = mt * ceil_div(f, 16), b2 = mt * ceil_div(d, 16);
         if (b1 > 4096) b1 = 4096;
         if (b2 > 4096) b2 = 4096;
         if (up)
