@@ -1234,7 +1234,8 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     if (rgrid > 4096) rgrid = 4096;
     if (rgrid < 1) rgrid = 1;
 
-    // gate/up product: big groups on the tiled kernel, small groups streamed
+    // gate/up product: tiled launch, then the streaming launch (the small groups of a
+    // short call), then the chunk sums
     GemmArgs a1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i)
         a1.w[i] = up && i < n_groups ? (const bf16_t*)w13[i] : nullptr;
