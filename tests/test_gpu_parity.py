@@ -446,6 +446,34 @@ def test_ffn_products_one_at_a_time_equal_the_whole_call(name, regime):
     assert torch.equal(share.y_perm[:N], whole)
 
 
+@pytest.mark.parametrize("name,regime", [("deepseek_v2_lite", "prefill"), ("qwen3_30b_a3b", "decode")])
+def test_rows_products_one_at_a_time_equal_the_whole_call(name, regime):
+    """moe_grouped_ffn_rows_products: the gate/up product (rows through row_token),
+    then the down product on the same workspace, with and without the share's hint,
+    gives the bits of moe_grouped_ffn_rows."""
+    cfg = synth.CONFIGS[name]
+    T = cfg.T(regime)
+    say("[rows products]", name, regime, "T=%d" % T)
+    inp = synth.make_layer(cfg, T, seed=7, device="cuda")
+    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                       shared=inp.shared, coact=cfg.coact, gather_in_ffn=True)
+    share.run()
+    torch.cuda.synchronize()
+    N = int(share.perm["group_offsets"][-1])
+    args = (share.X, share.perm["row_token"], share.perm["group_offsets"], share.weights)
+    moe.moe_grouped_ffn_rows(*args, cap_rows=share.cap_rows, y_perm=share.y_perm, ws=share.ws_ffn)
+    torch.cuda.synchronize()
+    whole = share.y_perm[:N].clone()
+    hint = share.ffn_products & (moe.MOE_FFN_SMALL_GROUPS | moe.MOE_FFN_LARGE_GROUPS)
+    for extra in sorted({0, hint}):
+        share.y_perm.zero_()
+        for products in (moe.MOE_FFN_GATE_UP, moe.MOE_FFN_DOWN):
+            moe.moe_grouped_ffn_rows(*args, cap_rows=share.cap_rows, y_perm=share.y_perm,
+                                     ws=share.ws_ffn, products=products | extra)
+        torch.cuda.synchronize()
+        assert torch.equal(share.y_perm[:N], whole), "hint %d" % extra
+
+
 @pytest.mark.parametrize("name,regime", [("mixtral_8x7b", "decode"), ("qwen3_30b_a3b", "decode"),
                                          ("deepseek_v2_lite", "decode")])
 def test_small_groups_hint_leaves_the_outputs_bitwise_unchanged(name, regime):
