@@ -16,10 +16,10 @@
  * (tokens or rows) across threads, which cannot change any result.
  *
  * Parity status: every function is pinned by the CPU test-suite
- * (library routines, closed forms, brute force on tiny inputs, invariants),
- * except the replica split rule in orc_permute, which the paper leaves open
- * and which is pinned only by its partition invariants ("parity unpinned" by
- * the paper itself for that rule).
+ * (library routines, closed forms, brute force on tiny inputs, invariants).
+ * The replica split rule in orc_permute is a convention the paper leaves open
+ * (the floor rule read here); it is pinned by its partition invariants and by
+ * a hand-worked example of that rule (tests/golden/replica_split_hand_example.json).
  */
 #include <math.h>
 #include <stdint.h>
