@@ -118,6 +118,11 @@ def ffn_call(share, products=None):
 
 def ffn_label(share):
     """What the routed experts' FFN call of `share` launches."""
+    if share.shared_in_ffn:
+        what = ("weight-streaming launches" if share.ffn_products & moe.MOE_FFN_SMALL_GROUPS
+                else "gate/up and down tiled GEMMs")
+        return ("moe_grouped_ffn_rows_shared call: the routed experts and the shared experts' "
+                "%d blocks of width f in one call (%s, chunk sums)" % (share.n_shared_blocks, what))
     if share.fused_combine:
         return ("moe_grouped_ffn_combine call (weight-streaming launches, the combine in the "
                 "down product's chunk sum)")
@@ -137,9 +142,18 @@ def ffn_work(share, cfg):
     # weights of the active experts once, the rows in, and the rows out (y_perm), or,
     # when the call combines, the tokens' outputs y with their row maps and gates
     out = (share.T * cfg.d * esz + share.T * cfg.k * 8.0) if share.fused_combine else N * cfg.d * esz
-    return {"N": N, "active": active, "sizes": sizes.tolist(),
-            "flops": 6.0 * cfg.d * cfg.f * N, "gate_up_flops": 4.0 * cfg.d * cfg.f * N,
-            "bytes": active * 3.0 * cfg.d * cfg.f * esz + N * cfg.d * esz + out}
+    w = {"N": N, "active": active, "sizes": sizes.tolist(),
+         "flops": 6.0 * cfg.d * cfg.f * N, "gate_up_flops": 4.0 * cfg.d * cfg.f * N,
+         "bytes": active * 3.0 * cfg.d * cfg.f * esz + N * cfg.d * esz + out}
+    if share.shared_in_ffn:
+        # the call also runs the shared experts' blocks over every token: their
+        # weights once, the token rows in, one output slice per block
+        nb, T = share.n_shared_blocks, share.T
+        w["shared_blocks"] = nb
+        w["flops"] += 6.0 * cfg.d * cfg.f * nb * T
+        w["gate_up_flops"] += 4.0 * cfg.d * cfg.f * nb * T
+        w["bytes"] += nb * 3.0 * cfg.d * cfg.f * esz + T * cfg.d * esz + nb * T * cfg.d * esz
+    return w
 
 
 def phase_calls(share):
@@ -157,13 +171,11 @@ def phase_calls(share):
         share.routed_ffn()
 
     def shared_ffn():
-        if share.shared_weights is not None:
-            share._shared_ffn()
+        share._shared_ffn()                # nothing when the shared experts share the call
 
     def combine():
         if not share.fused_combine:        # else part of grouped_ffn
-            moe.moe_combine(share.y_perm, share.perm["token_row"], share.topk_gate,
-                            share.y_shared, T=share.T, d=share.d, y=share.y)
+            share.combine()
 
     return dict(route_topk=route, histogram=histogram, permute=permute, grouped_ffn=grouped_ffn,
                 shared_ffn=shared_ffn, combine=combine)
@@ -268,7 +280,7 @@ def drift_sequence(steps, seed=0):
     flops = sum(w["flops"] for w in works) / len(works)
     moved = sum(1 for a, b in zip(shares, shares[1:])
                 if not np.array_equal(a.placement, b.placement))
-    return {"T": T, "batches": cfg.batches, "placement_swaps": moved,
+    return {"T": T, "batches": cfg.batches, "placement_swaps": moved, "ffn_call": ffn_label(shares[0]),
             "weight_bytes_per_batch": sum(weight_bytes_of(s) for s in shares) / len(shares),
             "rows_here_mean": sum(w["N"] for w in works) / len(works),
             "step_ms": step_ms, "ffn_ms": ffn_ms,
@@ -288,7 +300,7 @@ def shape_entry(name, regime, steps, warmup):
     e = {"T": m["T"], "rows_here": m.get("rows_here"), "active_experts": m.get("active_experts"),
          "local_experts": m["local_experts"], "weight_copies": m["weight_copies"],
          "step_ms": m["step_ms"], "tokens_per_s": m["T"] / (m["step_ms"] * 1e-3),
-         "ffn_ms": m.get("ffn_ms")}
+         "ffn_ms": m.get("ffn_ms"), "ffn_call": ffn_label(shares[0])}
     if work is not None:
         t = m["ffn_ms"] * 1e-3
         if cfg.dtype == "f32":

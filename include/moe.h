@@ -320,6 +320,44 @@ int moe_grouped_ffn_rows_products(const void* x, int64_t T, const int32_t* row_t
                                   int products, void* stream);
 
 /*
+ * moe_grouped_ffn_rows_shared -- moe_grouped_ffn_rows_products with the
+ * always-on shared experts (Sec. II-A: every token also passes through them)
+ * computed in the same launches as the routed experts, as n_shared leading
+ * groups of T rows each: one call instead of a second FFN call, so the tiles of
+ * both fill the GPU together.  A shared expert of width m * f takes m groups
+ * (its gate, up and down rows cut into m blocks of f: SwiGLU is elementwise in
+ * h, and the down product sums over h, so the m outputs sum to the expert's).
+ *
+ *   group s < n_shared       rows [s T, (s+1) T), weights w13[s], w2[s]
+ *   routed group g            rows n_shared T + [group_offsets[g], group_offsets[g+1]),
+ *                             weights w13[n_shared + g], w2[n_shared + g]
+ *
+ * row_token  device [n_shared T + cap_rows] int32: the caller's entries for the
+ *            shared rows (row s T + t is token t: 0, 1, ..., T-1 per group,
+ *            written once and kept), then the routed rows' map (moe_permute's
+ *            row_token written at row_token + n_shared T)
+ * group_offsets  device [n_groups+1], the routed groups as moe_permute writes
+ *            them (n_groups may be 0: only group_offsets[0] = 0 is then read)
+ * w13, w2    HOST arrays of n_shared + n_groups device pointers, shared first
+ * cap_rows   routed row capacity;  y_perm device [n_shared T + cap_rows][d]: group
+ *            s's output in rows [s T, (s+1) T) (the n_shared slices that
+ *            moe_combine_shared adds), routed rows from n_shared T
+ * ws         moe_grouped_ffn_ws_bytes(dtype, n_shared T + cap_rows, d, f,
+ *            n_shared + n_groups) bytes
+ * products   as for moe_grouped_ffn_rows_products; the hints state the sizes of
+ *            every group, shared ones included.
+ * Requires 0 <= n_shared, 1 <= n_shared + n_groups <= MOE_MAX_GROUPS, T >= 1
+ * when n_shared > 0 and n_shared T + cap_rows < 2^31; other requirements and
+ * errors as for moe_grouped_ffn_rows.  With n_shared = 0 it is
+ * moe_grouped_ffn_rows_products.
+ */
+int moe_grouped_ffn_rows_shared(const void* x, int64_t T, const int32_t* row_token, int dtype,
+                                const int32_t* group_offsets, int n_groups, int n_shared,
+                                const void* const* w13, const void* const* w2, int d, int f,
+                                int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes,
+                                int products, void* stream);
+
+/*
  * moe_combine -- gate-weighted sum of the experts' outputs (Sec. II-A) back
  * in token order (the return trip of Sec. II-B), plus shared experts with
  * weight 1:
@@ -335,6 +373,22 @@ int moe_grouped_ffn_rows_products(const void* x, int64_t T, const int32_t* row_t
  */
 int moe_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* topk_gate,
                 const void* y_shared, int64_t T, int d, int k, void* y, void* stream);
+
+/*
+ * moe_combine_shared -- moe_combine with the shared experts' output in
+ * n_shared slices (as moe_grouped_ffn_rows_shared leaves it), added after the
+ * routed sum in slice order:
+ *
+ *   y[t] = sum_{r ascending, token_row[t][r] >= 0} topk_gate[t][r] * y_perm[token_row[t][r]]
+ *          + y_shared[0][t] + y_shared[1][t] + ... + y_shared[n_shared-1][t]
+ *
+ * y_shared  device [n_shared][T][d] of `dtype` (NULL or n_shared = 0: none).
+ * Requires 0 <= n_shared <= MOE_MAX_GROUPS; other arguments as for
+ * moe_combine.  n_shared = 1 is exactly moe_combine.
+ */
+int moe_combine_shared(const void* y_perm, int dtype, const int32_t* token_row,
+                       const float* topk_gate, const void* y_shared, int n_shared, int64_t T,
+                       int d, int k, void* y, void* stream);
 
 /*
  * moe_quantize_e4m3 -- per-row FP8 quantization for the quantized routing

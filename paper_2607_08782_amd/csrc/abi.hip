@@ -240,24 +240,30 @@ int moe_grouped_ffn_combine(const void* x_perm, int dtype, const int32_t* group_
                                       (hipStream_t)stream);
 }
 
-int moe_grouped_ffn_rows_products(const void* x, int64_t T, const int32_t* row_token, int dtype,
-                                  const int32_t* group_offsets, int n_groups,
-                                  const void* const* w13, const void* const* w2, int d, int f,
-                                  int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes,
-                                  int products, void* stream) {
+int moe_grouped_ffn_rows_shared(const void* x, int64_t T, const int32_t* row_token, int dtype,
+                                const int32_t* group_offsets, int n_groups, int n_shared,
+                                const void* const* w13, const void* const* w2, int d, int f,
+                                int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes,
+                                int products, void* stream) {
     if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
     if (products & ~(MOE_FFN_GATE_UP | MOE_FFN_DOWN | MOE_FFN_SMALL_GROUPS | MOE_FFN_LARGE_GROUPS))
         return MOE_ERR_ARG;
     if ((products & MOE_FFN_SMALL_GROUPS) && (products & MOE_FFN_LARGE_GROUPS)) return MOE_ERR_ARG;
     const bool up = products & MOE_FFN_GATE_UP, down = products & MOE_FFN_DOWN;
     if (!up && !down) return MOE_ERR_ARG;
-    if (T < 0 || n_groups < 1 || n_groups > MOE_MAX_GROUPS || d < 1 || f < 1 || cap_rows < 0)
+    if (n_shared < 0 || n_groups < 0 || n_shared > MOE_MAX_GROUPS) return MOE_ERR_ARG;
+    const int groups = n_shared + n_groups;
+    if (T < 0 || groups < 1 || groups > MOE_MAX_GROUPS || d < 1 || f < 1 || cap_rows < 0)
         return MOE_ERR_ARG;
-    if (cap_rows > 0x7fffffff) return MOE_ERR_ARG;
+    if (n_shared > 0 && T < 1) return MOE_ERR_ARG;
+    // every row, shared and routed, is addressed with 32-bit row indices
+    if (cap_rows > 0x7fffffff || (int64_t)n_shared * T > 0x7fffffffLL - cap_rows)
+        return MOE_ERR_ARG;
+    const int64_t rows = (int64_t)n_shared * T + cap_rows;
     if (!group_offsets || (up && !w13) || (down && !w2)) return MOE_ERR_ARG;
-    for (int s = 0; s < n_groups; ++s)
+    for (int s = 0; s < groups; ++s)
         if ((up && !w13[s]) || (down && !w2[s])) return MOE_ERR_ARG;
-    if (cap_rows > 0 && ((up && (!x || !row_token || T < 1)) || (down && !y_perm)))
+    if (rows > 0 && ((up && (!x || !row_token || T < 1)) || (down && !y_perm)))
         return MOE_ERR_ARG;
     if (dtype == MOE_BF16) {
         if (d % 64 || f % 64) return MOE_ERR_SHAPE;
@@ -266,15 +272,26 @@ int moe_grouped_ffn_rows_products(const void* x, int64_t T, const int32_t* row_t
         if (T * (int64_t)d * 2 > 0x7fffffffLL) return MOE_ERR_SHAPE;
         if ((int64_t)d * 512 > 0x7fffffffLL || (int64_t)f * 512 > 0x7fffffffLL) return MOE_ERR_SHAPE;
         if ((x && !aligned16(x)) || (y_perm && !aligned16(y_perm))) return MOE_ERR_ARG;
-        for (int s = 0; s < n_groups; ++s)
+        for (int s = 0; s < groups; ++s)
             if ((up && !aligned16(w13[s])) || (down && !aligned16(w2[s]))) return MOE_ERR_ARG;
     }
-    if (cap_rows > 0 &&
-        (!ws || ws_bytes < grouped_ffn_ws_bytes(dtype, cap_rows, d, f, n_groups) ||
+    if (rows > 0 &&
+        (!ws || ws_bytes < grouped_ffn_ws_bytes(dtype, rows, d, f, groups) ||
          ((uintptr_t)ws & 255u)))
         return MOE_ERR_SHAPE;
-    return launch_grouped_ffn(x, dtype, group_offsets, n_groups, w13, w2, d, f, cap_rows, y_perm,
-                              ws, (hipStream_t)stream, row_token, T, products);
+    return launch_grouped_ffn(x, dtype, group_offsets, groups, w13, w2, d, f, rows, y_perm, ws,
+                              (hipStream_t)stream, row_token, T, products, nullptr, n_shared,
+                              (int)T);
+}
+
+int moe_grouped_ffn_rows_products(const void* x, int64_t T, const int32_t* row_token, int dtype,
+                                  const int32_t* group_offsets, int n_groups,
+                                  const void* const* w13, const void* const* w2, int d, int f,
+                                  int64_t cap_rows, void* y_perm, void* ws, size_t ws_bytes,
+                                  int products, void* stream) {
+    if (n_groups < 1) return MOE_ERR_ARG;
+    return moe_grouped_ffn_rows_shared(x, T, row_token, dtype, group_offsets, n_groups, 0, w13, w2,
+                                       d, f, cap_rows, y_perm, ws, ws_bytes, products, stream);
 }
 
 int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int dtype,
@@ -286,17 +303,26 @@ int moe_grouped_ffn_rows(const void* x, int64_t T, const int32_t* row_token, int
                                          MOE_FFN_GATE_UP | MOE_FFN_DOWN, stream);
 }
 
-int moe_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* topk_gate,
-                const void* y_shared, int64_t T, int d, int k, void* y, void* stream) {
+int moe_combine_shared(const void* y_perm, int dtype, const int32_t* token_row,
+                       const float* topk_gate, const void* y_shared, int n_shared, int64_t T,
+                       int d, int k, void* y, void* stream) {
     if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_ARG;
     if (T < 0 || d < 1 || k < 1 || k > MOE_MAX_K) return MOE_ERR_ARG;
+    if (n_shared < 0 || n_shared > MOE_MAX_GROUPS) return MOE_ERR_ARG;
     if (T > 0 && (!token_row || !topk_gate || !y || !y_perm)) return MOE_ERR_ARG;
+    if (n_shared == 0) y_shared = nullptr;
     const int V = dtype == MOE_BF16 ? 8 : 4;
     if (d % V == 0 && (!aligned16(y) || (y_perm && !aligned16(y_perm)) ||
                        (y_shared && !aligned16(y_shared))))
         return MOE_ERR_ARG;
-    return launch_combine(y_perm, dtype, token_row, topk_gate, y_shared, T, d, k, y,
+    return launch_combine(y_perm, dtype, token_row, topk_gate, y_shared, n_shared, T, d, k, y,
                           (hipStream_t)stream);
+}
+
+int moe_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* topk_gate,
+                const void* y_shared, int64_t T, int d, int k, void* y, void* stream) {
+    return moe_combine_shared(y_perm, dtype, token_row, topk_gate, y_shared, 1, T, d, k, y,
+                              stream);
 }
 
 int moe_quantize_e4m3(const void* x, int dtype, int64_t rows, int cols, uint8_t* q,

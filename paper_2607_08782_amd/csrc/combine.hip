@@ -1,6 +1,7 @@
 // Gate-weighted sum of the selected experts' outputs (Sec. II-A of the
 // Director paper), gathered back into token order (the return trip of
-// Sec. II-B), plus always-on shared experts with weight 1.
+// Sec. II-B), plus always-on shared experts with weight 1 (one or more
+// [T][d] slices of shared-expert output, added in slice order).
 //
 // Bandwidth-bound gather: each thread owns one 16-byte chunk of one token's
 // output row, reads the k expert rows it needs (all loads issued together;
@@ -61,12 +62,39 @@ struct Vec<float, 1> {
     static __device__ __forceinline__ void store(float* p, const float* v) { *p = v[0]; }
 };
 
+// acc += the n_shared slices y_shared[s][t][col..] (slice stride `stride`
+// elements), in slice order; more than one slice: four loads at a time, a slice
+// past the last re-reading the last and dropped by a select.
+template <typename Elem, int V>
+__device__ __forceinline__ void add_shared(const Elem* __restrict__ y_shared, int n_shared,
+                                           int64_t stride, int64_t off, float* acc) {
+    if (n_shared == 1) {
+        float w[V];
+        Vec<Elem, V>::load(y_shared + off, w);
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] += w[i];
+        return;
+    }
+    for (int s0 = 0; s0 < n_shared; s0 += 4) {
+        float w[4][V];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int sl = s0 + j < n_shared ? s0 + j : n_shared - 1;
+            Vec<Elem, V>::load(y_shared + sl * stride + off, w[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < V; ++i) acc[i] = s0 + j < n_shared ? acc[i] + w[j][i] : acc[i];
+    }
+}
+
 // KM: k rounded up to a power of two (compile-time trip counts, no spills)
 template <typename Elem, int V, int KM>
 __global__ __launch_bounds__(COMBINE_THREADS) void combine_kernel(
     const Elem* __restrict__ y_perm, const int32_t* __restrict__ token_row,
-    const float* __restrict__ gate, const Elem* __restrict__ y_shared, int64_t T, int d, int k,
-    int chunks_per_row, Elem* __restrict__ y) {
+    const float* __restrict__ gate, const Elem* __restrict__ y_shared, int n_shared, int64_t T,
+    int d, int k, int chunks_per_row, Elem* __restrict__ y) {
     const int64_t gid = (int64_t)blockIdx.x * COMBINE_THREADS + threadIdx.x;
     const int64_t t = gid / chunks_per_row;
     const int c = (int)(gid - t * chunks_per_row);
@@ -100,12 +128,7 @@ __global__ __launch_bounds__(COMBINE_THREADS) void combine_kernel(
 #pragma unroll
             for (int i = 0; i < V; ++i) acc[i] = p[r] >= 0 ? fmaf(g[r], v[r][i], acc[i]) : acc[i];
     }
-    if (y_shared) {
-        float w[V];
-        Vec<Elem, V>::load(y_shared + t * d + col, w);
-#pragma unroll
-        for (int i = 0; i < V; ++i) acc[i] += w[i];
-    }
+    add_shared<Elem, V>(y_shared, n_shared, T * d, t * d + col, acc);
     Vec<Elem, V>::store(y + t * d + col, acc);
 }
 
@@ -132,8 +155,8 @@ __device__ __forceinline__ void combine_rows(const Elem* __restrict__ y_perm, co
 template <typename Elem, int V, int KM>
 __global__ __launch_bounds__(COMBINE_THREADS) void combine_compact_kernel(
     const Elem* __restrict__ y_perm, const int32_t* __restrict__ token_row,
-    const float* __restrict__ gate, const Elem* __restrict__ y_shared, int64_t T, int d, int k,
-    int chunks_per_row, Elem* __restrict__ y) {
+    const float* __restrict__ gate, const Elem* __restrict__ y_shared, int n_shared, int64_t T,
+    int d, int k, int chunks_per_row, Elem* __restrict__ y) {
     const int64_t gid = (int64_t)blockIdx.x * COMBINE_THREADS + threadIdx.x;
     const int64_t t = gid / chunks_per_row;
     const int c = (int)(gid - t * chunks_per_row);
@@ -197,54 +220,51 @@ __global__ __launch_bounds__(COMBINE_THREADS) void combine_compact_kernel(
             }
             break;
     }
-    if (y_shared) {
-        float w[V];
-        Vec<Elem, V>::load(y_shared + t * d + col, w);
-#pragma unroll
-        for (int i = 0; i < V; ++i) acc[i] += w[i];
-    }
+    add_shared<Elem, V>(y_shared, n_shared, T * d, t * d + col, acc);
     Vec<Elem, V>::store(y + t * d + col, acc);
 }
 
 template <typename Elem, int V, int KM>
 int launch_k(const void* y_perm, const int32_t* token_row, const float* gate, const void* y_shared,
-             int64_t T, int d, int k, void* y, hipStream_t s) {
+             int n_shared, int64_t T, int d, int k, void* y, hipStream_t s) {
     const int chunks = d / V;
     const int64_t blocks = ceil_div(T * chunks, COMBINE_THREADS);
     if constexpr (KM > 2) {
         if (chunks % 64 == 0) {
             hipLaunchKernelGGL((combine_compact_kernel<Elem, V, KM>), dim3((unsigned)blocks),
                                dim3(COMBINE_THREADS), 0, s, (const Elem*)y_perm, token_row, gate,
-                               (const Elem*)y_shared, T, d, k, chunks, (Elem*)y);
+                               (const Elem*)y_shared, n_shared, T, d, k, chunks, (Elem*)y);
             return launch_status();
         }
     }
     hipLaunchKernelGGL((combine_kernel<Elem, V, KM>), dim3((unsigned)blocks), dim3(COMBINE_THREADS),
-                       0, s, (const Elem*)y_perm, token_row, gate, (const Elem*)y_shared, T, d, k,
-                       chunks, (Elem*)y);
+                       0, s, (const Elem*)y_perm, token_row, gate, (const Elem*)y_shared, n_shared,
+                       T, d, k, chunks, (Elem*)y);
     return launch_status();
 }
 
 template <typename Elem, int V>
 int launch_v(const void* y_perm, const int32_t* token_row, const float* gate, const void* y_shared,
-             int64_t T, int d, int k, void* y, hipStream_t s) {
-    if (k <= 2) return launch_k<Elem, V, 2>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
-    if (k <= 4) return launch_k<Elem, V, 4>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
-    if (k <= 8) return launch_k<Elem, V, 8>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
-    return launch_k<Elem, V, MOE_MAX_K>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
+             int n_shared, int64_t T, int d, int k, void* y, hipStream_t s) {
+#define MOE_CK(KM) launch_k<Elem, V, KM>(y_perm, token_row, gate, y_shared, n_shared, T, d, k, y, s)
+    if (k <= 2) return MOE_CK(2);
+    if (k <= 4) return MOE_CK(4);
+    if (k <= 8) return MOE_CK(8);
+    return MOE_CK(MOE_MAX_K);
+#undef MOE_CK
 }
 
 }  // namespace
 
 int launch_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* gate,
-                   const void* y_shared, int64_t T, int d, int k, void* y, hipStream_t s) {
+                   const void* y_shared, int n_shared, int64_t T, int d, int k, void* y,
+                   hipStream_t s) {
     if (T == 0 || d == 0) return MOE_OK;
-    if (dtype == MOE_BF16) {
-        if (d % 8 == 0) return launch_v<bf16_t, 8>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
-        return launch_v<bf16_t, 1>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
-    }
-    if (d % 4 == 0) return launch_v<float, 4>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
-    return launch_v<float, 1>(y_perm, token_row, gate, y_shared, T, d, k, y, s);
+    if (!y_shared) n_shared = 0;
+#define MOE_CV(E, V) launch_v<E, V>(y_perm, token_row, gate, y_shared, n_shared, T, d, k, y, s)
+    if (dtype == MOE_BF16) return d % 8 == 0 ? MOE_CV(bf16_t, 8) : MOE_CV(bf16_t, 1);
+    return d % 4 == 0 ? MOE_CV(float, 4) : MOE_CV(float, 1);
+#undef MOE_CV
 }
 
 }  // namespace moe

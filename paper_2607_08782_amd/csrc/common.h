@@ -133,12 +133,15 @@ int permute_scratch(void** ptr);
 
 // a_rows (nullable): row p of the first product's input is row a_rows[p] of
 // x_perm, which then holds a_total rows (the token rows; no packaged copy).
+// lead > 0: the first `lead` of the n_groups groups hold lead_rows rows each,
+// and offsets (n_groups - lead + 1 entries) counts the others' rows from row
+// lead * lead_rows.
 int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, int n_groups,
                        const void* const* w13, const void* const* w2, int d, int f,
                        int64_t cap_rows, void* y_perm, void* ws, hipStream_t s,
                        const int32_t* a_rows = nullptr, int64_t a_total = 0,
                        int products = MOE_FFN_GATE_UP | MOE_FFN_DOWN,
-                       const void* combine = nullptr);
+                       const void* combine = nullptr, int lead = 0, int lead_rows = 0);
 // moe_grouped_ffn with every group streamed and the down product's chunk sum
 // writing the gate-weighted combine (bf16)
 int launch_grouped_ffn_combine(const void* x_perm, const int32_t* offsets, int n_groups,
@@ -148,7 +151,9 @@ int launch_grouped_ffn_combine(const void* x_perm, const int32_t* offsets, int n
                                hipStream_t s);
 size_t grouped_ffn_ws_bytes(int dtype, int64_t cap_rows, int d, int f, int n_groups);
 
+// y_shared: n_shared slices of [T][d] (nullable: none)
 int launch_combine(const void* y_perm, int dtype, const int32_t* token_row, const float* gate,
-                   const void* y_shared, int64_t T, int d, int k, void* y, hipStream_t s);
+                   const void* y_shared, int n_shared, int64_t T, int d, int k, void* y,
+                   hipStream_t s);
 
 }  // namespace moe

@@ -53,12 +53,21 @@ constexpr int SG_MFMA = 0x008, SG_VMEM_READ = 0x020, SG_DS_READ = 0x100, SG_DS_W
 constexpr uint32_t RSRC_WORD3 = 0x00020000;        // raw buffer: 32-bit data format
 constexpr int A_OOB = 0x7fffff00;                  // offset past any descriptor: reads zero
 
+// First row of group g.  The first `lead` groups hold lead_rows rows each (the
+// shared experts' groups of moe_grouped_ffn_rows_shared, every token once); the
+// offsets array gives the row ranges of the groups after them, counted from
+// row lead * lead_rows, as moe_permute writes them.
+__device__ __forceinline__ int group_start(const int32_t* offsets, int lead, int lead_rows, int g) {
+    return g < lead ? g * lead_rows : lead * lead_rows + offsets[g - lead];
+}
+
 struct GemmArgs {
     const bf16_t* w[MOE_MAX_GROUPS];   // per-group weight matrix, rows contiguous along K
-    const int32_t* offsets;            // [n_groups + 1] row offsets (device)
+    const int32_t* offsets;            // [n_groups - lead + 1] row offsets (device), see group_start
     const bf16_t* a;                   // [rows][K]
     bf16_t* out;                       // [rows][ldo]
-    int n_groups;
+    int n_groups;                      // lead groups included
+    int lead, lead_rows;               // leading groups of lead_rows rows each (group_start)
     int K;                             // contraction length
     int N;                             // output columns per group (f for SWIGLU, d for PLAIN)
     int ldo;
@@ -237,7 +246,8 @@ __global__ __launch_bounds__(GEMM_THREADS) void grouped_gemm_kernel(GemmArgs arg
     // the down launch reads its row limit from the gate/up launch (no group can
     // exceed SMALL_ROWS when there is nowhere to keep it)
     int lim = args.limits != nullptr && args.product == 1 ? args.limits[1] : args.lim0;
-    for (int s = tid; s <= n_groups; s += GEMM_THREADS) s_off[s] = args.offsets[s];
+    for (int s = tid; s <= n_groups; s += GEMM_THREADS)
+        s_off[s] = group_start(args.offsets, args.lead, args.lead_rows, s);
     __syncthreads();
     if (wave == 0) {
         if (args.limits != nullptr && args.product == 0) {
@@ -623,11 +633,12 @@ static_assert(ST_A_PER == 2 && ST_B_PER == 4, "streaming tile");
 
 struct StreamArgs {
     const bf16_t* w[MOE_MAX_GROUPS];     // per group [N][K]
-    const int32_t* offsets;
+    const int32_t* offsets;              // as GemmArgs::offsets
     const bf16_t* a;                     // [rows][K]
     float* part;                         // [S][n_small][N]
     bf16_t* out;                         // reduce output [rows][ldo]
-    int n_groups;
+    int n_groups;                        // lead groups included
+    int lead, lead_rows;                 // as in GemmArgs
     int K;
     int N;                               // weight rows (2f for gate/up, d for down)
     int ldo;
@@ -649,7 +660,8 @@ struct StreamPlan {
 
 __device__ void make_stream_plan(const StreamArgs& a, StreamPlan& P, int nthreads) {
     const int lim = a.limits != nullptr ? a.limits[a.product] : a.lim0;
-    for (int g = threadIdx.x; g <= a.n_groups; g += nthreads) P.off[g] = a.offsets[g];
+    for (int g = threadIdx.x; g <= a.n_groups; g += nthreads)
+        P.off[g] = group_start(a.offsets, a.lead, a.lead_rows, g);
     __syncthreads();
     if (threadIdx.x < 64) {                          // one wave: prefix sums over the groups
         const int lane = threadIdx.x;
@@ -817,13 +829,49 @@ __global__ __launch_bounds__(ST_THREADS, ST_WG_PER_CU) void stream_gemm_kernel(S
     }
 }
 
+// Adds chunks [c, c + RU) of a partial sum to x (SWIGLU: the up half, `up`
+// floats further on, to y), in chunk order.  All RU loads are issued before the
+// first add: a chunk at or past S reads chunk S - 1 and its add is skipped, so
+// a short split costs one load round trip instead of one per chunk.
+template <bool SWIGLU, int RU>
+__device__ __forceinline__ void add_chunk_batch(const float* pr, int64_t cstride, int up, int c,
+                                                int S, float4& x, float4& y) {
+    float4 v[RU], u[RU];
+#pragma unroll
+    for (int j = 0; j < RU; ++j) {
+        const int cc = c + j < S ? c + j : S - 1;
+        v[j] = *(const float4*)(pr + cc * cstride);
+        if (SWIGLU) u[j] = *(const float4*)(pr + cc * cstride + up);
+    }
+#pragma unroll
+    for (int j = 0; j < RU; ++j)
+        if (c + j < S) {
+            x.x += v[j].x; x.y += v[j].y; x.z += v[j].z; x.w += v[j].w;
+            if (SWIGLU) { y.x += u[j].x; y.y += u[j].y; y.z += u[j].z; y.w += u[j].w; }
+        }
+}
+
+// x (and y) = the sum of chunks 0 .. S-1 (S >= 1) in chunk order: batches of 8
+// loads, the rest as one batch of 4 or 8.
+template <bool SWIGLU>
+__device__ __forceinline__ void add_chunks(const float* pr, int64_t cstride, int up, int S,
+                                           float4& x, float4& y) {
+    x = make_float4(0.f, 0.f, 0.f, 0.f);
+    y = x;
+    int c = 0;
+    for (; c + 8 <= S; c += 8) add_chunk_batch<SWIGLU, 8>(pr, cstride, up, c, S, x, y);
+    if (S - c > 4) add_chunk_batch<SWIGLU, 8>(pr, cstride, up, c, S, x, y);
+    else if (c < S) add_chunk_batch<SWIGLU, 4>(pr, cstride, up, c, S, x, y);
+}
+
 // Sums, in chunk order, the K chunks of the tiled kernel's split tiles (fp32
 // partial tiles [row][weight row]; SWIGLU: gate in tile columns [0, 128), up
 // in [128, 256)) and applies the epilogue: out = SiLU(gate) * up, or the sum.
 template <bool SWIGLU>
 __device__ void tile_split_reduce(const GemmArgs& t, int* s_off, int* s_tstart) {
     const int n_groups = t.n_groups;
-    for (int g = threadIdx.x; g <= n_groups; g += ST_THREADS) s_off[g] = t.offsets[g];
+    for (int g = threadIdx.x; g <= n_groups; g += ST_THREADS)
+        s_off[g] = group_start(t.offsets, t.lead, t.lead_rows, g);
     __syncthreads();
     const int lim = t.limits != nullptr ? t.limits[t.product] : t.lim0;
     if (threadIdx.x < 64) tile_starts(s_off, n_groups, lim, t.n_tiles, s_tstart, threadIdx.x);
@@ -849,19 +897,11 @@ __device__ void tile_split_reduce(const GemmArgs& t, int* s_off, int* s_tstart) 
         if (m0 + row >= rows) continue;
         const int n0 = nt * BN_OUT;
         if (n0 + j >= t.N) continue;
-        float x[4] = {0.f, 0.f, 0.f, 0.f}, y[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int c = 0; c < S; ++c) {
-            const float* pr = t.part + ((int64_t)(q * S + c) * BM + row) * BNW + j;
-            const float4 v = *(const float4*)pr;
-            x[0] += v.x; x[1] += v.y; x[2] += v.z; x[3] += v.w;
-            if (SWIGLU) {
-                const float4 w = *(const float4*)(pr + BNW / 2);
-                y[0] += w.x; y[1] += w.y; y[2] += w.z; y[3] += w.w;
-            }
-        }
-        float o[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = SWIGLU ? silu(x[e]) * y[e] : x[e];
+        float4 x, y;
+        add_chunks<SWIGLU>(t.part + ((int64_t)q * S * BM + row) * BNW + j, (int64_t)BM * BNW,
+                           BNW / 2, S, x, y);
+        const float o[4] = {SWIGLU ? silu(x.x) * y.x : x.x, SWIGLU ? silu(x.y) * y.y : x.y,
+                            SWIGLU ? silu(x.z) * y.z : x.z, SWIGLU ? silu(x.w) * y.w : x.w};
         uint2 pk;
         pk.x = pack_bf16x2(o[0], o[1]);
         pk.y = pack_bf16x2(o[2], o[3]);
@@ -901,33 +941,8 @@ __device__ __forceinline__ void stream_reduce(const StreamArgs& args, const Stre
         // the row's group: groups without small rows share qbase with the next one
         const int g = last_le(P.qbase, args.n_groups, q);
         const int p = P.off[g] + (q - P.qbase[g]);
-        const float* pr = args.part + (int64_t)q * args.N + c4;
-        float4 x = make_float4(0.f, 0.f, 0.f, 0.f), y = x;
-        // chunks are added one after another in chunk order; the loads of up to
-        // RU chunks are issued together ahead of their adds
-        constexpr int RU = 8;
-        int c = 0;
-        for (; c + RU <= S; c += RU) {
-            float4 v[RU], u[RU];
-#pragma unroll
-            for (int j = 0; j < RU; ++j) {
-                v[j] = *(const float4*)(pr + (c + j) * cstride);
-                if (SWIGLU) u[j] = *(const float4*)(pr + (c + j) * cstride + cols);
-            }
-#pragma unroll
-            for (int j = 0; j < RU; ++j) {
-                x.x += v[j].x; x.y += v[j].y; x.z += v[j].z; x.w += v[j].w;
-                if (SWIGLU) { y.x += u[j].x; y.y += u[j].y; y.z += u[j].z; y.w += u[j].w; }
-            }
-        }
-        for (; c < S; ++c) {
-            const float4 v = *(const float4*)(pr + c * cstride);
-            x.x += v.x; x.y += v.y; x.z += v.z; x.w += v.w;
-            if (SWIGLU) {
-                const float4 u = *(const float4*)(pr + c * cstride + cols);
-                y.x += u.x; y.y += u.y; y.z += u.z; y.w += u.w;
-            }
-        }
+        float4 x, y;
+        add_chunks<SWIGLU>(args.part + (int64_t)q * args.N + c4, cstride, cols, S, x, y);
         const float o0 = SWIGLU ? silu(x.x) * y.x : x.x, o1 = SWIGLU ? silu(x.y) * y.y : x.y;
         const float o2 = SWIGLU ? silu(x.z) * y.z : x.z, o3 = SWIGLU ? silu(x.w) * y.w : x.w;
         uint2 pk;
@@ -1055,9 +1070,10 @@ struct PtrTable {
 // one fmaf chain over K in ascending order, as a thread per output would sum it.
 constexpr int F32_T = 16, F32_K = 32;
 
-__device__ __forceinline__ void f32_tile_plan(const int32_t* offsets, int n_groups, int ncols,
-                                              int* s_off, int* s_tstart) {
-    for (int s = threadIdx.x; s <= n_groups; s += blockDim.x) s_off[s] = offsets[s];
+__device__ __forceinline__ void f32_tile_plan(const int32_t* offsets, int lead, int lead_rows,
+                                              int n_groups, int ncols, int* s_off, int* s_tstart) {
+    for (int s = threadIdx.x; s <= n_groups; s += blockDim.x)
+        s_off[s] = group_start(offsets, lead, lead_rows, s);
     __syncthreads();
     if (threadIdx.x == 0) {
         const int nt = (ncols + F32_T - 1) / F32_T;
@@ -1074,11 +1090,12 @@ __device__ __forceinline__ void f32_tile_plan(const int32_t* offsets, int n_grou
 __global__ __launch_bounds__(256) void ffn1_f32_kernel(const float* __restrict__ x,
                                                        const int32_t* __restrict__ a_rows,
                                                        const int32_t* __restrict__ offsets,
-                                                       int n_groups, PtrTable w13, int d, int f,
+                                                       int lead, int lead_rows, int n_groups,
+                                                       PtrTable w13, int d, int f,
                                                        float* __restrict__ h) {
     __shared__ int s_off[MOE_MAX_GROUPS + 1], s_tstart[MOE_MAX_GROUPS + 1];
     __shared__ float xs[F32_T][F32_K + 1], gs[F32_T][F32_K + 1], us[F32_T][F32_K + 1];
-    f32_tile_plan(offsets, n_groups, f, s_off, s_tstart);
+    f32_tile_plan(offsets, lead, lead_rows, n_groups, f, s_off, s_tstart);
     const int tid = threadIdx.x, tr = tid / F32_T, tc = tid % F32_T;
     const int nt = (f + F32_T - 1) / F32_T;
     for (int tile = blockIdx.x; tile < s_tstart[n_groups]; tile += gridDim.x) {
@@ -1112,11 +1129,12 @@ __global__ __launch_bounds__(256) void ffn1_f32_kernel(const float* __restrict__
 
 __global__ __launch_bounds__(256) void ffn2_f32_kernel(const float* __restrict__ h,
                                                        const int32_t* __restrict__ offsets,
-                                                       int n_groups, PtrTable w2, int d, int f,
+                                                       int lead, int lead_rows, int n_groups,
+                                                       PtrTable w2, int d, int f,
                                                        float* __restrict__ y) {
     __shared__ int s_off[MOE_MAX_GROUPS + 1], s_tstart[MOE_MAX_GROUPS + 1];
     __shared__ float hs[F32_T][F32_K + 1], ws[F32_T][F32_K + 1];
-    f32_tile_plan(offsets, n_groups, d, s_off, s_tstart);
+    f32_tile_plan(offsets, lead, lead_rows, n_groups, d, s_off, s_tstart);
     const int tid = threadIdx.x, tr = tid / F32_T, tc = tid % F32_T;
     const int nt = (d + F32_T - 1) / F32_T;
     for (int tile = blockIdx.x; tile < s_tstart[n_groups]; tile += gridDim.x) {
@@ -1184,7 +1202,7 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
                        const void* const* w13, const void* const* w2, int d, int f,
                        int64_t cap_rows, void* y_perm, void* ws, hipStream_t s,
                        const int32_t* a_rows, int64_t a_total, int products,
-                       const void* combine) {
+                       const void* combine, int lead, int lead_rows) {
     if (cap_rows == 0) return MOE_OK;
     const bool up = (products & MOE_FFN_GATE_UP) != 0, down = (products & MOE_FFN_DOWN) != 0;
     // every group within SMALL_ROWS_MAX rows (the caller's statement): all of them are
@@ -1208,10 +1226,12 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
         if (b2 > 4096) b2 = 4096;
         if (up)
             hipLaunchKernelGGL(ffn1_f32_kernel, dim3((unsigned)b1), dim3(256), 0, s,
-                               (const float*)x_perm, a_rows, offsets, n_groups, t13, d, f, h);
+                               (const float*)x_perm, a_rows, offsets, lead, lead_rows, n_groups,
+                               t13, d, f, h);
         if (down)
             hipLaunchKernelGGL(ffn2_f32_kernel, dim3((unsigned)b2), dim3(256), 0, s,
-                               (const float*)h, offsets, n_groups, t2, d, f, (float*)y_perm);
+                               (const float*)h, offsets, lead, lead_rows, n_groups, t2, d, f,
+                               (float*)y_perm);
         return launch_status();
     }
     const int cus = num_cus();
@@ -1240,6 +1260,8 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     for (int i = 0; i < MOE_MAX_GROUPS; ++i)
         a1.w[i] = up && i < n_groups ? (const bf16_t*)w13[i] : nullptr;
     a1.offsets = offsets;
+    a1.lead = lead;
+    a1.lead_rows = lead_rows;
     a1.a = (const bf16_t*)x_perm;
     a1.out = h;
     a1.n_groups = n_groups;
@@ -1264,6 +1286,8 @@ int launch_grouped_ffn(const void* x_perm, int dtype, const int32_t* offsets, in
     StreamArgs s1;
     for (int i = 0; i < MOE_MAX_GROUPS; ++i) s1.w[i] = a1.w[i];
     s1.offsets = offsets;
+    s1.lead = lead;
+    s1.lead_rows = lead_rows;
     s1.a = (const bf16_t*)x_perm;
     s1.part = part;
     s1.out = h;
@@ -1349,7 +1373,7 @@ int launch_grouped_ffn_combine(const void* x_perm, const int32_t* offsets, int n
     cb.k = k;
     if (cap_rows == 0) {
         // no local row: y is the shared experts' output (or zero), as the combine gives
-        return launch_combine(nullptr, MOE_BF16, token_row, gate, y_shared, T, d, k, y, s);
+        return launch_combine(nullptr, MOE_BF16, token_row, gate, y_shared, 1, T, d, k, y, s);
     }
     return launch_grouped_ffn(x_perm, MOE_BF16, offsets, n_groups, w13, w2, d, f, cap_rows,
                               nullptr, ws, s, nullptr, 0,

@@ -229,9 +229,7 @@ def run_step(share, mig: Optional[Migrator], budget_bytes: Optional[int] = None,
     # on the device, and issuing them (one host call per chunk) must not hold back
     # the launch of the computation they hide behind
     share.routed_ffn(fused=False)
-    if share.shared_weights is not None:
-        moe.moe_grouped_ffn(share.X, share.shared_offsets, share.shared_weights, cap_rows=share.T,
-                            y_perm=share.y_shared, ws=share.ws_shared)
+    share._shared_ffn()          # nothing when the shared experts share the routed call
     stall = None
     ffn_end = torch.cuda.Event(enable_timing=True)
     ffn_end.record(cur)
@@ -256,6 +254,5 @@ def run_step(share, mig: Optional[Migrator], budget_bytes: Optional[int] = None,
     if timing is not None:
         ffn_end.synchronize()
         timing.setdefault("ffn", []).append(opened.elapsed_time(ffn_end))
-    moe.moe_combine(share.y_perm, share.perm["token_row"], share.topk_gate, share.y_shared,
-                    T=share.T, d=share.d, y=share.y)
+    share.combine()
     return stall

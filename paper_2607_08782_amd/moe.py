@@ -28,9 +28,10 @@ MOE_PERMUTE_NOALLOC_MAX_WS = 4 << 20
 
 EXPORTS = ("moe_status_string", "moe_route_topk", "moe_route_topk_ws_bytes",
            "moe_expert_histogram", "moe_permute_ws_bytes",
-           "moe_permute", "moe_permute_noalloc", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn", "moe_grouped_ffn_products", "moe_grouped_ffn_combine",
-           "moe_grouped_ffn_rows", "moe_grouped_ffn_rows_products",
-           "moe_combine",
+           "moe_permute", "moe_permute_noalloc", "moe_grouped_ffn_ws_bytes", "moe_grouped_ffn",
+           "moe_grouped_ffn_products", "moe_grouped_ffn_combine",
+           "moe_grouped_ffn_rows", "moe_grouped_ffn_rows_products", "moe_grouped_ffn_rows_shared",
+           "moe_combine", "moe_combine_shared",
            "moe_quantize_e4m3", "moe_route_topk_e4m3")
 
 _lib = None
@@ -78,8 +79,12 @@ def load_library(path: str = LIB_PATH):
     lib.moe_grouped_ffn_rows.restype = I
     lib.moe_grouped_ffn_rows_products.argtypes = [P, L, P, I, P, I, P, P, I, I, L, P, P, S, I, P]
     lib.moe_grouped_ffn_rows_products.restype = I
+    lib.moe_grouped_ffn_rows_shared.argtypes = [P, L, P, I, P, I, I, P, P, I, I, L, P, P, S, I, P]
+    lib.moe_grouped_ffn_rows_shared.restype = I
     lib.moe_combine.argtypes = [P, I, P, P, P, L, I, I, P, P]
     lib.moe_combine.restype = I
+    lib.moe_combine_shared.argtypes = [P, I, P, P, P, I, L, I, I, P, P]
+    lib.moe_combine_shared.restype = I
     lib.moe_quantize_e4m3.argtypes = [P, I, L, I, P, P, P]
     lib.moe_quantize_e4m3.restype = I
     lib.moe_route_topk_e4m3.argtypes = [P, P, P, P, P, L, I, I, I, I, P, P, P, P]
@@ -415,6 +420,40 @@ def moe_grouped_ffn_rows(x: torch.Tensor, row_token: torch.Tensor, group_offsets
     return y_perm
 
 
+def moe_grouped_ffn_rows_shared(x: torch.Tensor, row_token: torch.Tensor,
+                                group_offsets: torch.Tensor, weights: WeightTable, n_shared: int, *,
+                                cap_rows: int, y_perm: Optional[torch.Tensor] = None,
+                                ws: Optional[torch.Tensor] = None, stream=None,
+                                products: int = 3) -> torch.Tensor:
+    """moe_grouped_ffn_rows_products with n_shared leading groups of T rows each
+    (the shared experts, weights[0 .. n_shared-1]); the routed groups follow, their
+    rows counted from n_shared * T.  Returns y_perm [n_shared * T + cap_rows, d]."""
+    lib = load_library()
+    T = x.shape[0]
+    d, f = weights.d, weights.f
+    dtype = _dtype_code(x)
+    if x.dtype != weights.dtype or x.shape[1] != d:
+        raise ValueError("x must be [T, d] of the weights' dtype")
+    n_groups = len(weights) - n_shared
+    if n_shared < 0 or n_groups < 0 or group_offsets.numel() != n_groups + 1:
+        raise ValueError("group_offsets must hold n_groups + 1 entries for the routed groups")
+    rows = n_shared * T + cap_rows
+    if row_token.numel() < rows:
+        raise ValueError("row_token must hold n_shared * T + cap_rows entries")
+    if y_perm is None:
+        y_perm = _empty((max(rows, 1), d), x.dtype, x.device)
+    if ws is None:
+        ws = workspace(moe_grouped_ffn_ws_bytes(dtype, rows, d, f, len(weights)), x.device)
+    st = lib.moe_grouped_ffn_rows_shared(
+        _dev(x, "x"), T, _dev(row_token, "row_token", torch.int32), dtype,
+        _dev(group_offsets, "group_offsets", torch.int32), n_groups, n_shared,
+        ctypes.cast(weights.p13, ctypes.c_void_p), ctypes.cast(weights.p2, ctypes.c_void_p), d, f,
+        cap_rows, _dev(y_perm, "y_perm", x.dtype), _dev(ws, "ws"), ws.numel(), products,
+        _stream(stream))
+    _check("moe_grouped_ffn_rows_shared", st)
+    return y_perm
+
+
 def moe_combine(y_perm: torch.Tensor, token_row: torch.Tensor, topk_gate: torch.Tensor,
                 y_shared: Optional[torch.Tensor], *, T: int, d: int,
                 y: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
@@ -430,4 +469,25 @@ def moe_combine(y_perm: torch.Tensor, token_row: torch.Tensor, topk_gate: torch.
                          _dev(y_shared, "y_shared", y.dtype), T, d, k,
                          _dev(y, "y", y.dtype), _stream(stream))
     _check("moe_combine", st)
+    return y
+
+
+def moe_combine_shared(y_perm: torch.Tensor, token_row: torch.Tensor, topk_gate: torch.Tensor,
+                       y_shared: Optional[torch.Tensor], n_shared: int, *, T: int, d: int,
+                       y: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """moe_combine with the shared experts' output in n_shared [T, d] slices
+    (y_shared [n_shared, T, d], added in slice order).  Returns y [T, d]."""
+    lib = load_library()
+    k = token_row.shape[1] if token_row.dim() == 2 else 1
+    dtype = _dtype_code(y_perm)
+    if y is None:
+        y = _empty((T, d), y_perm.dtype, y_perm.device)
+    if y_shared is not None and n_shared > 0 and y_shared.numel() < n_shared * T * d:
+        raise ValueError("y_shared must hold n_shared slices of [T, d]")
+    st = lib.moe_combine_shared(_dev(y_perm, "y_perm", y.dtype), dtype,
+                                _dev(token_row, "token_row", torch.int32),
+                                _dev(topk_gate, "topk_gate", torch.float32),
+                                _dev(y_shared, "y_shared", y.dtype), n_shared, T, d, k,
+                                _dev(y, "y", y.dtype), _stream(stream))
+    _check("moe_combine_shared", st)
     return y

@@ -204,7 +204,8 @@ def check_ffn_and_combine(case: Case, idx, gate, pm, sample=None, seed: int = 0,
     for (a, c) in shared:
         ref_y += oracle.expert_ffn(xs, a, c)
     if shared:
-        close(np32(share.y_shared[torch.from_numpy(toks).cuda()]), ref_y, tol, "y_shared")
+        close(share.shared_output()[torch.from_numpy(toks).cuda()].cpu().numpy(), ref_y, tol,
+              "shared experts' output")
     local = oracle.local_slots(case.inp.placement, share.dev)
     slot = {e: s for s, e in enumerate(local)}
     for n, t in enumerate(toks):

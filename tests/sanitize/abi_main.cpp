@@ -96,10 +96,21 @@ int main() {
                                          16, F, W, 1 << 30, 3 | 4 | 8, nullptr), MOE_ERR_ARG);
     EXPECT(moe_grouped_ffn_rows_products(F, 64, nullptr, 1, (int32_t*)F, 2, wp, wp, 128, 64, 16,
                                          F, W, 1 << 30, 1, nullptr), MOE_ERR_ARG);
+    EXPECT(moe_grouped_ffn_rows_shared(F, 64, (int32_t*)F, 1, (int32_t*)F, 2, -1, wp, wp, 128,
+                                       64, 16, F, W, 1 << 30, 3, nullptr), MOE_ERR_ARG);
+    EXPECT(moe_grouped_ffn_rows_shared(F, 0, (int32_t*)F, 1, (int32_t*)F, 0, 1, wp, wp, 128, 64,
+                                       16, F, W, 1 << 30, 3, nullptr), MOE_ERR_ARG);
+    EXPECT(moe_grouped_ffn_rows_shared(F, 1 << 20, (int32_t*)F, 1, (int32_t*)F, 0, 2, wp, wp, 128,
+                                       64, (1LL << 31) - (1 << 20), F, W, 1 << 30, 3, nullptr),
+           MOE_ERR_ARG);
     // moe_combine
     EXPECT(moe_combine(nullptr, 1, (int32_t*)F, (float*)F, nullptr, 4, 64, 2, F, nullptr),
            MOE_ERR_ARG);
     EXPECT(moe_combine(F, 1, (int32_t*)F, (float*)F, nullptr, 4, 64, 0, F, nullptr), MOE_ERR_ARG);
+    EXPECT(moe_combine_shared(F, 1, (int32_t*)F, (float*)F, F, -1, 4, 64, 2, F, nullptr),
+           MOE_ERR_ARG);
+    EXPECT(moe_combine_shared(F, 1, (int32_t*)F, (float*)F, F, MOE_MAX_GROUPS + 1, 4, 64, 2, F,
+                              nullptr), MOE_ERR_ARG);
     // quantized predictor
     EXPECT(moe_quantize_e4m3(F, 2, 4, 64, (uint8_t*)F, (float*)F, nullptr), MOE_ERR_ARG);
     EXPECT(moe_route_topk_e4m3((uint8_t*)F, (float*)F, (uint8_t*)F, (float*)F, nullptr, 4, 96, 8,

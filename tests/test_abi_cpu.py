@@ -248,6 +248,42 @@ def test_grouped_ffn_rows_products_validation(lib):
     assert call(products=3 | 8, ws_bytes=10) == moe.MOE_ERR_SHAPE
 
 
+def test_grouped_ffn_rows_shared_validation(lib):
+    f = lib.moe_grouped_ffn_rows_shared
+    arr = (ctypes.c_void_p * 4)(0x1000, 0x2000, 0x3000, 0x4000)
+    P = ctypes.cast(arr, ctypes.c_void_p)
+
+    def call(T=64, n_groups=2, n_shared=2, products=3, rows=FAKE, x=FAKE, y=FAKE, d=128, cap=16,
+             offsets=FAKE, ws_bytes=1 << 30):
+        return f(x, T, rows, 1, offsets, n_groups, n_shared, P, P, d, 64, cap, y,
+                 ctypes.c_void_p(0x100000), ws_bytes, products, None)
+    assert call(n_shared=-1) == moe.MOE_ERR_ARG
+    assert call(n_groups=-1) == moe.MOE_ERR_ARG
+    assert call(n_groups=0, n_shared=0) == moe.MOE_ERR_ARG          # no group at all
+    assert call(n_groups=100, n_shared=29) == moe.MOE_ERR_ARG       # past MOE_MAX_GROUPS
+    assert call(T=0) == moe.MOE_ERR_ARG                             # shared rows need tokens
+    assert call(offsets=None) == moe.MOE_ERR_ARG
+    assert call(rows=None) == moe.MOE_ERR_ARG                       # the shared rows' map too
+    assert call(products=2, y=None) == moe.MOE_ERR_ARG
+    assert call(products=3 | 4 | 8) == moe.MOE_ERR_ARG
+    assert call(d=100) == moe.MOE_ERR_SHAPE
+    assert call(T=1 << 20, n_shared=2, cap=(1 << 31) - (1 << 20)) == moe.MOE_ERR_ARG   # rows past 2^31
+    # the workspace covers the shared rows as well: enough for the routed rows alone fails
+    routed_only = lib.moe_grouped_ffn_ws_bytes(1, 16, 128, 64, 4)
+    assert call(ws_bytes=routed_only) == moe.MOE_ERR_SHAPE
+    assert call(n_shared=0, ws_bytes=routed_only - 1) == moe.MOE_ERR_SHAPE
+
+
+def test_combine_shared_validation(lib):
+    f = lib.moe_combine_shared
+    assert f(FAKE, 1, FAKE, FAKE, FAKE, -1, 4, 64, 2, FAKE, None) == moe.MOE_ERR_ARG
+    assert f(FAKE, 1, FAKE, FAKE, FAKE, 129, 4, 64, 2, FAKE, None) == moe.MOE_ERR_ARG
+    assert f(FAKE, 1, FAKE, FAKE, ctypes.c_void_p(0x1008), 2, 4, 64, 2, FAKE, None) == \
+        moe.MOE_ERR_ARG                                             # slices not 16-byte aligned
+    assert f(None, 1, FAKE, FAKE, FAKE, 2, 4, 64, 2, FAKE, None) == moe.MOE_ERR_ARG
+    assert f(FAKE, 1, FAKE, FAKE, FAKE, 2, 4, 64, 0, FAKE, None) == moe.MOE_ERR_ARG
+
+
 def test_combine_validation(lib):
     f = lib.moe_combine
     assert f(FAKE, 1, FAKE, FAKE, None, 4, 64, 0, FAKE, None) == moe.MOE_ERR_ARG

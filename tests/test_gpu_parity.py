@@ -193,7 +193,9 @@ def test_drift_sequence_swaps_placement_without_reallocating():
     T = cfg.T("batch")
     base = Case(cfg, T, batch=0)
     share = base.share
-    ptr_before = share.perm["x_perm"].data_ptr()
+    bufs = lambda: [t.data_ptr() for t in (share.y_perm, share.perm["row_token"], share.ws_ffn,
+                                           share.y)]
+    ptr_before = bufs()
     for b in (0, 3, 4, 9, 15):
         say("[case] drift batch", b)
         inp = synth.make_layer(cfg, T, seed=0, device="cuda", batch=b)
@@ -207,7 +209,7 @@ def test_drift_sequence_swaps_placement_without_reallocating():
         check_ffn_and_combine(case, idx, gate, pm, sample="tiles", seed=b, max_tokens=128)
         idx, gate, pm = check_timed_path(case)
         check_ffn_and_combine(case, idx, gate, pm, sample="tiles", seed=b, max_tokens=128)
-    assert share.perm["x_perm"].data_ptr() == ptr_before
+    assert bufs() == ptr_before
 
 
 def _share(cfg, T, logits=None, placement=None, dev=0):
@@ -355,7 +357,7 @@ def _both_paths(cfg, T, logits=None, seed=1):
     for gather in (False, True):
         share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
                            shared=inp.shared, coact=cfg.coact, gather_in_ffn=gather,
-                           fuse_combine=False)
+                           fuse_combine=False, shared_in_ffn=False)
         share.run(logits_in=logits)
         torch.cuda.synchronize()
         N = int(share.perm["group_offsets"][-1])
@@ -432,7 +434,8 @@ def test_ffn_products_one_at_a_time_equal_the_whole_call(name, regime):
     say("[products]", name, regime, "T=%d" % T)
     inp = synth.make_layer(cfg, T, seed=2, device="cuda")
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
-                       shared=inp.shared, coact=cfg.coact, fuse_combine=False)
+                       shared=inp.shared, coact=cfg.coact, fuse_combine=False,
+                       shared_in_ffn=False)
     share.run()
     torch.cuda.synchronize()
     N = int(share.perm["group_offsets"][-1])
@@ -456,7 +459,8 @@ def test_rows_products_one_at_a_time_equal_the_whole_call(name, regime):
     say("[rows products]", name, regime, "T=%d" % T)
     inp = synth.make_layer(cfg, T, seed=7, device="cuda")
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
-                       shared=inp.shared, coact=cfg.coact, gather_in_ffn=True)
+                       shared=inp.shared, coact=cfg.coact, gather_in_ffn=True,
+                       shared_in_ffn=False)
     share.run()
     torch.cuda.synchronize()
     N = int(share.perm["group_offsets"][-1])
@@ -488,7 +492,8 @@ def test_small_groups_hint_leaves_the_outputs_bitwise_unchanged(name, regime):
     say("[small groups]", name, regime, "T=%d" % T)
     inp = synth.make_layer(cfg, T, seed=3, device="cuda")
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
-                       shared=inp.shared, coact=cfg.coact, fuse_combine=False)
+                       shared=inp.shared, coact=cfg.coact, fuse_combine=False,
+                       shared_in_ffn=False)
     assert share.ffn_products & moe.MOE_FFN_SMALL_GROUPS
     share.run()
     torch.cuda.synchronize()
@@ -517,7 +522,7 @@ def test_large_groups_hint_leaves_the_shared_call_bitwise_unchanged(name, regime
     say("[large groups]", name, regime, "T=%d" % T)
     inp = synth.make_layer(cfg, T, seed=4, device="cuda")
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
-                       shared=inp.shared, coact=cfg.coact)
+                       shared=inp.shared, coact=cfg.coact, shared_in_ffn=False)
     assert share.shared_products & moe.MOE_FFN_LARGE_GROUPS
     share.run()
     torch.cuda.synchronize()
@@ -541,7 +546,7 @@ def test_large_groups_hint_leaves_the_routed_call_bitwise_unchanged(name, regime
     say("[large groups, routed]", name, regime, "T=%d" % T)
     inp = synth.make_layer(cfg, T, seed=6, device="cuda")
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
-                       shared=inp.shared, coact=cfg.coact)
+                       shared=inp.shared, coact=cfg.coact, shared_in_ffn=False)
     assert share.ffn_products & moe.MOE_FFN_LARGE_GROUPS
     share.run()
     torch.cuda.synchronize()
@@ -641,7 +646,8 @@ def test_fused_ffn_combine_is_bitwise_the_ffn_then_the_combine(name, regime, cus
     say("[fused]", name, regime, "T=%d" % T)
     inp = synth.make_layer(cfg, T, seed=5, device="cuda")
     fused, plain = (LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
-                               shared=inp.shared, coact=cfg.coact, fuse_combine=fz)
+                               shared=inp.shared, coact=cfg.coact, fuse_combine=fz,
+                               shared_in_ffn=False)
                     for fz in (True, False))
     assert fused.fused_combine and not plain.fused_combine
     fused.y.fill_(7.0)
@@ -914,3 +920,139 @@ def test_combine_with_compacted_rows_is_exact_on_exact_values(k, d):
         torch.cuda.synchronize()
         ref = oracle.combine(y_perm, token_row, gate, ys, T, d, k)
         np.testing.assert_array_equal(np32(got[:T]), ref.astype(np.float32))
+
+
+# ---------------------------------------------------------------------------
+# shared experts as leading groups of the routed experts' call
+# ---------------------------------------------------------------------------
+def _rand_bf16(shape, gen, scale):
+    return (torch.randn(shape, generator=gen) * scale).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("dtype,sizes,n_shared,T,d,f,hint", [
+    ("bf16", [130, 0, 7, 300, 64, 65], 3, 200, 256, 128, 0),
+    ("bf16", [40, 1, 0, 256, 17], 2, 256, 128, 192, moe.MOE_FFN_SMALL_GROUPS),
+    ("bf16", [900, 5, 600], 1, 700, 128, 128, moe.MOE_FFN_LARGE_GROUPS),
+    ("bf16", [], 4, 300, 128, 64, 0),                       # no routed group at all
+    ("f32", [33, 0, 70], 2, 50, 72, 40, 0),
+])
+def test_rows_shared_call_every_row(dtype, sizes, n_shared, T, d, f, hint):
+    """moe_grouped_ffn_rows_shared: n_shared leading groups of T rows (every token
+    once, rows [s T, (s+1) T)), then the routed groups (rows counted from n_shared T,
+    read through row_token), in one call; every output row against the oracle's
+    expert FFN on the row's token and its group's weights (ragged and empty routed
+    groups, streamed and tiled sizes, both hints, fp32)."""
+    say("[rows shared]", dtype, sizes, "n_shared=%d T=%d d=%d f=%d hint=%d" % (n_shared, T, d, f, hint))
+    gen = torch.Generator().manual_seed(sum(sizes) + 31 * n_shared + T)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    n_groups, N = len(sizes), sum(sizes)
+    groups = n_shared + n_groups
+    x = (torch.randn((T, d), generator=gen)).to(tdt)
+    w13 = [(torch.randn((2 * f, d), generator=gen) * d ** -0.5).to(tdt) for _ in range(groups)]
+    w2 = [(torch.randn((d, f), generator=gen) * f ** -0.5).to(tdt) for _ in range(groups)]
+    cap = N + 3                                              # rows past the groups stay untouched
+    routed_tok = torch.randint(0, T, (cap,), generator=gen, dtype=torch.int32)
+    lead = n_shared * T
+    row_token = torch.cat([torch.arange(T, dtype=torch.int32).repeat(n_shared), routed_tok])
+    offsets = torch.tensor(np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32))
+    y = torch.full((lead + cap, d), 5.0, dtype=tdt).cuda()
+    wt = moe.WeightTable([w.cuda() for w in w13], [w.cuda() for w in w2])
+    moe.moe_grouped_ffn_rows_shared(x.cuda(), row_token.cuda(), offsets.cuda(), wt, n_shared,
+                                    cap_rows=cap, y_perm=y, products=3 | hint)
+    torch.cuda.synchronize()
+    got = np32(y)
+    xs = np32(x)
+    tol = OUT_TOL[dtype]
+    starts = [s * T for s in range(n_shared)] + [lead + int(o) for o in offsets[:-1]]
+    counts = [T] * n_shared + list(sizes)
+    tok = np32(row_token).astype(np.int64)
+    for g in range(groups):
+        a, n = starts[g], counts[g]
+        if n == 0:
+            continue
+        ref = oracle.expert_ffn(xs[tok[a:a + n]], np32(w13[g]), np32(w2[g]))
+        close(got[a:a + n], ref, tol, "group %d" % g)
+    assert np.all(got[lead + N:] == 5.0)
+
+
+@pytest.mark.parametrize("n_shared", [0, 1, 2, 3, 5])
+@pytest.mark.parametrize("k,d", [(2, 512), (8, 512), (6, 72)])
+def test_combine_shared_slices_exact(n_shared, k, d):
+    """moe_combine_shared: the routed sum, then n_shared slices in order; on values
+    exact in bf16 and fp32 the output equals the oracle's combine of the slices'
+    sum bit for bit, and n_shared = 1 is moe_combine bit for bit."""
+    say("[combine shared]", "n_shared=%d k=%d d=%d" % (n_shared, k, d))
+    rng = np.random.default_rng(n_shared * 100 + k * 10 + d)
+    T = 190
+    local = rng.integers(0, k + 1, size=T)
+    N = int(local.sum())
+    rows = rng.permutation(N)
+    token_row = np.full((T, k), -1, np.int32)
+    p = 0
+    for t in range(T):
+        for r in rng.choice(k, size=int(local[t]), replace=False):
+            token_row[t, r] = rows[p]
+            p += 1
+    gate = rng.choice(np.array([0.25, 0.5, 1.0], np.float32), size=(T, k)).astype(np.float32)
+    y_perm = rng.integers(-2, 3, size=(max(N, 1), d)).astype(np.float32)
+    sl = rng.integers(-2, 3, size=(max(n_shared, 1), T, d)).astype(np.float32)
+    dev = lambda a: torch.from_numpy(a).bfloat16().cuda()
+    got = moe.moe_combine_shared(dev(y_perm), torch.from_numpy(token_row).cuda(),
+                                 torch.from_numpy(gate).cuda(), dev(sl) if n_shared else None,
+                                 n_shared, T=T, d=d)
+    torch.cuda.synchronize()
+    ref = oracle.combine(y_perm, token_row, gate, sl[:n_shared].sum(0) if n_shared else None,
+                         T, d, k)
+    np.testing.assert_array_equal(np32(got[:T]), ref.astype(np.float32))
+    if n_shared == 1:
+        one = moe.moe_combine(dev(y_perm), torch.from_numpy(token_row).cuda(),
+                              torch.from_numpy(gate).cuda(), dev(sl[0]), T=T, d=d)
+        torch.cuda.synchronize()
+        assert torch.equal(one, got)
+
+
+@pytest.mark.parametrize("T", [300, 64, 1])
+def test_layer_share_with_shared_experts_in_the_routed_call(T):
+    """LayerShare(shared_in_ffn=True): the shared experts (widths 2f and f, cut into
+    three blocks of width f) run as leading groups of the routed call and the combine
+    adds their slices.  y matches the oracle's layer share on the same routing and
+    the two-stream share within the output tolerance, the blocks' summed output
+    matches the oracle's shared experts, and graph replays with new hidden states
+    give the eager run's bits."""
+    cfg = synth.custom_config(d=256, E=16, k=4, f=128, shared_f=(256, 128), G=2, replicas=1,
+                              zipf=1.1)
+    say("[shared in ffn]", "T=%d" % T)
+    inp = synth.make_layer(cfg, T, seed=9, device="cuda")
+    merged = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                        shared=inp.shared)
+    two = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                     shared=inp.shared, shared_in_ffn=False)
+    assert merged.shared_in_ffn and merged.n_shared_blocks == 3 and not two.shared_in_ffn
+    merged.run()
+    two.run()
+    torch.cuda.synchronize()
+    assert torch.equal(merged.topk_idx, two.topk_idx)
+    X, Wr, b = np32(inp.X), np32(inp.Wr), np32(inp.bias)
+    ref = oracle.layer_share(X, Wr, b, cfg.k, inp.placement, 0, [np32(w) for w in inp.w13],
+                             [np32(w) for w in inp.w2],
+                             shared=[(np32(a), np32(c)) for a, c in inp.shared],
+                             logits_f32=np32(merged.logits))
+    tol = OUT_TOL["bf16"]
+    np.testing.assert_array_equal(np32(merged.topk_idx), ref["idx"])
+    close(np32(merged.y[:T]), ref["y"], tol, "y (shared in the routed call)")
+    close(np32(merged.y[:T]), np32(two.y[:T]), tol, "y vs the two-stream share")
+    close(merged.shared_output().cpu().numpy(), ref["y_shared"], tol, "shared experts' output")
+    N = int(merged.perm["group_offsets"][-1])
+    close(np32(merged.y_perm[:N]), ref["y_perm"], tol, "routed rows")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        merged.run()
+    gen = torch.Generator(device="cuda").manual_seed(11)
+    for _ in range(3):
+        inp.X.copy_(torch.randn(inp.X.shape, device="cuda", generator=gen).to(inp.X.dtype))
+        g.replay()
+        torch.cuda.synchronize()
+        replayed = merged.y[:T].clone()
+        merged.run()
+        torch.cuda.synchronize()
+        assert torch.equal(replayed, merged.y[:T])
