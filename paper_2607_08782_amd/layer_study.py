@@ -94,8 +94,15 @@ def measure(name, regime, seed, steps):
     first_graphs = [_graph(s.run) for s in fshares]
 
     ffn_graphs = [_graph(s.routed_ffn) for s in shares]
+    # the two step variants interleaved (default, first-built, first-built, default),
+    # each the mean of its two runs: the first timed run of a shape runs a few %
+    # slower than later ones (clocks, first touches), which would favour whichever
+    # variant came second
+    _time(step_graphs, steps)
     step_us = _time(step_graphs, steps)
     first_us = _time(first_graphs, steps)
+    first_us = (first_us + _time(first_graphs, steps)) / 2
+    step_us = (step_us + _time(step_graphs, steps)) / 2
     ffn_us = _time(ffn_graphs, steps)
     flops = 6.0 * cfg.d * cfg.f * N
     # out: y_perm, or, when the call combines, y with the row maps and gates it reads
