@@ -126,6 +126,10 @@ def ffn_label(share):
     if share.fused_combine:
         return ("moe_grouped_ffn_combine call (weight-streaming launches, the combine in the "
                 "down product's chunk sum)")
+    if share.gather_in_ffn:
+        what = ("weight-streaming launches" if share.ffn_products & moe.MOE_FFN_SMALL_GROUPS
+                else "gate/up and down tiled GEMMs")
+        return ("moe_grouped_ffn_rows call: rows read through the row map (%s, chunk sums)" % what)
     if share.ffn_products & moe.MOE_FFN_SMALL_GROUPS:
         return "moe_grouped_ffn call (weight-streaming launches, chunk sums)"
     if share.ffn_products & moe.MOE_FFN_LARGE_GROUPS:

@@ -102,10 +102,15 @@ class LayerShare:
         # FFN reads its rows from X through row_token (moe_grouped_ffn_rows).  None:
         # for bf16 batches of at least 16384 token-expert assignments, where the row
         # copy it saves is large (measured faster at the DeepSeek-V2-Lite and Qwen3
-        # prefill shapes, even at Mixtral's, slower at Qwen1.5's 8192)
+        # prefill shapes, even at Mixtral's, slower at Qwen1.5's 8192), and for bf16
+        # batches of at most 256 tokens, where the copy is a launch of its own for
+        # little data (Qwen3-30B-A3B-shaped decode step 74.4 -> 71.3 us), unless
+        # the share fuses the combine into the FFN call, which reads the packaged rows
         packaged_asked = gather_in_ffn is False
         if gather_in_ffn is None:
-            gather_in_ffn = X.dtype == torch.bfloat16 and X.shape[0] * k >= 16384
+            fusable = fuse_combine is True or (fuse_combine is None and X.shape[0] <= 64 and k <= 2)
+            gather_in_ffn = X.dtype == torch.bfloat16 and (
+                X.shape[0] * k >= 16384 or (X.shape[0] <= 256 and not fusable))
         # shared_in_ffn: the shared experts as leading groups of the routed call (see
         # the module docstring), which reads its rows through row_token.  None: bf16
         # batches of at most SHARED_IN_FFN_MAX_T tokens whose shared experts' widths

@@ -435,7 +435,7 @@ def test_ffn_products_one_at_a_time_equal_the_whole_call(name, regime):
     inp = synth.make_layer(cfg, T, seed=2, device="cuda")
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
                        shared=inp.shared, coact=cfg.coact, fuse_combine=False,
-                       shared_in_ffn=False)
+                       shared_in_ffn=False, gather_in_ffn=False)
     share.run()
     torch.cuda.synchronize()
     N = int(share.perm["group_offsets"][-1])
@@ -493,7 +493,7 @@ def test_small_groups_hint_leaves_the_outputs_bitwise_unchanged(name, regime):
     inp = synth.make_layer(cfg, T, seed=3, device="cuda")
     share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
                        shared=inp.shared, coact=cfg.coact, fuse_combine=False,
-                       shared_in_ffn=False)
+                       shared_in_ffn=False, gather_in_ffn=False)
     assert share.ffn_products & moe.MOE_FFN_SMALL_GROUPS
     share.run()
     torch.cuda.synchronize()
