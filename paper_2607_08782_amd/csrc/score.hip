@@ -32,6 +32,7 @@ constexpr int SC_BM = 64;          // tokens per workgroup
 constexpr int SC_THREADS = 256;    // 4 waves
 constexpr int SC_BKB = 128;        // bytes of K per row per stage
 constexpr uint32_t SC_RSRC_WORD3 = 0x00020000;
+constexpr int SC_OOB = 0x7fffff00;  // an offset past every descriptor's range: the store is dropped
 
 // chunk position of 16-byte chunk c of LDS row r: c ^ sc_swz(r)
 __device__ __forceinline__ int sc_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
@@ -109,6 +110,18 @@ __global__ __launch_bounds__(SC_THREADS) void score_tiles_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
 
+    // the lane's column terms (bias; the FP8 router-row scales), loaded before the
+    // K loop: a load still pending at the stores made the compiler wait for every
+    // earlier store before each one, serialising the epilogue
+    float b_c[NTW], s_c[NTW];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+        const int col = wn * 32 * NTW + j * 32 + fr;
+        const int cc = col < E ? col : E - 1;
+        b_c[j] = (S == 1 && bias) ? bias[cc] : 0.0f;
+        s_c[j] = FP8 ? sw[cc] : 1.0f;
+    }
+
     auto compute = [&](int slot) {
         const char* st = lds + slot * STAGE;
         if constexpr (FP8) {
@@ -159,23 +172,29 @@ __global__ __launch_bounds__(SC_THREADS) void score_tiles_kernel(
     }
 
     // accumulator element r of a 32x32 tile: row 8 (r / 4) + 4 h + r % 4, column fr;
-    // S == 1: out[t][e] = score + bias[e];  S > 1: out[chunk][t][e] = partial score
-    float* o = out + (S > 1 ? (int64_t)chunk * T * E : 0);
+    // S == 1: out[t][e] = score + bias[e];  S > 1: out[chunk][t][e] = partial score.
+    // Branch-free stores through a descriptor over the block's rows: an element past
+    // the batch or past E gets an offset outside it and is dropped.
+    float* o = out + (S > 1 ? (int64_t)chunk * T * E : 0) + t0 * E;
+    const __amdgpu_buffer_rsrc_t orsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)o, (short)0, nt * E * 4, SC_RSRC_WORD3);
+    float sx_r[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int row = wm * 32 + (r >> 2) * 8 + 4 * h + (r & 3);
+        sx_r[r] = FP8 ? sx[t0 + (row < nt ? row : nt - 1)] : 1.0f;
+    }
 #pragma unroll
     for (int j = 0; j < NTW; ++j) {
         const int col = wn * 32 * NTW + j * 32 + fr;
-        if (col >= E) continue;
-        const float s_w = FP8 ? sw[col] : 1.0f;
-        const float b_e = (S == 1 && bias) ? bias[col] : 0.0f;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int row = wm * 32 + (r >> 2) * 8 + 4 * h + (r & 3);
-            if (row < nt) {
-                float v = acc[j][r];
-                if (FP8) v = v * sx[t0 + row] * s_w;
-                if (S == 1 && bias) v += b_e;
-                o[(t0 + row) * E + col] = v;
-            }
+            float v = acc[j][r];
+            if (FP8) v = v * sx_r[r] * s_c[j];
+            if (S == 1 && bias) v += b_c[j];
+            const int off = (row < nt && col < E) ? (row * E + col) * 4 : SC_OOB;
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), orsrc, off, 0, 0);
         }
     }
 }
