@@ -120,7 +120,7 @@ class LayerShare:
         blocks = shared_blocks(list(shared), f_routed) if shared and shared_in_ffn is not False else None
         if shared_in_ffn is None:
             shared_in_ffn = (blocks is not None and X.dtype == torch.bfloat16
-                             and X.shape[0] <= SHARED_IN_FFN_MAX_T and not packaged_asked)
+                             and 1 <= X.shape[0] <= SHARED_IN_FFN_MAX_T and not packaged_asked)
         if shared_in_ffn and blocks is None:
             raise ValueError("shared_in_ffn needs shared experts whose widths are multiples "
                              "of the routed experts' f")

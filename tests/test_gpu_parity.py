@@ -1056,3 +1056,16 @@ def test_layer_share_with_shared_experts_in_the_routed_call(T):
         merged.run()
         torch.cuda.synchronize()
         assert torch.equal(replayed, merged.y[:T])
+
+
+def test_empty_batch_with_shared_experts_takes_the_two_call_path():
+    """A batch of no tokens with shared experts whose widths suit the routed call:
+    the share keeps the shared experts' own call (their leading groups would hold
+    no rows) and a step runs without error."""
+    cfg = synth.custom_config(d=128, E=8, k=2, f=64, shared_f=(128,), G=2)
+    inp = synth.make_layer(cfg, 0, seed=1, device="cuda")
+    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, inp.placement, 0, inp.w13, inp.w2,
+                       shared=inp.shared)
+    assert not share.shared_in_ffn
+    share.run()
+    torch.cuda.synchronize()
