@@ -108,6 +108,12 @@ int score_tiles_split(int64_t T, int rowbytes, int E, bool allow_split);
 int launch_score_tiles(bool fp8, const void* x, const void* w, const float* sx, const float* sw,
                        const float* bias, int64_t T, int rowbytes, int E, int S, float* out,
                        hipStream_t s);
+// The bf16 tiled score kernel with one K chunk over 33-64 experts (MOE_ERR_SHAPE
+// otherwise), finishing with the top-k and gates of its tokens (logits nullable:
+// scores + bias stored there when given).
+int launch_score_tiles_topk(const void* x, const void* w, const float* bias, int64_t T,
+                            int rowbytes, int E, int k, int renorm, float* logits, int32_t* idx,
+                            float* gate, hipStream_t s);
 // Top-k and gates of given scores (route.hip): scores[T][E] read in place.
 int launch_topk_given(const float* scores, int64_t T, int E, int k, int flags, int32_t* idx,
                       float* gate, hipStream_t s);

@@ -334,9 +334,18 @@ int launch_kmv(const void* x, int dtype, const void* w, const float* bias, int64
         const size_t lds = (size_t)4 * rows * (E_pad + 1) * sizeof(float);
         const dim3 grid((unsigned)ceil_div(T, rows), (unsigned)S), block(RB_THREADS);
         float* part = (float*)ws;
+        if (St == 1 && E <= 64) {
+            // long batch over 33-64 experts: the tiled score kernel with its top-k in
+            // the same launch (scores + bias to `logits` when requested).  Wider E
+            // keeps the separate top-k launch: there the workgroup's own top-k (more
+            // lanes per token, more passes over its 64 tokens) cost more than the
+            // launch it saves (E = 128: 33.4 -> 34.6 us, E = 256: 35 -> 45 us per call;
+            // E = 64: 22.8 -> 21.5 us)
+            return launch_score_tiles_topk(x, w, bias, T, 2 * d, E, k, renorm, logits, idx, gate,
+                                           s);
+        }
         if (St > 0) {
-            // long batch over many experts: the tiled score kernel; with one K
-            // chunk its scores (bias added) go to `logits`, or to the workspace
+            // the tiled score kernel with its K split: partial scores to the workspace
             float* out = (St == 1 && logits) ? logits : part;
             const int st = launch_score_tiles(false, x, w, nullptr, nullptr, bias, T, 2 * d, E,
                                               St, out, s);

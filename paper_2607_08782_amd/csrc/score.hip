@@ -18,9 +18,11 @@
 //
 // With one K chunk the workgroup stores its scores (bias added); with S > 1
 // chunks it stores fp32 partial scores part[chunk][t][e], which the caller
-// sums in chunk order.  Top-k runs in a separate many-workgroup kernel: in the
-// epilogue of a workgroup it would leave the CU's memory pipes idle.
+// sums in chunk order.  The bf16 gate with one chunk can also finish with the
+// top-k of its own 64 tokens (KM > 0): the scores go through LDS to the same
+// top-k as for given scores, so no second launch reads them back.
 #include "common.h"
+#include "topk.h"
 
 namespace moe {
 namespace {
@@ -44,11 +46,14 @@ __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <bool FP8, int NTW, int R>
+// KM > 0 (S == 1): top-k (k <= KM, top-k class C) of the workgroup's tokens
+// into idx / gate after the scores; out (the scores) may then be null.
+template <bool FP8, int NTW, int R, int KM = 0, int C = 0>
 __global__ __launch_bounds__(SC_THREADS) void score_tiles_kernel(
     const uint8_t* __restrict__ x, const uint8_t* __restrict__ w, const float* __restrict__ sx,
     const float* __restrict__ sw, const float* __restrict__ bias, int64_t T, int rowbytes, int E,
-    int S, float* __restrict__ out) {
+    int S, float* __restrict__ out, int k = 0, int renorm = 0, int32_t* __restrict__ idx = nullptr,
+    float* __restrict__ gate = nullptr) {
     extern __shared__ __attribute__((aligned(1024))) char lds[];
     constexpr int A_BYTES = SC_BM * SC_BKB;           // 8 KB
     constexpr int NB = 64 * NTW;                      // router rows per tile
@@ -175,9 +180,14 @@ __global__ __launch_bounds__(SC_THREADS) void score_tiles_kernel(
     // S == 1: out[t][e] = score + bias[e];  S > 1: out[chunk][t][e] = partial score.
     // Branch-free stores through a descriptor over the block's rows: an element past
     // the batch or past E gets an offset outside it and is dropped.
-    float* o = out + (S > 1 ? (int64_t)chunk * T * E : 0) + t0 * E;
+    float* o = out ? out + (S > 1 ? (int64_t)chunk * T * E : 0) + t0 * E : nullptr;
     const __amdgpu_buffer_rsrc_t orsrc =
-        __builtin_amdgcn_make_buffer_rsrc((void*)o, (short)0, nt * E * 4, SC_RSRC_WORD3);
+        __builtin_amdgcn_make_buffer_rsrc((void*)o, (short)0, o ? nt * E * 4 : 0, SC_RSRC_WORD3);
+    // fused top-k: the scores also go to an LDS tile [64][E_pad + 1] over the
+    // ring, which every wave has finished reading once past this barrier
+    const int ldS = ((E + 15) & ~15) + 1;
+    float* const sc = (float*)lds;
+    if constexpr (KM > 0) asm volatile("s_barrier" ::: "memory");
     float sx_r[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -195,7 +205,13 @@ __global__ __launch_bounds__(SC_THREADS) void score_tiles_kernel(
             if (S == 1 && bias) v += b_c[j];
             const int off = (row < nt && col < E) ? (row * E + col) * 4 : SC_OOB;
             __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), orsrc, off, 0, 0);
+            if constexpr (KM > 0)
+                if (row < nt && col < E) sc[row * ldS + col] = v;
         }
+    }
+    if constexpr (KM > 0) {
+        __syncthreads();
+        topk_tokens<KM, C>(sc, ldS, nt, t0, E, k, renorm, idx, gate);
     }
 }
 
@@ -211,6 +227,33 @@ int launch_tiles(const uint8_t* x, const uint8_t* w, const float* sx, const floa
     hipLaunchKernelGGL((score_tiles_kernel<FP8, NTW, R>), grid, dim3(SC_THREADS), lds, s, x, w, sx,
                        sw, bias, T, rowbytes, E, S, out);
     return launch_status();
+}
+
+template <int NTW, int R, int KM, int C>
+int launch_tiles_topk(const uint8_t* x, const uint8_t* w, const float* bias, int64_t T,
+                      int rowbytes, int E, int k, int renorm, float* logits, int32_t* idx,
+                      float* gate, hipStream_t s) {
+    constexpr size_t ring = (size_t)R * (SC_BM * SC_BKB + 64 * NTW * SC_BKB);
+    constexpr size_t tile = (size_t)SC_BM * (64 * NTW + 1) * sizeof(float);
+    constexpr size_t lds = ring > tile ? ring : tile;
+    static_assert(lds <= 160 * 1024, "ring fits the LDS of a CU");
+    if (lds > 65536 &&
+        allow_dynamic_lds<score_tiles_kernel<false, NTW, R, KM, C>>(lds) != MOE_OK)
+        return MOE_ERR_DEVICE;
+    hipLaunchKernelGGL((score_tiles_kernel<false, NTW, R, KM, C>), dim3((unsigned)ceil_div(T, SC_BM)),
+                       dim3(SC_THREADS), lds, s, x, w, nullptr, nullptr, bias, T, rowbytes, E, 1,
+                       logits, k, renorm, idx, gate);
+    return launch_status();
+}
+
+template <int KM>
+int launch_topk_by_width(const uint8_t* x, const uint8_t* w, const float* bias, int64_t T,
+                         int rowbytes, int E, int k, int renorm, float* logits, int32_t* idx,
+                         float* gate, hipStream_t s) {
+    // 33-64 experts: one 64-wide tile, top-k class 2
+    if (E > 64) return MOE_ERR_SHAPE;
+    return launch_tiles_topk<1, 8, KM, 2>(x, w, bias, T, rowbytes, E, k, renorm, logits, idx,
+                                          gate, s);
 }
 
 }  // namespace
@@ -246,6 +289,20 @@ int launch_score_tiles(bool fp8, const void* x, const void* w, const float* sx, 
     }
     MOE_SC(false);
 #undef MOE_SC
+}
+
+int launch_score_tiles_topk(const void* x, const void* w, const float* bias, int64_t T,
+                            int rowbytes, int E, int k, int renorm, float* logits, int32_t* idx,
+                            float* gate, hipStream_t s) {
+    const uint8_t* xb = (const uint8_t*)x;
+    const uint8_t* wb = (const uint8_t*)w;
+#define MOE_ST(KM) \
+    launch_topk_by_width<KM>(xb, wb, bias, T, rowbytes, E, k, renorm, logits, idx, gate, s)
+    if (k <= 2) return MOE_ST(2);
+    if (k <= 4) return MOE_ST(4);
+    if (k <= 8) return MOE_ST(8);
+    return MOE_ST(MOE_MAX_K);
+#undef MOE_ST
 }
 
 }  // namespace moe
