@@ -13,8 +13,11 @@ graph replays of the gate/up product alone (moe_grouped_ffn_products), beside th
 whole FFN call.  The decode batch (T = 64) is reported beside it, and `shapes`
 holds every other configured layer (the tiny fp32 layer, DeepSeek-V2-Lite and
 Qwen3-30B-A3B prefill and decode, the 16-batch Qwen1.5-MoE drift sequence with
-its placement swaps).  `gather_in_ffn` reports the headline step with the row
-copy x_perm elided.  Prints ONE JSON line.
+its placement swaps), each as LayerShare sets itself up (at the Qwen1.5-MoE and
+DeepSeek-V2-Lite decode shapes the shared experts run inside the routed FFN
+call, whose rate then counts their work too; `ffn_call` names what each call
+launches).  `gather_in_ffn` reports the headline step with the row copy x_perm
+elided.  Prints ONE JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME:REGIME]
                     [--shapes all|none] [--no-cpu-baseline] [--no-gather-variant]
