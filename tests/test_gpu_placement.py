@@ -68,6 +68,7 @@ def _against_oracle(share, inp, cfg, P, what):
     local = [int(e) for e in np.nonzero(P[:, share.dev])[0]]
     ref = oracle.layer_share(np32(inp.X), np32(inp.Wr), np32(inp.bias), cfg.k, P, share.dev,
                              [np32(inp.w13[e]) for e in local], [np32(inp.w2[e]) for e in local],
+                             shared=[(np32(a), np32(c)) for a, c in inp.shared],
                              logits_f32=np32(share.logits))
     np.testing.assert_array_equal(share.topk_idx.cpu().numpy(), ref["idx"])
     np.testing.assert_array_equal(share.perm["token_row"].cpu().numpy(), ref["token_row"])
@@ -75,16 +76,18 @@ def _against_oracle(share, inp, cfg, P, what):
     close(np32(share.y), ref["y"], OUT_TOL["bf16"], what)
 
 
-def test_migration_in_ffn_windows_keeps_serving_then_switches_exactly():
+@pytest.mark.parametrize("shared_f", [(), (256,)])
+def test_migration_in_ffn_windows_keeps_serving_then_switches_exactly(shared_f):
     """Experts moving in are copied, chunk by chunk, into spare buffers inside the FFN
     windows of successive steps (Sec. V-B); every step during the migration gives the
     old placement's output bit for bit, and after the switch the layer gives bit for bit
     what a share built directly on the new placement gives.  The output before the
     migration and after the switch matches the oracle's layer on the old and the new
-    placement."""
+    placement.  With a shared expert of the routed width, the share runs it inside the
+    routed experts' call."""
     from paper_2607_08782_amd.migration import ExpertStore, Migrator, run_step
 
-    cfg = synth.custom_config(d=256, E=16, k=4, f=256, G=4, zipf=1.2)
+    cfg = synth.custom_config(d=256, E=16, k=4, f=256, G=4, zipf=1.2, shared_f=shared_f)
     T = 256
     inp = synth.make_layer(cfg, T, seed=2, device="cuda", experts="all")
     P0 = np.ascontiguousarray(inp.placement, dtype=np.uint8)
@@ -96,7 +99,8 @@ def test_migration_in_ffn_windows_keeps_serving_then_switches_exactly():
     store = ExpertStore(inp.w13, inp.w2)
     mig = Migrator(store, P0, 0, spare=2, chunk_bytes=32 << 10)
     w13, w2 = mig.weights()
-    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, P0, 0, w13, w2)
+    share = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, P0, 0, w13, w2, shared=inp.shared)
+    assert share.shared_in_ffn == bool(shared_f)
     share.run()
     torch.cuda.synchronize()
     y0 = share.y.clone()
@@ -117,7 +121,7 @@ def test_migration_in_ffn_windows_keeps_serving_then_switches_exactly():
     _against_oracle(share, inp, cfg, P1, "y after the switch")
     local1 = [int(e) for e in np.nonzero(P1[:, 0])[0]]
     fresh = LayerShare(inp.X, inp.Wr, inp.bias, cfg.k, P1, 0, [inp.w13[e] for e in local1],
-                       [inp.w2[e] for e in local1])
+                       [inp.w2[e] for e in local1], shared=inp.shared)
     fresh.run()
     torch.cuda.synchronize()
     assert torch.equal(share.y, fresh.y)
